@@ -1,0 +1,512 @@
+"""Pins of the CPU oracle to the paper and to mathematics, not to itself.
+
+Each test fixes a part of the oracle against something independent: a
+hand-worked example, brute force with exact arithmetic, a closed form, a
+library routine, or an invariant the method's definition implies (OmniCache
+§3.2.1-§3.2.3, §3.3).
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oc_oracle as O
+from oracle import brute as B
+from oc_synth import small_workload
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _w(wl):
+    return {k: wl.f64(getattr(wl, k)) for k in ("wq", "wk", "wv", "wo")}
+
+
+def _shape(wl):
+    return O.LayerShape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, wl.n_ctx)
+
+
+def _frac(s):
+    if s.startswith("sqrt1/2"):
+        return math.sqrt(0.5)
+    if "/" in s:
+        a, b = s.split("/")
+        return int(a) / int(b)
+    return float(s)
+
+
+# ----------------------------------------------------------------------------
+# hand-worked example (tests/golden/token_4x4_worked.json)
+# ----------------------------------------------------------------------------
+
+def test_golden_token_4x4_matching_selection_and_map():
+    g = json.load(open(os.path.join(GOLDEN, "token_4x4_worked.json")))
+    H, W, C = g["H"], g["W"], g["C"]
+    x = np.array(g["tokens"], dtype=np.float64).reshape(1, H * W, C)
+    shape = O.LayerShape(1, H, W, C, 1, 4)
+    for r, expect in g["cached"].items():
+        cfg = O.CacheCfg(O.TOKEN, r=float(r))
+        dec = O.decide(x, shape, cfg)
+        assert len(dec.groups) == 1
+        grp = dec.groups[0]
+        assert grp.dst == [0, 2, 8, 10]
+        assert grp.src == g["candidates"]
+        np.testing.assert_allclose(dec.node_max[0], [_frac(s) for s in g["node_max"]], rtol=0, atol=1e-15)
+        assert list(dec.node_idx[0]) == g["node_idx"]
+        assert O.selection_order(dec.node_max[0], grp.src) == g["selection_order"]
+        assert dec.cached[0] == expect, r
+    cfg = O.CacheCfg(O.TOKEN, r=0.5)
+    dec = O.decide(x, shape, cfg)
+    seqs = O.build_sequences(shape, cfg, dec)
+    kept, cached, rmap = O.kept_and_map(shape, cfg, dec, seqs, cache_valid=True)
+    assert list(kept) == g["r0.5"]["kept_idx"]
+    assert list(rmap) == g["r0.5"]["restore_map_valid_cache"]
+    kept, cached, rmap = O.kept_and_map(shape, cfg, dec, seqs, cache_valid=False)
+    assert list(rmap) == g["r0.5"]["restore_map_cold_matched"]
+
+
+def test_golden_block_variant_matches_token_example():
+    """Block descriptors concatenate a position over frames (§3.2.1).  With the
+    second frame all zeros, every block similarity equals the token example's
+    exactly, so the same decisions must come out for positions."""
+    g = json.load(open(os.path.join(GOLDEN, "token_4x4_worked.json")))
+    H, W, C = g["H"], g["W"], g["C"]
+    x = np.zeros((2, H * W, C))
+    x[0] = np.array(g["tokens"], dtype=np.float64)
+    shape = O.LayerShape(2, H, W, C, 1, 4)
+    cfg = O.CacheCfg(O.BLOCK, r=0.5)
+    dec = O.decide(x, shape, cfg)
+    assert dec.groups[0].src == g["candidates"]
+    assert list(dec.node_idx[0]) == g["node_idx"]
+    assert dec.cached[0] == g["cached"]["0.5"]
+    seqs = O.build_sequences(shape, cfg, dec)
+    assert [s[0] for s in seqs] == g["r0.5"]["kept_idx"]
+    assert all(s == [s[0], s[0] + H * W] for s in seqs)
+
+
+# ----------------------------------------------------------------------------
+# brute force on tiny inputs
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+@pytest.mark.parametrize("k", [1, 2])
+def test_brute_force_match_token(seed, k):
+    rng = np.random.default_rng(seed)
+    H = W = 4 if k == 1 else 8
+    C = 8
+    x = rng.standard_normal((1, H * W, C))
+    x[0, 5] = 0.0                                # a zero-norm candidate
+    x[0, 7] = x[0, 2] * 2.0                      # an exact duplicate direction
+    shape = O.LayerShape(1, H, W, C, 1, 4)
+    dec = O.decide(x, shape, O.CacheCfg(O.TOKEN, r=0.5, patch_k=k))
+    xf = x.reshape(-1, C)
+    for gi, g in enumerate(dec.groups):
+        desc = {i: list(xf[i]) for i in g.items}
+        bv, bi = B.brute_best_match(desc, g.src, g.dst)
+        np.testing.assert_allclose(dec.node_max[gi], [bv[s] for s in g.src], rtol=0, atol=1e-14)
+        assert list(dec.node_idx[gi]) == [bi[s] for s in g.src]
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_brute_force_match_block(seed):
+    rng = np.random.default_rng(seed)
+    F, H, W, C = 3, 4, 4, 5
+    x = rng.standard_normal((F, H * W, C))
+    shape = O.LayerShape(F, H, W, C, 1, 4)
+    dec = O.decide(x, shape, O.CacheCfg(O.BLOCK, r=0.5))
+    g = dec.groups[0]
+    desc = {n: [x[f, n, c] for f in range(F) for c in range(C)] for n in g.items}
+    bv, bi = B.brute_best_match(desc, g.src, g.dst)
+    np.testing.assert_allclose(dec.node_max[0], [bv[s] for s in g.src], rtol=0, atol=1e-14)
+    assert list(dec.node_idx[0]) == [bi[s] for s in g.src]
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_brute_force_selection_every_R(seed):
+    """Every R from 0 to 12 on a 4x4 grid, with deliberately tied similarity
+    values: the oracle's selection is the brute-force optimum."""
+    rng = np.random.default_rng(seed)
+    src = [1, 3, 4, 5, 6, 7, 9, 11, 12, 13, 14, 15]
+    vals = rng.choice([0.1, 0.5, 0.5, 0.9, 0.9, 0.9, 0.3], size=len(src))
+    nm = {s: float(v) for s, v in zip(src, vals)}
+    for R in range(0, 13):
+        assert O.select_cached([nm[s] for s in src], src, R) == B.brute_select(nm, R), R
+
+
+@pytest.mark.parametrize("ratio,n,nsrc,expect", [
+    (0.5, 16, 12, 8), (0.25, 16, 12, 4), (0.75, 16, 12, 12), (0.9, 16, 12, 12),
+    (0.0, 16, 12, 0), (0.5, 4096, 3072, 2048), (0.25, 4096, 3072, 1024),
+    (0.75, 4096, 3072, 3072), (0.25, 16, 8, 4), (0.2, 25, 12, 5), (0.6, 25, 12, 12),
+    (0.3, 10, 7, 3), (0.7, 10, 7, 7), (0.1, 30, 22, 3),
+])
+def test_skip_count_values(ratio, n, nsrc, expect):
+    """floor(r * n) clamped to the candidates; 0.3*10 and 0.7*10 are
+    2.9999999999999996 and 7.000000000000001 in binary, the guard keeps the
+    intended floor."""
+    assert O.skip_count(ratio, n, nsrc) == expect
+
+
+def test_pair_skip_count_values():
+    # one SVD-XT-like frame (72x128): n_f=9216 -> 9216 + 4608; cap 7/8 of 2*9216
+    assert O.pair_skip_count(0.5, 9216, 16128) == 13824
+    assert O.pair_skip_count(0.5, 576, 1008) == 864       # 18x32 patches
+    assert O.pair_skip_count(0.9, 16, 28) == 28           # clamped at 7/8
+    assert O.pair_skip_count(0.0, 16, 28) == 16           # the paired frame alone
+
+
+# ----------------------------------------------------------------------------
+# closed forms
+# ----------------------------------------------------------------------------
+
+def test_cosine_vs_torch_library():
+    rng = np.random.default_rng(5)
+    U = rng.standard_normal((7, 33))
+    V = rng.standard_normal((5, 33))
+    U[3] = 0.0
+    S = O.cosine_matrix(U, V)
+    T = torch.nn.functional.cosine_similarity(torch.tensor(U)[:, None, :], torch.tensor(V)[None, :, :], dim=-1,
+                                              eps=1e-300).numpy()
+    np.testing.assert_allclose(S, T, rtol=0, atol=1e-14)
+    assert np.all(S[3] == 0.0)
+    for i in range(7):
+        for j in range(5):
+            assert abs(O.cosine(U[i], V[j]) - S[i, j]) < 1e-14
+
+
+@pytest.mark.parametrize("scale", [0.5, 2.0])
+def test_duplicated_tokens_closed_form(scale):
+    """Candidates planted as positive multiples of distinct representatives
+    have similarity exactly 1 with them; with every other candidate below
+    0.9, those are exactly the R most redundant."""
+    rng = np.random.default_rng(11)
+    H = W = 8
+    C = 16
+    N = H * W
+    x = rng.standard_normal((1, N, C))
+    reps = [y * W + xx for y in range(0, H, 2) for xx in range(0, W, 2)]
+    cands = [i for i in range(N) if i not in reps]
+    # push every candidate away from every representative: orthogonalise
+    # against the representative span is not possible in C=16, so use a
+    # fresh random direction and check the bound explicitly
+    planted = {cands[3]: reps[0], cands[10]: reps[5], cands[20]: reps[9], cands[33]: reps[15]}
+    for c, r in planted.items():
+        x[0, c] = scale * x[0, r]
+    shape = O.LayerShape(1, H, W, C, 1, 4)
+    R = len(planted)
+    ratio = R / N
+    dec = O.decide(x, shape, O.CacheCfg(O.TOKEN, r=ratio))
+    g = dec.groups[0]
+    pos = {s: i for i, s in enumerate(g.src)}
+    others = [s for s in g.src if s not in planted]
+    assert max(dec.node_max[0][pos[s]] for s in others) < 0.9
+    for c, r in planted.items():
+        assert abs(dec.node_max[0][pos[c]] - 1.0) < 1e-14
+        assert dec.node_idx[0][pos[c]] == r
+    assert dec.cached[0] == sorted(planted)
+
+
+def test_planted_frames_closed_form():
+    """Odd frame 2m+1 = frame 2m + 0.01 (m+1) noise: frame 1 is the most
+    similar, then 3, 5, ...; each matches the frame it was copied from."""
+    wl = small_workload("frame", F=8, H=8, W=8, C=32, r_frame=0.25, planted=True, seed=3)
+    x = wl.f64(wl.steps[0])
+    shape = _shape(wl)
+    dec = O.decide(x, shape, O.CacheCfg(O.FRAME, r_frame=0.25))
+    g = dec.groups[0]
+    assert g.src == [1, 3, 5, 7] and g.dst == [0, 2, 4, 6] and g.R == 2
+    assert list(dec.node_idx[0]) == [0, 2, 4, 6]
+    assert list(np.argsort(-dec.node_max[0])) == [0, 1, 2, 3]
+    assert dec.cached[0] == [1, 3]
+
+
+def test_uniform_attention_closed_form():
+    """Wq = 0 makes every score 0, so every output row is the mean of the
+    values times the output projection."""
+    rng = np.random.default_rng(1)
+    L, C, heads, dh = 9, 12, 3, 4
+    X = rng.standard_normal((L, C))
+    wq = np.zeros((heads * dh, C))
+    wk, wv = rng.standard_normal((2, heads * dh, C))
+    wo = rng.standard_normal((C, heads * dh))
+    Y = O.multi_head_attention(X, wq, wk, wv, wo, heads, dh)
+    expect = (X @ wv.T).mean(axis=0) @ wo.T
+    np.testing.assert_allclose(Y, np.broadcast_to(expect, Y.shape), rtol=1e-12, atol=1e-12)
+
+
+def test_single_token_sequence_closed_form():
+    rng = np.random.default_rng(2)
+    C, heads, dh = 10, 2, 5
+    X = rng.standard_normal((1, C))
+    wq, wk, wv = rng.standard_normal((3, heads * dh, C))
+    wo = rng.standard_normal((C, heads * dh))
+    Y = O.multi_head_attention(X, wq, wk, wv, wo, heads, dh)
+    np.testing.assert_allclose(Y, X @ wv.T @ wo.T, rtol=1e-12, atol=1e-12)
+
+
+def test_mha_vs_torch_sdpa_fp64():
+    """Projections, head split, 1/sqrt(head_dim) scale, softmax and head
+    concatenation against torch's scaled_dot_product_attention in fp64."""
+    rng = np.random.default_rng(3)
+    L, C, heads, dh = 37, 24, 3, 8
+    X = rng.standard_normal((L, C))
+    wq, wk, wv = rng.standard_normal((3, heads * dh, C)) * 0.3
+    wo = rng.standard_normal((C, heads * dh)) * 0.3
+    Y = O.multi_head_attention(X, wq, wk, wv, wo, heads, dh)
+    Xt = torch.tensor(X)
+    q = torch.nn.functional.linear(Xt, torch.tensor(wq)).view(L, heads, dh).transpose(0, 1)
+    k = torch.nn.functional.linear(Xt, torch.tensor(wk)).view(L, heads, dh).transpose(0, 1)
+    v = torch.nn.functional.linear(Xt, torch.tensor(wv)).view(L, heads, dh).transpose(0, 1)
+    o = torch.nn.functional.scaled_dot_product_attention(q[None], k[None], v[None])[0]
+    T = torch.nn.functional.linear(o.transpose(0, 1).reshape(L, heads * dh), torch.tensor(wo)).numpy()
+    np.testing.assert_allclose(Y, T, rtol=1e-11, atol=1e-11)
+
+
+def test_attention_permutation_equivariance():
+    rng = np.random.default_rng(4)
+    L, C, heads, dh = 11, 8, 2, 4
+    X = rng.standard_normal((L, C))
+    wq, wk, wv = rng.standard_normal((3, heads * dh, C))
+    wo = rng.standard_normal((C, heads * dh))
+    perm = rng.permutation(L)
+    Y = O.multi_head_attention(X, wq, wk, wv, wo, heads, dh)
+    Yp = O.multi_head_attention(X[perm], wq, wk, wv, wo, heads, dh)
+    np.testing.assert_allclose(Yp, Y[perm], rtol=1e-12, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# whole-step properties
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("gran", [O.TOKEN, O.FRAME, O.BLOCK, O.FRAME_TOKEN])
+def test_r0_equals_full_attention(gran):
+    """With every ratio 0 nothing is cached and the layer is plain attention
+    (checked against torch's SDPA through ``full_attention``'s definition)."""
+    wl = small_workload(gran, F=4 if gran != O.TOKEN else 1, H=4, W=4, C=16, heads=2, head_dim=8, seed=9)
+    shape = _shape(wl)
+    w = _w(wl)
+    x = wl.f64(wl.steps[0])
+    cfg = O.CacheCfg(gran, r=0.0, r_frame=0.0)
+    res = O.layer_step(x, None, w, shape, cfg, None, cache_valid=False)
+    assert len(res.cached_idx) == 0
+    temporal = gran == O.BLOCK
+    yf, _ = O.full_attention(x, None, w, shape, temporal=temporal)
+    np.testing.assert_array_equal(res.y, yf)
+    # and full attention itself against torch
+    xs = torch.tensor(x)
+    seqs = xs.transpose(0, 1) if temporal else xs
+    q = torch.nn.functional.linear(seqs, torch.tensor(w["wq"]))
+    k = torch.nn.functional.linear(seqs, torch.tensor(w["wk"]))
+    v = torch.nn.functional.linear(seqs, torch.tensor(w["wv"]))
+    S, L = q.shape[0], q.shape[1]
+    sp = lambda t: t.view(S, L, shape.heads, shape.head_dim).transpose(1, 2)
+    o = torch.nn.functional.scaled_dot_product_attention(sp(q), sp(k), sp(v))
+    y = torch.nn.functional.linear(o.transpose(1, 2).reshape(S, L, -1), torch.tensor(w["wo"]))
+    y = y.transpose(0, 1) if temporal else y
+    np.testing.assert_allclose(yf, y.numpy(), rtol=1e-11, atol=1e-11)
+
+
+def test_text_context_appended_and_never_cached():
+    wl = small_workload(O.TOKEN, F=1, H=4, W=4, C=16, heads=2, head_dim=8, n_ctx=5, seed=12)
+    shape = _shape(wl)
+    w = _w(wl)
+    x = wl.f64(wl.steps[0])
+    ctx = wl.f64(wl.ctx)
+    res = O.layer_step(x, ctx, w, shape, O.CacheCfg(O.TOKEN, r=0.5), None, cache_valid=False)
+    X = np.concatenate([x[0][res.kept_idx], ctx], axis=0)
+    Y = O.multi_head_attention(X, w["wq"], w["wk"], w["wv"], w["wo"], 2, 8)
+    np.testing.assert_allclose(res.y_kept, Y[:len(res.kept_idx)], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(res.y_ctx, Y[len(res.kept_idx):], rtol=1e-12, atol=1e-12)
+    # r=0 with context equals full attention with context
+    r0 = O.layer_step(x, ctx, w, shape, O.CacheCfg(O.TOKEN, r=0.0), None, cache_valid=False)
+    yf, yc = O.full_attention(x, ctx, w, shape)
+    np.testing.assert_array_equal(r0.y, yf)
+    np.testing.assert_array_equal(r0.y_ctx, yc)
+
+
+def test_window_permutation_consistency():
+    """Moving whole 2x2 windows to other window slots keeps representatives
+    representatives, so similarities, matches and selection move with them
+    (no ties in this input)."""
+    rng = np.random.default_rng(21)
+    H = W = 8
+    C = 6
+    x = rng.standard_normal((1, H * W, C))
+    nwin = (H // 2) * (W // 2)
+    perm = rng.permutation(nwin)     # new window slot -> old window slot
+
+    def tok(win, dy, dx):
+        wy, wx = divmod(win, W // 2)
+        return (2 * wy + dy) * W + 2 * wx + dx
+
+    newid = {}
+    xp = np.empty_like(x)
+    for new in range(nwin):
+        old = perm[new]
+        for dy in (0, 1):
+            for dx in (0, 1):
+                xp[0, tok(new, dy, dx)] = x[0, tok(old, dy, dx)]
+                newid[tok(old, dy, dx)] = tok(new, dy, dx)
+    shape = O.LayerShape(1, H, W, C, 1, 2)
+    cfg = O.CacheCfg(O.TOKEN, r=0.4)
+    d0 = O.decide(x, shape, cfg)
+    d1 = O.decide(xp, shape, cfg)
+    m0 = {s: (v, i) for s, v, i in zip(d0.groups[0].src, d0.node_max[0], d0.node_idx[0])}
+    m1 = {s: (v, i) for s, v, i in zip(d1.groups[0].src, d1.node_max[0], d1.node_idx[0])}
+    vals = sorted(v for v, _ in m0.values())
+    assert min(np.diff(vals)) > 1e-9
+    for s, (v, i) in m0.items():
+        v1, i1 = m1[newid[s]]
+        assert abs(v - v1) < 1e-13 and i1 == newid[i]
+    assert sorted(newid[c] for c in d0.cached[0]) == d1.cached[0]
+
+
+def test_odd_frame_permutation_consistency():
+    """Permuting odd frames among themselves permutes frame decisions."""
+    wl = small_workload(O.FRAME, F=8, H=4, W=4, C=8, seed=17, frame_drift=0.3)
+    x = wl.f64(wl.steps[0])
+    shape = _shape(wl)
+    perm = {1: 5, 3: 1, 5: 7, 7: 3}
+    xp = x.copy()
+    for a, b in perm.items():
+        xp[b] = x[a]
+    cfg = O.CacheCfg(O.FRAME, r_frame=0.25)
+    d0 = O.decide(x, shape, cfg)
+    d1 = O.decide(xp, shape, cfg)
+    m0 = dict(zip(d0.groups[0].src, zip(d0.node_max[0], d0.node_idx[0])))
+    m1 = dict(zip(d1.groups[0].src, zip(d1.node_max[0], d1.node_idx[0])))
+    for a, b in perm.items():
+        assert m0[a][0] == pytest.approx(m1[b][0], abs=1e-14) and m0[a][1] == m1[b][1]
+    assert sorted(perm[c] for c in d0.cached[0]) == d1.cached[0]
+
+
+@pytest.mark.parametrize("gran,F,k", [(O.TOKEN, 2, 1), (O.TOKEN, 1, 2), (O.BLOCK, 3, 1), (O.BLOCK, 3, 2),
+                                      (O.FRAME, 6, 1), (O.FRAME_TOKEN, 7, 1), (O.FRAME_TOKEN, 6, 2)])
+def test_counts_and_partition(gran, F, k):
+    wl = small_workload(gran, F=F, H=8, W=8, C=8, heads=1, head_dim=8, seed=31, r=0.5, r_frame=0.35)
+    shape = _shape(wl)
+    x = wl.f64(wl.steps[0])
+    cfg = O.CacheCfg(gran, r=0.5, r_frame=0.35, patch_k=k)
+    dec = O.decide(x, shape, cfg)
+    for g, c in zip(dec.groups, dec.cached):
+        assert len(c) == g.R
+        assert set(c) <= set(g.src)
+        assert set(g.src).isdisjoint(g.dst)
+        assert sorted(g.src + g.dst) == sorted(g.items)
+    seqs = O.build_sequences(shape, cfg, dec)
+    assert len({len(s) for s in seqs}) == 1
+    kept, cached, rmap = O.kept_and_map(shape, cfg, dec, seqs, cache_valid=True)
+    FN = shape.F * shape.N
+    assert len(set(kept)) == len(kept)
+    assert sorted(list(kept) + list(cached)) == list(range(FN))
+    assert list(cached) == sorted(cached)
+    assert all(rmap[p] == -1 for p in cached)
+    assert all(rmap[p] == i for i, p in enumerate(kept))
+    # representatives are always retained
+    reps = set()
+    for g in dec.groups:
+        if g.kind == "token":
+            reps.update(g.dst)
+        elif g.kind == "block":
+            reps.update(f * shape.N + n for n in g.dst for f in range(shape.F))
+        else:
+            reps.update(f * shape.N + n for f in g.dst for n in range(shape.N))
+    assert reps <= set(kept)
+    # sequences ordered by smallest covered item, ascending inside
+    if gran != O.BLOCK:
+        assert all(s == sorted(s) for s in seqs)
+    # cold map points every cached position to a retained row
+    _, _, cmap = O.kept_and_map(shape, cfg, dec, seqs, cache_valid=False)
+    assert np.all(cmap >= 0) and np.all(cmap < len(kept))
+
+
+def test_frame_token_pairing_invariants_and_independent_greedy():
+    for seed in range(6):
+        wl = small_workload(O.FRAME_TOKEN, F=9, H=4, W=4, C=8, seed=40 + seed, frame_drift=0.2)
+        shape = _shape(wl)
+        x = wl.f64(wl.steps[0])
+        cfg = O.CacheCfg(O.FRAME_TOKEN, r=0.5, r_frame=0.45)
+        dec = O.decide(x, shape, cfg)
+        fg = dec.frame_group
+        assert fg.R == 4 and len(dec.pairs) == 4
+        ss = [s for s, _ in dec.pairs]
+        ds = [d for _, d in dec.pairs]
+        assert ss == dec.frame_cached_order
+        assert len(set(ds)) == len(ds) and all(d % 2 == 0 for d in ds) and all(s % 2 == 1 for s in ss)
+        sim = {(s, d): float(dec.frame_sim[i, j]) for i, s in enumerate(fg.src) for j, d in enumerate(fg.dst)}
+        assert dec.pairs == B.brute_pairs(dec.frame_cached_order, sim, fg.dst)
+        # frame similarities against brute force
+        xf = x.reshape(shape.F, -1)
+        for (s, d), v in sim.items():
+            assert abs(v - B.cos_exact_order(list(xf[s]), list(xf[d]))) < 1e-13
+        # attention units: pairs and unmatched frames
+        seqs = O.build_sequences(shape, cfg, dec)
+        assert len(seqs) == shape.F - 4
+        # every pair group keeps the rep frame's top-left tokens
+        N = shape.N
+        for g in dec.groups:
+            frames = {i // N for i in g.items}
+            if len(frames) == 2:
+                assert len(g.src) == 7 * len(g.items) // 8
+                assert g.R == min(len(g.items) // 2 + (len(g.items) // 2) // 2, len(g.src))
+
+
+def test_restore_identities():
+    rng = np.random.default_rng(8)
+    FN, C = 12, 5
+    yk = rng.standard_normal((FN, C))
+    cache = rng.standard_normal((FN, C))
+    np.testing.assert_array_equal(O.restore(yk, np.full(FN, -1), cache), cache)
+    np.testing.assert_array_equal(O.restore(yk, np.arange(FN), None), yk)
+    m = np.array([3, -1, 0, -1, 1, 2, -1, 4, 5, -1, 6, 7])
+    y = O.restore(yk, m, cache)
+    for p in range(FN):
+        np.testing.assert_array_equal(y[p], yk[m[p]] if m[p] >= 0 else cache[p])
+
+
+def test_cold_matched_rows_equal_their_representative():
+    wl = small_workload(O.TOKEN, F=1, H=8, W=8, C=16, heads=2, head_dim=8, seed=13)
+    shape = _shape(wl)
+    w = _w(wl)
+    x = wl.f64(wl.steps[0])
+    cfg = O.CacheCfg(O.TOKEN, r=0.5)
+    res = O.layer_step(x, None, w, shape, cfg, None, cache_valid=False)
+    mt = O.matched_token(shape, cfg, res.decisions)
+    y = res.y.reshape(-1, shape.C)
+    for p in res.cached_idx:
+        np.testing.assert_array_equal(y[p], y[mt[int(p)]])
+
+
+def test_cache_chain_full_cold_then_reuse():
+    """Two steps with identical input, "full" cold policy: step 0 computes
+    everything; at step 1 every cached position carries step 0's output."""
+    wl = small_workload(O.TOKEN, F=2, H=4, W=4, C=16, heads=2, head_dim=8, seed=14)
+    shape = _shape(wl)
+    w = _w(wl)
+    x = wl.f64(wl.steps[0])
+    cfg = O.CacheCfg(O.TOKEN, r=0.5, cold=O.COLD_FULL)
+    s0 = O.layer_step(x, None, w, shape, cfg, None, cache_valid=False)
+    assert len(s0.cached_idx) == 0
+    yf, _ = O.full_attention(x, None, w, shape)
+    np.testing.assert_array_equal(s0.y, yf)
+    s1 = O.layer_step(x, None, w, shape, cfg, s0.y, cache_valid=True)
+    assert len(s1.cached_idx) > 0
+    y0 = s0.y.reshape(-1, shape.C)
+    y1 = s1.y.reshape(-1, shape.C)
+    for p in s1.cached_idx:
+        np.testing.assert_array_equal(y1[p], y0[p])
+
+
+def test_forced_decisions_only_change_what_they_override():
+    wl = small_workload(O.TOKEN, F=1, H=8, W=8, C=16, heads=2, head_dim=8, seed=15)
+    shape = _shape(wl)
+    w = _w(wl)
+    x = wl.f64(wl.steps[0])
+    cfg = O.CacheCfg(O.TOKEN, r=0.5)
+    a = O.layer_step(x, None, w, shape, cfg, None, cache_valid=False)
+    forced = {"cached": set(int(c) for c in a.cached_idx)}
+    b = O.layer_step(x, None, w, shape, cfg, None, cache_valid=False, forced=forced)
+    np.testing.assert_array_equal(a.y, b.y)
+    np.testing.assert_array_equal(a.restore_map, b.restore_map)
