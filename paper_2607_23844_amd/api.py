@@ -1,0 +1,308 @@
+"""Python entry points with the same names as the C ABI (include/oc.h).
+
+Argument marshalling only: torch supplies device memory and the current
+stream; every step runs in the HIP library.  Tensors must be contiguous,
+on the same GPU, bf16 or fp32 as the shape says; int tensors are int32.
+"""
+from __future__ import annotations
+
+import ctypes as C
+from dataclasses import dataclass
+from typing import Dict, Optional, Tuple
+
+import torch
+
+from . import _lib as L
+
+
+@dataclass(frozen=True)
+class Shape:
+    """Token tensor [F, N=H*W, C] of one attention layer plus its heads."""
+    F: int
+    H: int
+    W: int
+    C: int
+    heads: int
+    head_dim: int
+    n_ctx: int = 0
+    dtype: str = "bf16"      # "bf16" or "f32"
+
+    @property
+    def N(self) -> int:
+        return self.H * self.W
+
+    @property
+    def torch_dtype(self) -> torch.dtype:
+        return torch.bfloat16 if self.dtype == "bf16" else torch.float32
+
+    def c(self) -> L.oc_shape:
+        return L.oc_shape(self.F, self.H, self.W, self.C, self.heads, self.head_dim, self.n_ctx,
+                          L.OC_BF16 if self.dtype == "bf16" else L.OC_F32)
+
+
+@dataclass(frozen=True)
+class Cfg:
+    gran: str = "token"      # token | frame | block | frame_token
+    r: float = 0.0
+    r_frame: float = 0.0
+    patch_k: int = 1
+    cold: str = "matched"    # matched | full
+
+    def c(self) -> L.oc_cfg:
+        return L.oc_cfg(L.GRANS[self.gran], self.patch_k, self.r, self.r_frame, L.COLDS[self.cold], 0)
+
+
+@dataclass
+class PlanInfo:
+    n_groups: int
+    n_src_max: int
+    n_dst_max: int
+    n_frame_src: int
+    n_frame_dst: int
+    n_frame_cached: int
+    n_kept: int
+    n_cached: int
+    n_seq: int
+    seq_len: int
+    workspace_bytes: int
+
+
+class LayerCache:
+    """The layer cache of one attention layer: a device buffer [F, N, C] that
+    is also the layer output, plus the host-side valid flag and step count."""
+
+    def __init__(self, shape: Shape, device, y: Optional[torch.Tensor] = None):
+        self.shape = shape
+        self.y = y if y is not None else torch.empty((shape.F, shape.N, shape.C), dtype=shape.torch_dtype,
+                                                     device=device)
+        self.valid = 0
+        self.step = 0
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(t: torch.Tensor) -> int:
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _need(t: torch.Tensor, dtype: torch.dtype, name: str) -> None:
+    if not t.is_cuda:
+        raise L.OmniCacheError(L.OC_ERR_INVALID_ARG, f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise L.OmniCacheError(L.OC_ERR_DTYPE, f"{name} has dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise L.OmniCacheError(L.OC_ERR_INVALID_ARG, f"{name} must be contiguous")
+
+
+def _weights(w: Dict[str, torch.Tensor], shape: Shape) -> L.oc_attn_weights:
+    hd = shape.heads * shape.head_dim
+    for k, s in (("wq", (hd, shape.C)), ("wk", (hd, shape.C)), ("wv", (hd, shape.C)), ("wo", (shape.C, hd))):
+        _need(w[k], shape.torch_dtype, k)
+        if tuple(w[k].shape) != s:
+            raise L.OmniCacheError(L.OC_ERR_SHAPE, f"{k} has shape {tuple(w[k].shape)}, expected {s}")
+    return L.oc_attn_weights(w["wq"].data_ptr(), w["wk"].data_ptr(), w["wv"].data_ptr(), w["wo"].data_ptr())
+
+
+def plan(shape: Shape, cfg: Cfg) -> PlanInfo:
+    info = L.oc_plan_info()
+    sh, cf = shape.c(), cfg.c()
+    L.check(L.lib().oc_plan(C.byref(sh), C.byref(cf), C.byref(info)))
+    return PlanInfo(*(getattr(info, f) for f, _ in L.oc_plan_info._fields_))
+
+
+def workspace(shape: Shape, cfg: Cfg, device) -> torch.Tensor:
+    return torch.empty(max(plan(shape, cfg).workspace_bytes, 256), dtype=torch.uint8, device=device)
+
+
+def match(x: torch.Tensor, shape: Shape, cfg: Cfg, ws: torch.Tensor, frames: bool = False):
+    """(node_max [G, S] f32, node_idx [G, S] i32[, frame info dict])"""
+    _need(x, shape.torch_dtype, "x")
+    pl = plan(shape, cfg)
+    dev = x.device
+    nm = torch.empty((pl.n_groups, pl.n_src_max), dtype=torch.float32, device=dev)
+    ni = torch.empty((pl.n_groups, pl.n_src_max), dtype=torch.int32, device=dev)
+    fi = None
+    out = {}
+    if frames:
+        out = dict(frame_max=torch.empty(max(pl.n_frame_src, 1), dtype=torch.float32, device=dev),
+                   frame_idx=torch.empty(max(pl.n_frame_src, 1), dtype=torch.int32, device=dev),
+                   pairs=torch.empty((max(pl.n_frame_cached, 1), 2), dtype=torch.int32, device=dev))
+        fi = L.oc_frame_info(out["frame_max"].data_ptr(), out["frame_idx"].data_ptr(), out["pairs"].data_ptr())
+    sh, cf = shape.c(), cfg.c()
+    L.check(L.lib().oc_match(C.byref(sh), C.byref(cf), x.data_ptr(), nm.data_ptr(), ni.data_ptr(),
+                             C.byref(fi) if fi is not None else None, ws.data_ptr(), ws.numel(), _stream(x)))
+    if frames:
+        out["frame_max"] = out["frame_max"][:pl.n_frame_src]
+        out["frame_idx"] = out["frame_idx"][:pl.n_frame_src]
+        out["pairs"] = out["pairs"][:pl.n_frame_cached]
+        return nm, ni, out
+    return nm, ni
+
+
+def select(node_max: torch.Tensor, node_idx: torch.Tensor, shape: Shape, cfg: Cfg, ws: torch.Tensor,
+           map_matched: bool = False) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """(kept_idx [n_kept], cached_idx [n_cached], restore_map [F*N]), int32"""
+    _need(node_max, torch.float32, "node_max")
+    _need(node_idx, torch.int32, "node_idx")
+    pl = plan(shape, cfg)
+    dev = node_max.device
+    kept = torch.empty(max(pl.n_kept, 1), dtype=torch.int32, device=dev)
+    cached = torch.empty(max(pl.n_cached, 1), dtype=torch.int32, device=dev)
+    rmap = torch.empty(shape.F * shape.N, dtype=torch.int32, device=dev)
+    sh, cf = shape.c(), cfg.c()
+    L.check(L.lib().oc_select(C.byref(sh), C.byref(cf), node_max.data_ptr(), node_idx.data_ptr(), kept.data_ptr(),
+                              cached.data_ptr(), rmap.data_ptr(), 1 if map_matched else 0, ws.data_ptr(),
+                              ws.numel(), _stream(node_max)))
+    return kept[:pl.n_kept], cached[:pl.n_cached], rmap
+
+
+def gather(x: torch.Tensor, kept_idx: torch.Tensor, shape: Shape, cfg: Cfg) -> torch.Tensor:
+    _need(x, shape.torch_dtype, "x")
+    _need(kept_idx, torch.int32, "kept_idx")
+    pl = plan(shape, cfg)
+    out = torch.empty((max(pl.n_seq, 1), max(pl.seq_len, 1), shape.C), dtype=x.dtype, device=x.device)
+    sh, cf = shape.c(), cfg.c()
+    L.check(L.lib().oc_gather(C.byref(sh), C.byref(cf), x.data_ptr(), kept_idx.data_ptr(), out.data_ptr(),
+                              _stream(x)))
+    return out[:pl.n_seq, :pl.seq_len]
+
+
+def attn_workspace_bytes(shape: Shape, n_seq: int, seq_len: int) -> int:
+    sh = shape.c()
+    return int(L.lib().oc_attn_workspace_bytes(C.byref(sh), n_seq, seq_len))
+
+
+def attn_reduced(x_kept: torch.Tensor, n_seq: int, seq_len: int, weights: Dict[str, torch.Tensor], shape: Shape,
+                 ctx: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
+    """(y_kept [n_seq*seq_len, C], y_ctx [n_ctx, C] or None)"""
+    _need(x_kept, shape.torch_dtype, "x_kept")
+    w = _weights(weights, shape)
+    dev = x_kept.device
+    y = torch.empty((max(n_seq * seq_len, 1), shape.C), dtype=x_kept.dtype, device=dev)
+    y_ctx = None
+    if shape.n_ctx > 0:
+        _need(ctx, shape.torch_dtype, "ctx")
+        y_ctx = torch.empty((shape.n_ctx, shape.C), dtype=x_kept.dtype, device=dev)
+    need = attn_workspace_bytes(shape, n_seq, seq_len)
+    if ws is None:
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    sh = shape.c()
+    L.check(L.lib().oc_attn_reduced(C.byref(sh), x_kept.data_ptr(), n_seq, seq_len, _ptr(ctx), C.byref(w),
+                                    y.data_ptr(), _ptr(y_ctx), ws.data_ptr(), ws.numel(), _stream(x_kept)))
+    return y[:n_seq * seq_len], y_ctx
+
+
+def restore(y_kept: torch.Tensor, restore_map: torch.Tensor, shape: Shape, cache_y: Optional[torch.Tensor] = None,
+            y: Optional[torch.Tensor] = None) -> torch.Tensor:
+    _need(y_kept, shape.torch_dtype, "y_kept")
+    _need(restore_map, torch.int32, "restore_map")
+    if y is None:
+        y = torch.empty((shape.F, shape.N, shape.C), dtype=y_kept.dtype, device=y_kept.device)
+    sh = shape.c()
+    L.check(L.lib().oc_restore(C.byref(sh), y_kept.data_ptr(), y_kept.shape[0], restore_map.data_ptr(),
+                               _ptr(cache_y), y.data_ptr(), _stream(y_kept)))
+    return y
+
+
+def layer_cached(x: torch.Tensor, weights: Dict[str, torch.Tensor], cache: LayerCache, shape: Shape, cfg: Cfg,
+                 ctx: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, trace: bool = False):
+    """One cached layer call; returns (cache.y, y_ctx, trace dict or None)."""
+    _need(x, shape.torch_dtype, "x")
+    _need(cache.y, shape.torch_dtype, "cache.y")
+    w = _weights(weights, shape)
+    dev = x.device
+    pl = plan(shape, cfg)
+    if ws is None:
+        ws = workspace(shape, cfg, dev)
+    y_ctx = None
+    if shape.n_ctx > 0:
+        _need(ctx, shape.torch_dtype, "ctx")
+        y_ctx = torch.empty((shape.n_ctx, shape.C), dtype=x.dtype, device=dev)
+    tr = None
+    out = None
+    if trace:
+        cold_full = cache.valid == 0 and cfg.cold == "full"
+        # a cold "full" step runs with every ratio at 0
+        tp = plan(shape, Cfg(cfg.gran, 0.0, 0.0, cfg.patch_k, cfg.cold)) if cold_full else pl
+        n_kept, n_cached = tp.n_kept, tp.n_cached
+        out = dict(node_max=torch.empty((tp.n_groups, tp.n_src_max), dtype=torch.float32, device=dev),
+                   node_idx=torch.empty((tp.n_groups, tp.n_src_max), dtype=torch.int32, device=dev),
+                   kept_idx=torch.empty(max(n_kept, 1), dtype=torch.int32, device=dev),
+                   cached_idx=torch.empty(max(n_cached, 1), dtype=torch.int32, device=dev),
+                   restore_map=torch.empty(shape.F * shape.N, dtype=torch.int32, device=dev),
+                   frame_max=torch.empty(max(pl.n_frame_src, 1), dtype=torch.float32, device=dev),
+                   frame_idx=torch.empty(max(pl.n_frame_src, 1), dtype=torch.int32, device=dev),
+                   pairs=torch.empty((max(pl.n_frame_cached, 1), 2), dtype=torch.int32, device=dev))
+        fi = L.oc_frame_info(out["frame_max"].data_ptr(), out["frame_idx"].data_ptr(), out["pairs"].data_ptr())
+        tr = L.oc_trace(out["node_max"].data_ptr(), out["node_idx"].data_ptr(), out["kept_idx"].data_ptr(),
+                        out["cached_idx"].data_ptr(), out["restore_map"].data_ptr(), fi)
+        out["kept_idx"] = out["kept_idx"][:n_kept]
+        out["cached_idx"] = out["cached_idx"][:n_cached]
+        out["frame_max"] = out["frame_max"][:pl.n_frame_src]
+        out["frame_idx"] = out["frame_idx"][:pl.n_frame_src]
+        out["pairs"] = out["pairs"][:tp.n_frame_cached]
+    c = L.oc_cache(cache.y.data_ptr(), cache.valid, cache.step)
+    sh, cf = shape.c(), cfg.c()
+    L.check(L.lib().oc_layer_cached(C.byref(sh), C.byref(cf), x.data_ptr(), _ptr(ctx), C.byref(w), C.byref(c),
+                                    _ptr(y_ctx), C.byref(tr) if tr is not None else None, ws.data_ptr(), ws.numel(),
+                                    _stream(x)))
+    cache.valid, cache.step = c.valid, c.step
+    return cache.y, y_ctx, out
+
+
+def attn_full(x: torch.Tensor, weights: Dict[str, torch.Tensor], shape: Shape, cfg: Cfg,
+              ctx: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
+    """The uncached layer on the same input: (y [F, N, C], y_ctx)."""
+    _need(x, shape.torch_dtype, "x")
+    w = _weights(weights, shape)
+    dev = x.device
+    if ws is None:
+        ws = workspace(shape, cfg, dev)
+    y = torch.empty((shape.F, shape.N, shape.C), dtype=x.dtype, device=dev)
+    y_ctx = None
+    if shape.n_ctx > 0:
+        _need(ctx, shape.torch_dtype, "ctx")
+        y_ctx = torch.empty((shape.n_ctx, shape.C), dtype=x.dtype, device=dev)
+    sh, cf = shape.c(), cfg.c()
+    L.check(L.lib().oc_attn_full(C.byref(sh), C.byref(cf), x.data_ptr(), _ptr(ctx), C.byref(w), y.data_ptr(),
+                                 _ptr(y_ctx), ws.data_ptr(), ws.numel(), _stream(x)))
+    return y, y_ctx
+
+
+class StageTimer:
+    """Per-stage kernel time from HIP events the library records around each
+    launch while this timer is attached to the calling thread."""
+
+    def __init__(self):
+        self._t = C.c_void_p()
+        L.check(L.lib().oc_timer_create(C.byref(self._t)))
+
+    def __enter__(self):
+        L.check(L.lib().oc_timer_use(self._t))
+        return self
+
+    def __exit__(self, *exc):
+        L.lib().oc_timer_use(None)
+        return False
+
+    def reset(self):
+        L.check(L.lib().oc_timer_reset(self._t))
+
+    def collect(self) -> Dict[str, Tuple[float, int]]:
+        """{stage: (total ms, launches)} including everything recorded so far."""
+        L.check(L.lib().oc_timer_collect(self._t))
+        out = {}
+        for i in range(L.lib().oc_timer_stage_count(self._t)):
+            name, ms, n = C.c_char_p(), C.c_double(), C.c_int64()
+            L.check(L.lib().oc_timer_stage(self._t, i, C.byref(name), C.byref(ms), C.byref(n)))
+            out[name.value.decode()] = (ms.value, n.value)
+        return out
+
+    def __del__(self):
+        try:
+            if self._t:
+                L.lib().oc_timer_destroy(self._t)
+        except Exception:
+            pass

@@ -1,0 +1,230 @@
+// Frame stage (OmniCache §3.2.2 Frame Cache; §3.2.3 frame-pair metadata):
+// the F x F Gram matrix of whole-frame descriptors (N*C values each) on
+// MFMA with a deterministic split-K reduction, then frame similarities,
+// best matches, the selection of the most redundant odd frames and their
+// one-to-one pairing with even frames.
+#include "oc_internal.h"
+#include "oc_device.h"
+
+namespace oc {
+
+constexpr int GRAM_WAVES = 4;
+constexpr int GRAM_TARGET_BLOCKS = 1024;
+constexpr int FMAX = 32;   // frames supported by the frame stage
+
+inline int gram_kw(const Plan &p) {
+    const long D = (long)p.N * p.C;
+    long kw = (D + (long)GRAM_WAVES * GRAM_TARGET_BLOCKS - 1) / ((long)GRAM_WAVES * GRAM_TARGET_BLOCKS);
+    kw = ((kw + 63) / 64) * 64;
+    return (int)(kw < 64 ? 64 : kw);
+}
+int gram_blocks(const Plan &p) {
+    const long D = (long)p.N * p.C;
+    const long per_block = (long)gram_kw(p) * GRAM_WAVES;
+    return (int)((D + per_block - 1) / per_block);
+}
+
+// Partial Gram of frames over k in this block's range; lane l of a wave feeds
+// frame (l % 16) (+16 for the second tile) and k chunks [g*16, g*16+8) and
+// [g*16+8, g*16+16) of each 64-wide step (g = l / 16); the same fragment is
+// both MFMA operands, so the result is X X^T.
+template <bool TWO>
+__global__ __launch_bounds__(256) void k_frame_gram(const uint16_t *__restrict__ x, int F, long D, int kw,
+                                                     float *__restrict__ part) {
+    __shared__ float red[GRAM_WAVES][FMAX * FMAX];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const long k_begin = ((long)blockIdx.x * GRAM_WAVES + wave) * kw;
+    const long k_end = min(k_begin + kw, D);
+    const int fr = lane & 15, g = lane >> 4;
+    const uint16_t *row0 = fr < F ? x + (long)fr * D : nullptr;
+    const uint16_t *row1 = (TWO && fr + 16 < F) ? x + (long)(fr + 16) * D : nullptr;
+    f32x4 acc00 = {0, 0, 0, 0}, acc01 = {0, 0, 0, 0}, acc10 = {0, 0, 0, 0}, acc11 = {0, 0, 0, 0};
+    for (long k = k_begin; k < k_end; k += 64) {
+        bf16x8 a0[2], a1[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const long kk = k + g * 16 + t * 8;
+            uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
+            if (kk < k_end) {
+                if (row0) v0 = *reinterpret_cast<const uint4 *>(row0 + kk);
+                if (TWO && row1) v1 = *reinterpret_cast<const uint4 *>(row1 + kk);
+            }
+            a0[t] = *reinterpret_cast<bf16x8 *>(&v0);
+            a1[t] = *reinterpret_cast<bf16x8 *>(&v1);
+        }
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            acc00 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[t], a0[t], acc00, 0, 0, 0);
+            if (TWO) {
+                acc01 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[t], a1[t], acc01, 0, 0, 0);
+                acc10 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[t], a0[t], acc10, 0, 0, 0);
+                acc11 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[t], a1[t], acc11, 0, 0, 0);
+            }
+        }
+    }
+    // lane holds rows m = 4*g + e, column n = lane % 16 of each 16x16 tile
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int m = 4 * g + e, n = fr;
+        red[wave][m * FMAX + n] = acc00[e];
+        if (TWO) {
+            red[wave][m * FMAX + n + 16] = acc01[e];
+            red[wave][(m + 16) * FMAX + n] = acc10[e];
+            red[wave][(m + 16) * FMAX + n + 16] = acc11[e];
+        } else {
+            red[wave][m * FMAX + n + 16] = 0.f;
+            red[wave][(m + 16) * FMAX + n] = 0.f;
+            red[wave][(m + 16) * FMAX + n + 16] = 0.f;
+        }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < FMAX * FMAX; e += blockDim.x) {
+        float s = red[0][e];
+#pragma unroll
+        for (int w = 1; w < GRAM_WAVES; ++w) s += red[w][e];
+        part[(long)blockIdx.x * FMAX * FMAX + e] = s;
+    }
+}
+
+// fp32 frames (small layers): one block per frame pair, fp64 accumulation,
+// a single partial.
+__global__ void k_frame_gram_f32(const float *__restrict__ x, int F, long D, float *__restrict__ part) {
+    __shared__ double red[256];
+    const int i = blockIdx.x / F, j = blockIdx.x % F;
+    double s = 0.0;
+    for (long k = threadIdx.x; k < D; k += blockDim.x) s += (double)x[(long)i * D + k] * (double)x[(long)j * D + k];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if ((int)threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) part[i * FMAX + j] = (float)red[0];
+}
+
+// Deterministic fp64 sum of the partial Grams, frame cosines, best matches
+// of odd frames, and (pairing mode) selection, greedy pairing and the
+// attention-unit table.  One block.
+__global__ __launch_bounds__(1024) void k_frame_final(const float *__restrict__ part, int n_part, int F, int R_f,
+                                                      int pairing, double *__restrict__ fsim,
+                                                      float *__restrict__ node_max, int32_t *__restrict__ node_idx,
+                                                      int32_t *__restrict__ forder, int32_t *__restrict__ pairs,
+                                                      int32_t *__restrict__ units) {
+    __shared__ double G[FMAX * FMAX];
+    __shared__ double cs[FMAX * FMAX];
+    const int t = threadIdx.x;
+    if (t < FMAX * FMAX) {
+        double s = 0.0;
+        for (int b = 0; b < n_part; ++b) s += (double)part[(long)b * FMAX * FMAX + t];
+        G[t] = s;
+    }
+    __syncthreads();
+    if (t < FMAX * FMAX) {
+        const int i = t / FMAX, j = t % FMAX;
+        double c = 0.0;
+        if (i < F && j < F) {
+            const double d = sqrt(G[i * FMAX + i]) * sqrt(G[j * FMAX + j]);
+            c = d > 0.0 ? G[t] / d : 0.0;
+        }
+        cs[t] = c;
+        fsim[t] = c;
+    }
+    __syncthreads();
+    if (t != 0) return;
+    const int n_src = F / 2, n_dst = (F + 1) / 2;
+    double bm[FMAX / 2];
+    for (int i = 0; i < n_src; ++i) {
+        const int s = 2 * i + 1;
+        double best = -INFINITY;
+        int bi = -1;
+        for (int j = 0; j < n_dst; ++j) {
+            const double c = cs[s * FMAX + 2 * j];
+            if (c > best) { best = c; bi = 2 * j; }
+        }
+        bm[i] = best;
+        node_max[i] = (float)best;
+        node_idx[i] = bi;
+    }
+    if (!pairing) return;
+    // the R_f most redundant odd frames, largest similarity first, smallest
+    // frame on ties
+    bool taken_src[FMAX / 2];
+    for (int i = 0; i < n_src; ++i) taken_src[i] = false;
+    for (int r = 0; r < R_f; ++r) {
+        int best = -1;
+        for (int i = 0; i < n_src; ++i)
+            if (!taken_src[i] && (best < 0 || bm[i] > bm[best])) best = i;
+        taken_src[best] = true;
+        forder[r] = 2 * best + 1;
+    }
+    // greedy one-to-one pairing in selection order
+    bool taken_dst[FMAX];
+    for (int f = 0; f < FMAX; ++f) taken_dst[f] = false;
+    bool in_pair[FMAX];
+    for (int f = 0; f < FMAX; ++f) in_pair[f] = false;
+    for (int r = 0; r < R_f; ++r) {
+        const int s = forder[r];
+        int bd = -1;
+        for (int j = 0; j < n_dst; ++j) {
+            const int d = 2 * j;
+            if (taken_dst[d]) continue;
+            if (bd < 0 || cs[s * FMAX + d] > cs[s * FMAX + bd]) bd = d;
+        }
+        taken_dst[bd] = true;
+        pairs[2 * r] = s;
+        pairs[2 * r + 1] = bd;
+        in_pair[s] = in_pair[bd] = true;
+    }
+    // attention units ordered by their smallest frame
+    int u = 0;
+    for (int f = 0; f < F; ++f) {
+        if (!in_pair[f]) {
+            units[2 * u] = f;
+            units[2 * u + 1] = -1;
+            ++u;
+            continue;
+        }
+        for (int r = 0; r < R_f; ++r) {
+            const int s = pairs[2 * r], d = pairs[2 * r + 1];
+            if (min(s, d) == f) {
+                units[2 * u] = s;
+                units[2 * u + 1] = d;
+                ++u;
+            }
+        }
+    }
+}
+
+hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, char *ws, float *node_max,
+                              int32_t *node_idx, hipStream_t st) {
+    const long D = (long)p.N * p.C;
+    int nb = gram_blocks(p);
+    float *part = (float *)(ws + L.gram_part);
+    if (!p.bf16) {
+        nb = 1;
+        {
+            StageScope _stage(st, "frame_gram");
+            k_frame_gram_f32<<<p.F * p.F, 256, 0, st>>>((const float *)x, p.F, D, part);
+        }
+    } else if (p.F > 16)
+        {
+            StageScope _stage(st, "frame_gram");
+            k_frame_gram<true><<<nb, 256, 0, st>>>((const uint16_t *)x, p.F, D, gram_kw(p), part);
+        }
+    else
+        {
+            StageScope _stage(st, "frame_gram");
+            k_frame_gram<false><<<nb, 256, 0, st>>>((const uint16_t *)x, p.F, D, gram_kw(p), part);
+        }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    {
+        StageScope _stage(st, "frame_final");
+        k_frame_final<<<1, 1024, 0, st>>>(part, nb, p.F, p.R_f, p.gran == 3 ? 1 : 0, (double *)(ws + L.fsim), node_max,
+                                          node_idx, (int32_t *)(ws + L.forder), (int32_t *)(ws + L.pairs),
+                                          (int32_t *)(ws + L.units));
+    }
+    return hipGetLastError();
+}
+
+}  // namespace oc

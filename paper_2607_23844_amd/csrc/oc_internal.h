@@ -1,0 +1,110 @@
+// Internal plan and kernel-launcher declarations of the OmniCache library.
+// Host code (oc_api.cpp) validates, plans and carves the workspace; the
+// launchers below enqueue gfx950 kernels on the caller's stream.
+#pragma once
+#include <cstddef>
+#include <cstdint>
+#include <hip/hip_runtime_api.h>
+
+namespace oc {
+
+enum Kind { KIND_TOKEN = 0, KIND_BLOCK = 1, KIND_FRAME = 2 };
+
+// Static sizes of one call; everything depends only on shape and cfg.
+struct Plan {
+    int F, H, W, C, N, heads, dh, hd, n_ctx;
+    bool bf16;
+    int esz;                 // bytes per element of x / weights
+    int gran, k;             // granularity, patch_k
+    int ph, pw, np;          // patch height, width, tokens per patch
+    int np_src, np_dst;      // candidates / representatives per frame-patch (3/4, 1/4)
+    double r, r_frame;
+    // matching stage reported by oc_match
+    int kind;                // KIND_TOKEN (token / pair groups), KIND_BLOCK, KIND_FRAME
+    int n_groups, n_src_max, n_dst_max;
+    int R_tok;               // budget of a token / block group (unmatched frame-patch)
+    int R_pair;              // budget of a frame-pair patch group
+    // frame stage (FRAME and FRAME_TOKEN)
+    int n_fsrc, n_fdst, R_f;
+    int n_units;             // attention units: frames (TOKEN), pairs + unmatched (FRAME_TOKEN)
+    // reduced batch
+    int n_kept, n_cached, n_seq, seq_len;
+    int n_items;             // matched items: F*N tokens, N blocks, F frames
+};
+
+// Workspace carve-up (byte offsets from the caller's ws base).
+struct Layout {
+    size_t inv, part_max, part_idx, node_max, node_idx, src_ids, dst_ids, grp_R;
+    size_t gram_part, fsim, fmax, fidx, forder, pairs, units;
+    size_t flag, mtok, fcnt, kept, cached, rmap;
+    size_t attn;             // start of the attention workspace (Q, K, O, V)
+    size_t total;
+};
+
+// Attention workspace carved at `base`: Q, K, O [rows, H*dh] and V
+// (bf16: Vt [H][seq][dh][lpad]; fp32: [rows, H*dh]).
+struct AttnWs { size_t q, k, o, v, bytes; int lpad; };
+AttnWs attn_ws(const Plan &p, int n_seq, int L, size_t base);
+int gram_blocks(const Plan &p);
+
+// Representative-range splits of the similarity GEMM (its tile height in
+// representatives is 128, 64 or 32 by group size; bf16 only).
+inline int match_split(const Plan &p) {
+    if (!p.bf16) return 1;
+    const int D = p.n_dst_max;
+    const int BA = D > 64 ? 128 : (D > 32 ? 64 : 32);
+    return (D + BA - 1) / BA;
+}
+
+// Stage timing: when a timer is attached to the calling thread, the kernels
+// launched between stage_begin and stage_end are bracketed by HIP events on
+// the launch stream (oc_timer.cpp).
+struct StageScope {
+    StageScope(hipStream_t st, const char *name);
+    ~StageScope();
+    int slot;
+    hipStream_t st;
+};
+
+// ---- launchers (k_*.hip) ---------------------------------------------------
+// group id lists: src_ids [G, S] / dst_ids [G, D] (-1 padded), grp_R [G]
+hipError_t launch_group_ids(const Plan &p, const int32_t *units, int32_t *src_ids, int32_t *dst_ids,
+                            int32_t *grp_R, hipStream_t st);
+hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, hipStream_t st);
+hipError_t launch_match(const Plan &p, const Layout &L, const void *x, const float *inv,
+                        const int32_t *src_ids, const int32_t *dst_ids, float *part_max,
+                        int32_t *part_idx, float *node_max, int32_t *node_idx, hipStream_t st);
+hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, char *ws,
+                              float *node_max, int32_t *node_idx, hipStream_t st);
+hipError_t launch_select(const Plan &p, const float *node_max, const int32_t *node_idx,
+                         const int32_t *src_ids, const int32_t *dst_ids, const int32_t *grp_R,
+                         int32_t *flag, int32_t *mtok, hipStream_t st);
+hipError_t launch_compact(const Plan &p, const int32_t *units, const int32_t *flag, const int32_t *mtok,
+                          int32_t *fcnt, int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap,
+                          int map_matched, hipStream_t st);
+hipError_t launch_gather(const Plan &p, const void *x, const int32_t *kept_idx, int n_rows, void *x_kept,
+                         hipStream_t st);
+hipError_t launch_restore(const Plan &p, const void *y_kept, int n_rows, const int32_t *rmap,
+                          const void *cache_y, void *y, hipStream_t st);
+hipError_t launch_copy_matched(const Plan &p, const int32_t *cached_idx, int n_cached,
+                               const int32_t *rmap, const int32_t *kept_idx, void *y, hipStream_t st);
+hipError_t launch_fill_i32(int32_t *dst, long n, int32_t value, hipStream_t st);
+
+// Reduced attention: rows r < n_main come from x rows (row_idx[r] if row_idx,
+// else r), rows n_main..n_main+n_ctx from ctx.  Sequence s owns rows
+// [s*L, s*L+L) plus, for a single sequence, the context rows.  Output rows
+// r < n_main go to y[out_idx[r]] (or y[r]); context rows go to y_ctx.
+struct AttnArgs {
+    const void *x; const int32_t *row_idx; int n_main;
+    const void *ctx; int n_ctx;
+    int n_seq, L;                     // sequences and retained tokens per sequence
+    const void *wq, *wk, *wv, *wo;
+    void *y; const int32_t *out_idx;  // main outputs
+    void *y_ctx;
+    void *q, *k, *vt, *o;             // workspace
+    int lpad;                         // padded keys per sequence in vt
+};
+hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st);
+bool attn_head_dim_supported(int dh);
+
+}  // namespace oc

@@ -1,0 +1,190 @@
+"""Helpers that compare the HIP library with the CPU oracle.
+
+Decision parity (OmniCache §3.2 matching and selection):
+  * node_idx must equal the oracle's wherever the oracle's top-two similarity
+    margin exceeds BAND;
+  * a candidate whose oracle best-match similarity is more than BAND away
+    from its group's threshold (the R-th largest) must be cached on both
+    sides or on neither; counts are always exact;
+  * kept_idx and restore_map must equal, bit for bit, those of the oracle
+    run with the library's in-band choices forced on it;
+  * outputs: max |y - y_oracle| / RMS(y_oracle) <= 2e-2 (bf16) or 1e-4 (fp32).
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from oracle import oc_oracle as O
+import paper_2607_23844_amd as oc
+
+BAND = 1e-4
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+NODE_MAX_TOL = {"token": 2e-6, "block": 2e-6, "frame": 1e-5}
+
+
+def dev_tensor(wl, arr) -> torch.Tensor:
+    if wl.dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(arr)).cuda()
+
+
+def weights_dev(wl, w=None):
+    w = w or dict(wq=wl.wq, wk=wl.wk, wv=wl.wv, wo=wl.wo)
+    return {k: dev_tensor(wl, v) for k, v in w.items()}
+
+
+def weights_f64(wl, w=None):
+    w = w or dict(wq=wl.wq, wk=wl.wk, wv=wl.wv, wo=wl.wo)
+    return {k: wl.f64(v) for k, v in w.items()}
+
+
+def to_f64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def shapes(wl, gran=None, r=None, r_frame=None, patch_k=None, cold="matched"):
+    gran = gran or wl.gran
+    r = wl.r if r is None else r
+    r_frame = wl.r_frame if r_frame is None else r_frame
+    k = wl.patch_k if patch_k is None else patch_k
+    sh = oc.Shape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, wl.n_ctx, wl.dtype)
+    cf = oc.Cfg(gran, r, r_frame, k, cold)
+    osh = O.LayerShape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, wl.n_ctx)
+    ocf = O.CacheCfg(gran, r, r_frame, k, cold)
+    return sh, cf, osh, ocf
+
+
+def rel_err(y: np.ndarray, ref: np.ndarray) -> float:
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    return float(np.max(np.abs(y - ref))) / max(rms, 1e-30)
+
+
+def group_margins(x64: np.ndarray, g: O.Group) -> np.ndarray:
+    """Per candidate: top-1 minus top-2 cosine similarity (inf with one rep)."""
+    S = O.cosine_matrix(O.descriptors(x64, g.kind, g.src), O.descriptors(x64, g.kind, g.dst))
+    if S.shape[1] < 2:
+        return np.full(S.shape[0], np.inf)
+    top = np.sort(S, axis=1)
+    return top[:, -1] - top[:, -2]
+
+
+def check_match(x64, dec: O.Decisions, nm_gpu: np.ndarray, ni_gpu: np.ndarray, kind: str):
+    """node_max within tolerance; node_idx equal outside the margin band.
+    Returns {candidate id: gpu rep id} for in-band disagreements."""
+    tol = NODE_MAX_TOL[kind]
+    overrides = {}
+    worst = 0.0
+    for gi, g in enumerate(dec.groups):
+        n = len(g.src)
+        d = np.abs(nm_gpu[gi, :n].astype(np.float64) - dec.node_max[gi])
+        worst = max(worst, float(d.max()) if n else 0.0)
+        assert np.all(d <= tol), f"group {gi}: node_max off by {d.max():.3g} > {tol}"
+        assert np.all(nm_gpu[gi, n:] == -np.inf) and np.all(ni_gpu[gi, n:] == -1)
+        diff = np.nonzero(ni_gpu[gi, :n] != dec.node_idx[gi])[0]
+        if len(diff):
+            marg = group_margins(x64, g)
+            for i in diff:
+                assert marg[i] <= BAND, f"group {gi} cand {g.src[i]}: idx {ni_gpu[gi, i]} vs {dec.node_idx[gi][i]}, " \
+                                        f"margin {marg[i]:.3g}"
+                overrides[int(g.src[i])] = int(ni_gpu[gi, i])
+    return overrides, worst
+
+
+def check_selection(dec: O.Decisions, gpu_cached_items: set):
+    """Same cached/kept status outside the band around each group's threshold;
+    exact counts.  Returns the number of in-band disagreements."""
+    n_diff = 0
+    for gi, g in enumerate(dec.groups):
+        gset = set(i for i in g.src if i in gpu_cached_items)
+        assert len(gset) == g.R, f"group {gi}: {len(gset)} cached, budget {g.R}"
+        oset = set(dec.cached[gi])
+        if gset == oset:
+            continue
+        vals = np.sort(dec.node_max[gi])[::-1]
+        tau = vals[g.R - 1] if g.R > 0 else np.inf
+        pos = {s: i for i, s in enumerate(g.src)}
+        for item in gset ^ oset:
+            v = dec.node_max[gi][pos[item]]
+            assert abs(v - tau) <= BAND, f"group {gi} item {item}: similarity {v} vs threshold {tau}"
+            n_diff += 1
+    return n_diff
+
+
+def gpu_cached_items(kind_gran: str, cached_idx: np.ndarray, N: int) -> set:
+    if kind_gran == "block":
+        return set(int(p) % N for p in cached_idx)
+    if kind_gran == "frame":
+        return set(int(p) // N for p in cached_idx)
+    return set(int(p) for p in cached_idx)
+
+
+def check_frame_stage(x64, osh, ocf, dec: O.Decisions, fmax, fidx, pairs):
+    """Frame similarities, frame selection and pairing (frame_token)."""
+    fg = dec.frame_group
+    d = np.abs(np.asarray(fmax, np.float64) - dec.frame_max)
+    assert np.all(d <= NODE_MAX_TOL["frame"]), d.max()
+    marg = group_margins(x64, fg)
+    for i, (a, b) in enumerate(zip(fidx, dec.frame_idx)):
+        assert a == b or marg[i] <= BAND
+    g_order = [int(s) for s, _ in pairs]
+    assert len(g_order) == fg.R
+    gset, oset = set(g_order), set(dec.frame_cached_order)
+    if gset != oset:
+        vals = np.sort(dec.frame_max)[::-1]
+        tau = vals[fg.R - 1]
+        pos = {s: i for i, s in enumerate(fg.src)}
+        for f in gset ^ oset:
+            assert abs(dec.frame_max[pos[f]] - tau) <= BAND
+    # pairing: each chosen rep frame is, among the free ones, within the band of the best
+    S = dec.frame_sim
+    spos = {s: i for i, s in enumerate(fg.src)}
+    dpos = {dd: j for j, dd in enumerate(fg.dst)}
+    taken = set()
+    for s, dd in pairs:
+        s, dd = int(s), int(dd)
+        free = [j for j in fg.dst if j not in taken]
+        best = max(S[spos[s], dpos[j]] for j in free)
+        assert dd in free and S[spos[s], dpos[dd]] >= best - BAND
+        taken.add(dd)
+    return dict(frame_order=g_order, pairs=[(int(s), int(dd)) for s, dd in pairs])
+
+
+def layer_step_parity(wl, x_np, sh, cf, osh, ocf, cache, ws, ora_cache, valid, ctx_dev=None, ctx64=None,
+                      W=None, W64=None):
+    """One oc_layer_cached step against the oracle (with in-band forcing).
+    Returns the oracle's StepResult and the max relative error."""
+    W = W or weights_dev(wl)
+    W64 = W64 or weights_f64(wl)
+    x = dev_tensor(wl, x_np)
+    y, y_ctx, tr = oc.layer_cached(x, W, cache, sh, cf, ctx=ctx_dev, ws=ws, trace=True)
+    torch.cuda.synchronize()
+    x64 = wl.f64(x_np).reshape(osh.F, osh.N, osh.C)
+    no_skip = (not valid) and ocf.cold == O.COLD_FULL
+    forced = {}
+    if ocf.gran == O.FRAME_TOKEN and not no_skip:
+        dec0 = O.decide(x64, osh, ocf)
+        forced.update(check_frame_stage(x64, osh, ocf, dec0, tr["frame_max"].cpu().numpy(),
+                                        tr["frame_idx"].cpu().numpy(), tr["pairs"].cpu().numpy()))
+    dec = O.decide(x64, osh, ocf, no_skip=no_skip, forced=dict(forced))
+    kind = "block" if ocf.gran == O.BLOCK else ("frame" if ocf.gran == O.FRAME else "token")
+    nm = tr["node_max"].cpu().numpy()
+    ni = tr["node_idx"].cpu().numpy()
+    ov, worst_nm = check_match(x64, dec, nm, ni, kind)
+    cached_idx = tr["cached_idx"].cpu().numpy()
+    items = gpu_cached_items(ocf.gran, cached_idx, osh.N)
+    n_band = check_selection(dec, items)
+    forced.update(cached=items, match=ov)
+    res = O.layer_step(x64, ctx64, W64, osh, ocf, ora_cache, valid, forced=forced)
+    np.testing.assert_array_equal(tr["kept_idx"].cpu().numpy(), res.kept_idx)
+    np.testing.assert_array_equal(np.sort(cached_idx), res.cached_idx)
+    np.testing.assert_array_equal(cached_idx, res.cached_idx)
+    np.testing.assert_array_equal(tr["restore_map"].cpu().numpy(), res.restore_map)
+    err = rel_err(to_f64(y).reshape(res.y.shape), res.y)
+    tol = TOL[wl.dtype]
+    assert err <= tol, f"layer output error {err:.3g} > {tol}"
+    if ctx64 is not None:
+        e2 = rel_err(to_f64(y_ctx), res.y_ctx)
+        assert e2 <= tol, f"context output error {e2:.3g} > {tol}"
+        err = max(err, e2)
+    return res, dict(err=err, node_max_err=worst_nm, in_band=n_band, idx_overrides=len(ov))

@@ -1,0 +1,235 @@
+"""GPU parity of the HIP library against the CPU oracle (run on an MI355X).
+
+Every test calls through the C ABI (via the thin Python binding) on seeded
+synthetic inputs and compares with the oracle under the rules in
+tests/parity.py.  Sizes span several tiles with ragged tails; the full-size
+workloads run the launch configuration the benchmark times.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oc_synth import make_workload, small_workload
+from oracle import oc_oracle as O
+import paper_2607_23844_amd as oc
+
+from parity import (TOL, dev_tensor, layer_step_parity, rel_err, shapes, to_f64, weights_dev, weights_f64,
+                    check_match, group_margins)
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    oc.lib()
+    return torch.device("cuda:0")
+
+
+def chain(wl, n_steps, cold="matched", gran=None, r=None, r_frame=None, patch_k=None):
+    sh, cf, osh, ocf = shapes(wl, gran, r, r_frame, patch_k, cold)
+    dev = torch.device("cuda:0")
+    ws = oc.workspace(sh, cf, dev)
+    cache = oc.LayerCache(sh, dev)
+    ctx_dev = dev_tensor(wl, wl.ctx) if wl.n_ctx else None
+    ctx64 = wl.f64(wl.ctx) if wl.n_ctx else None
+    W, W64 = weights_dev(wl), weights_f64(wl)
+    ora, valid = None, False
+    stats = []
+    for s in range(n_steps):
+        _say(f"  step {s} of {wl.name} gran={cf.gran} r={cf.r} rf={cf.r_frame} k={cf.patch_k} cold={cold}")
+        res, st = layer_step_parity(wl, wl.steps[s], sh, cf, osh, ocf, cache, ws, ora, valid, ctx_dev, ctx64, W, W64)
+        _say(f"    {st}")
+        stats.append(st)
+        ora, valid = res.y, True
+        assert cache.valid == 1 and cache.step == s + 1
+    return stats
+
+
+# ---------------------------------------------------------------------------
+# small layers: every granularity, both dtypes, patches, context, head dims
+# ---------------------------------------------------------------------------
+SMALL = [
+    dict(gran="token", F=1, H=8, W=8, C=32, heads=2, head_dim=16, dtype="f32"),
+    dict(gran="token", F=2, H=8, W=8, C=32, heads=2, head_dim=16, dtype="f32", patch_k=2),
+    dict(gran="token", F=1, H=16, W=16, C=64, heads=2, head_dim=32, dtype="bf16"),
+    dict(gran="token", F=1, H=16, W=16, C=64, heads=2, head_dim=32, dtype="bf16", patch_k=2),
+    dict(gran="token", F=1, H=12, W=20, C=64, heads=2, head_dim=32, dtype="bf16", n_ctx=7),
+    dict(gran="token", F=3, H=16, W=12, C=144, heads=2, head_dim=72, dtype="bf16"),
+    dict(gran="token", F=1, H=24, W=24, C=128, heads=2, head_dim=64, dtype="bf16", r=0.75, patch_k=3),
+    dict(gran="block", F=6, H=8, W=8, C=64, heads=2, head_dim=16, dtype="bf16"),
+    dict(gran="block", F=5, H=8, W=12, C=48, heads=3, head_dim=16, dtype="f32", patch_k=2),
+    dict(gran="frame", F=8, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", planted=True, r_frame=0.25),
+    dict(gran="frame", F=7, H=4, W=8, C=32, heads=2, head_dim=16, dtype="f32", planted=True, r_frame=0.45),
+    dict(gran="frame_token", F=7, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r_frame=0.3, planted=True),
+    dict(gran="frame_token", F=9, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r_frame=0.45, patch_k=2,
+         planted=True),
+    dict(gran="frame_token", F=6, H=8, W=8, C=32, heads=2, head_dim=16, dtype="f32", r_frame=0.35, planted=True),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SMALL)))
+@pytest.mark.parametrize("cold", ["matched", "full"])
+def test_small_layer_chain(case, cold):
+    kw = dict(SMALL[case])
+    kw.setdefault("r", 0.5)
+    wl = small_workload(n_steps=3, seed=100 + case, **kw)
+    _say(f"case {case}: {kw} cold={cold}")
+    chain(wl, 3, cold=cold)
+
+
+# ---------------------------------------------------------------------------
+# individual entry points
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype,dh,n_seq,L,n_ctx", [
+    ("bf16", 64, 1, 2381 - 333, 333), ("bf16", 64, 3, 130, 0), ("bf16", 72, 5, 77, 0), ("bf16", 72, 7, 16, 0),
+    ("bf16", 16, 2, 9, 0), ("bf16", 128, 1, 200, 5), ("f32", 64, 1, 128, 0), ("f32", 16, 3, 33, 0),
+])
+def test_attn_reduced_vs_oracle(dtype, dh, n_seq, L, n_ctx):
+    _say(f"attn_reduced {dtype} dh={dh} n_seq={n_seq} L={L} n_ctx={n_ctx}")
+    heads = 3 if dh != 64 or n_ctx == 0 else 24
+    C = 256 if heads == 3 else 1536
+    wl = small_workload("token", F=1, H=4, W=4, C=C, heads=heads, head_dim=dh, dtype=dtype, seed=5)
+    rng = np.random.default_rng(3)
+    sh = oc.Shape(1, 4, 4, C, heads, dh, n_ctx, dtype)
+    xk = rng.standard_normal((n_seq, L, C)).astype(np.float32)
+    ctx = rng.standard_normal((n_ctx, C)).astype(np.float32) if n_ctx else None
+    from oc_synth import bf16_bits
+    store = (lambda a: bf16_bits(a)) if dtype == "bf16" else (lambda a: a)
+    xk_s = store(xk)
+    ctx_s = store(ctx) if n_ctx else None
+    y, yc = oc.attn_reduced(dev_tensor(wl, xk_s), n_seq, L, weights_dev(wl), sh,
+                            ctx=dev_tensor(wl, ctx_s) if n_ctx else None)
+    torch.cuda.synchronize()
+    yk64, yc64 = O.attn_reduced(wl.f64(xk_s), wl.f64(ctx_s) if n_ctx else None, weights_f64(wl), heads, dh)
+    e = rel_err(to_f64(y), yk64)
+    _say(f"  err {e:.3g}")
+    assert e <= TOL[dtype]
+    if n_ctx:
+        assert rel_err(to_f64(yc), yc64) <= TOL[dtype]
+
+
+def test_gather_restore_bit_exact():
+    wl = small_workload("token", F=2, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", seed=9)
+    sh, cf, osh, ocf = shapes(wl, r=0.5)
+    x = dev_tensor(wl, wl.steps[0])
+    ws = oc.workspace(sh, cf, x.device)
+    nm, ni = oc.match(x, sh, cf, ws)
+    kept, cached, rmap = oc.select(nm, ni, sh, cf, ws)
+    xk = oc.gather(x, kept, sh, cf)
+    torch.cuda.synchronize()
+    xs = x.view(torch.int16).cpu().numpy().reshape(-1, sh.C)
+    k = kept.cpu().numpy()
+    np.testing.assert_array_equal(xk.view(torch.int16).cpu().numpy().reshape(-1, sh.C), xs[k])
+    # restore: kept rows from y_kept, -1 rows from the cache, in and out of place
+    yk = torch.randn((len(k), sh.C), device=x.device).to(torch.bfloat16)
+    cache = torch.randn((sh.F, sh.N, sh.C), device=x.device).to(torch.bfloat16)
+    y = oc.restore(yk, rmap, sh, cache_y=cache)
+    torch.cuda.synchronize()
+    m = rmap.cpu().numpy()
+    ref = cache.view(torch.int16).cpu().numpy().reshape(-1, sh.C).copy()
+    ykn = yk.view(torch.int16).cpu().numpy()
+    ref[m >= 0] = ykn[m[m >= 0]]
+    np.testing.assert_array_equal(y.view(torch.int16).cpu().numpy().reshape(-1, sh.C), ref)
+    c2 = cache.clone()
+    oc.restore(yk, rmap, sh, cache_y=c2, y=c2)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(c2.view(torch.int16).cpu().numpy().reshape(-1, sh.C), ref)
+
+
+def test_select_is_exact_on_library_similarities():
+    """The selection kernel is integer work: given the library's own fp32
+    node_max, its cached set equals the definition (largest first, smallest id
+    on ties) evaluated on exactly those values, with many deliberate ties."""
+    wl = small_workload("token", F=1, H=32, W=32, C=64, heads=2, head_dim=32, dtype="bf16", seed=4)
+    sh, cf, osh, ocf = shapes(wl, r=0.5, patch_k=2)
+    x = dev_tensor(wl, wl.steps[0])
+    ws = oc.workspace(sh, cf, x.device)
+    nm, ni = oc.match(x, sh, cf, ws)
+    # quantise the similarities to force many exact ties
+    nmq = (torch.round(nm * 64) / 64).contiguous()
+    nmq[torch.isinf(nm)] = -float("inf")
+    kept, cached, rmap = oc.select(nmq, ni, sh, cf, ws)
+    torch.cuda.synchronize()
+    dec = O.decide(wl.f64(wl.steps[0]).reshape(osh.F, osh.N, osh.C), osh, ocf)
+    v = nmq.cpu().numpy().astype(np.float64)
+    expect = []
+    for gi, g in enumerate(dec.groups):
+        expect += O.select_cached(v[gi, :len(g.src)], g.src, g.R)
+    np.testing.assert_array_equal(cached.cpu().numpy(), np.array(sorted(expect)))
+
+
+@pytest.mark.parametrize("gran,F", [("token", 1), ("block", 4), ("frame", 4), ("frame_token", 5)])
+def test_r0_is_bit_identical_to_full_attention(gran, F):
+    wl = small_workload(gran, F=F, H=16, W=16, C=64, heads=2, head_dim=32, dtype="bf16", seed=21)
+    sh, cf, osh, ocf = shapes(wl, r=0.0, r_frame=0.0)
+    dev = torch.device("cuda:0")
+    x = dev_tensor(wl, wl.steps[0])
+    ws = oc.workspace(sh, cf, dev)
+    cache = oc.LayerCache(sh, dev)
+    y, _, _ = oc.layer_cached(x, weights_dev(wl), cache, sh, cf, ws=ws)
+    yf, _ = oc.attn_full(x, weights_dev(wl), sh, cf, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), yf.view(torch.int16))
+
+
+def test_repeat_runs_are_bit_identical():
+    wl = small_workload("frame_token", F=7, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r_frame=0.3, seed=2)
+    sh, cf, osh, ocf = shapes(wl)
+    dev = torch.device("cuda:0")
+    x = dev_tensor(wl, wl.steps[0])
+    ws = oc.workspace(sh, cf, dev)
+    outs = []
+    for _ in range(3):
+        cache = oc.LayerCache(sh, dev)
+        y, _, tr = oc.layer_cached(x, weights_dev(wl), cache, sh, cf, ws=ws, trace=True)
+        torch.cuda.synchronize()
+        outs.append((y.view(torch.int16).clone(), tr["restore_map"].clone(), tr["node_max"].clone()))
+    for o in outs[1:]:
+        assert all(torch.equal(a, b) for a, b in zip(o, outs[0]))
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads (the shapes the benchmark times)
+# ---------------------------------------------------------------------------
+def test_tok16_f32_chain():
+    wl = make_workload("tok16_f32", 4)
+    chain(wl, 4)
+
+
+@pytest.mark.parametrize("k", [2, 4, 8])
+def test_sd3_match_patch_sizes(k):
+    wl = make_workload("sd3_1024", 1)
+    sh, cf, osh, ocf = shapes(wl, r=0.5, patch_k=k)
+    x = dev_tensor(wl, wl.steps[0])
+    ws = oc.workspace(sh, cf, x.device)
+    nm, ni = oc.match(x, sh, cf, ws)
+    torch.cuda.synchronize()
+    x64 = wl.f64(wl.steps[0])
+    dec = O.decide(x64, osh, ocf)
+    ov, worst = check_match(x64, dec, nm.cpu().numpy(), ni.cpu().numpy(), "token")
+    _say(f"sd3 k={k}: node_max err {worst:.3g}, in-band idx differences {len(ov)}")
+
+
+@pytest.mark.parametrize("r", [0.25, 0.5, 0.75])
+def test_sd3_chain(r):
+    wl = make_workload("sd3_1024", 4 if r == 0.5 else 2)
+    chain(wl, 4 if r == 0.5 else 2, r=r)
+
+
+def test_latte_spatial_planted_chain():
+    wl = make_workload("latte_spatial_planted", 3)
+    chain(wl, 3)
+
+
+def test_latte_temporal_chain():
+    wl = make_workload("latte_temporal", 2)
+    chain(wl, 2)
