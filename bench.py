@@ -172,11 +172,21 @@ def main():
     ap.add_argument("--r", type=float, default=0.5)
     ap.add_argument("--cpu-steps", type=int, default=2)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="first run a plain 256 MiB read + 256 MiB write elementwise kernel (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU: the cached layer is measured whole on a single MI355X and there is "
               f"no multi-GPU path (asked for --gpus {args.gpus})", file=sys.stderr)
         sys.exit(2)
+    if args.copy_probe:
+        import torch
+        src = torch.ones(64 << 20, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     g = run_gpu(args)
     cpu = None if args.no_cpu else run_cpu_baseline(args)
     ms = g["ms"]
