@@ -23,7 +23,9 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "liboc.so")
 ARCH = "gfx950"
 
-DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# no packed fp32 vector instructions; MFMA accumulators in ordinary VGPRs
+# (the softmax and epilogues then read them without AGPR<->VGPR copies)
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 COMMON = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
           "-Wno-unused-result"]
 

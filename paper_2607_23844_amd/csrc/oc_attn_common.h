@@ -1,0 +1,44 @@
+// Shared pieces of the reduced-attention kernels.
+#pragma once
+#include "oc_internal.h"
+#include "oc_device.h"
+
+namespace oc {
+
+// Batch row r of the reduced attention: x rows (through row_idx) then the
+// context rows.  nullptr past the end (a zero row for the tile loaders).
+struct RowMap {
+    const uint16_t *x; const int32_t *row_idx; int n_main;
+    const uint16_t *ctx; int n_rows; int C;
+    __device__ __forceinline__ const uint16_t *row(int r) const {
+        if (r >= n_rows) return nullptr;
+        if (r < n_main) return x + (long)(row_idx ? row_idx[r] : r) * C;
+        return ctx + (long)(r - n_main) * C;
+    }
+};
+
+// sequence and position of batch row r (a single sequence also owns the
+// context rows appended after its L retained tokens)
+__device__ __forceinline__ void seq_pos(int r, int n_seq, int L, int &s, int &j) {
+    if (n_seq == 1) { s = 0; j = r; }
+    else { s = r / L; j = r - s * L; }
+}
+
+// Work-groups are dispatched round-robin over the 8 XCDs (id % 8).  This
+// maps a dispatch id to a logical id such that logical ids
+// [start_x, start_x + count_x) all run on XCD x: consecutive logical blocks
+// share an XCD and its L2.  A bijection on [0, total).
+__device__ __forceinline__ int xcd_remap(int id, int total) {
+    const int x = id & 7, k = id >> 3;
+    int start = 0;
+#pragma unroll
+    for (int j = 0; j < 7; ++j)
+        if (j < x) start += (total - j + 7) >> 3;
+    return start + k;
+}
+
+hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, hipStream_t st);
+hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStream_t st);
+hipError_t launch_flash(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st);
+
+}  // namespace oc
