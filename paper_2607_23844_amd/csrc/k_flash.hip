@@ -95,9 +95,9 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
         // keys 8kc..8kc+3 -> position off, keys 8kc+4..8kc+7 -> 8+off of their 16-key block
         vlds[i] = d * LDV + (kc >> 1) * 16 + (kc & 1) * 4;
     }
-    uint4 kr[KPT], vr[VPT];
+    uint4 kr0[KPT], vr0[VPT], kr1[KPT], vr1[VPT];
     const long kstep = (long)KT * hd;
-    auto load = [&](int k0, bool tail) {
+    auto load = [&](int k0, bool tail, uint4 *kr, uint4 *vr) {
 #pragma unroll
         for (int i = 0; i < KPT; ++i) {
             uint4 v = make_uint4(0, 0, 0, 0);
@@ -120,7 +120,7 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
             vr[i] = v;
         }
     };
-    auto store = [&](int buf) {
+    auto store = [&](int buf, const uint4 *kr, const uint4 *vr) {
 #pragma unroll
         for (int i = 0; i < KPT; ++i)
             if (threadIdx.x + i * NT < KCH) *reinterpret_cast<uint4 *>(&Ks[buf][klds[i]]) = kr[i];
@@ -143,14 +143,16 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
         for (int db = 0; db < DV / 32; ++db) o[qb][db] = f32x16{};
     }
 
+    // tile kt lives in LDS buffer kt&1; global loads run two tiles ahead of
+    // the buffer they fill, through two register sets
     const int n_kt = cdiv(Lk, KT);
-    load(0, KT > Lk);
-    store(0);
+    load(0, KT > Lk, kr0, vr0);
+    store(0, kr0, vr0);
+    if (n_kt > 1) load(KT, 2 * KT > Lk, kr1, vr1);
+    if (n_kt > 2) load(2 * KT, 3 * KT > Lk, kr0, vr0);
     __syncthreads();
-    for (int kt = 0; kt < n_kt; ++kt) {
-        const int buf = kt & 1, k0 = kt * KT;
-        const bool more = kt + 1 < n_kt;
-        if (more) load(k0 + KT, k0 + 2 * KT > Lk);
+    auto tile = [&](int kt, int buf) {
+        const int k0 = kt * KT;
         f32x16 sc[QB][2];
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
@@ -227,7 +229,16 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
                 for (int qb = 0; qb < QB; ++qb)
                     o[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf[qb][kstep4], o[qb][db], 0, 0, 0);
             }
-        if (more) store(buf ^ 1);
+    };
+    for (int kt = 0; kt < n_kt; kt += 2) {
+        tile(kt, 0);
+        if (kt + 1 < n_kt) store(1, kr1, vr1);
+        if (kt + 3 < n_kt) load((kt + 3) * KT, (kt + 4) * KT > Lk, kr1, vr1);
+        __syncthreads();
+        if (kt + 1 >= n_kt) break;
+        tile(kt + 1, 1);
+        if (kt + 2 < n_kt) store(0, kr0, vr0);
+        if (kt + 4 < n_kt) load((kt + 4) * KT, (kt + 5) * KT > Lk, kr0, vr0);
         __syncthreads();
     }
     // normalise and store: lane holds query ln, d = db*32 + 8*g4 + 4*lg + e

@@ -4,6 +4,7 @@
 #include "oc_internal.h"
 #include "oc_device.h"
 #include "oc_mfma_tile.h"
+#include "oc_attn_common.h"
 
 namespace oc {
 
@@ -75,18 +76,13 @@ __global__ void k_frame_ids(int F, int S, int D, int R, int32_t *src_ids, int32_
 
 hipError_t launch_group_ids(const Plan &p, const int32_t *units, int32_t *src_ids, int32_t *dst_ids,
                             int32_t *grp_R, hipStream_t st) {
+    StageScope _stage(st, "group_ids");
     if (p.kind == KIND_FRAME) {
-        {
-            StageScope _stage(st, "group_ids");
-            k_frame_ids<<<1, 64, 0, st>>>(p.F, p.n_src_max, p.n_dst_max, p.R_f, src_ids, dst_ids, grp_R);
-        }
+        k_frame_ids<<<1, 64, 0, st>>>(p.F, p.n_src_max, p.n_dst_max, p.R_f, src_ids, dst_ids, grp_R);
     } else {
-        {
-            StageScope _stage(st, "group_ids");
-            k_group_ids<<<p.n_groups, 256, 0, st>>>(p.kind, p.F, p.N, p.W, p.k, p.ph, p.pw, p.np, p.np_src, p.np_dst,
-                                                    p.n_src_max, p.n_dst_max, p.R_tok, p.R_pair, units, src_ids,
-                                                    dst_ids, grp_R);
-        }
+        k_group_ids<<<p.n_groups, 256, 0, st>>>(p.kind, p.F, p.N, p.W, p.k, p.ph, p.pw, p.np, p.np_src, p.np_dst,
+                                                p.n_src_max, p.n_dst_max, p.R_tok, p.R_pair, units, src_ids,
+                                                dst_ids, grp_R);
     }
     return hipGetLastError();
 }
@@ -119,40 +115,39 @@ __global__ void k_inv_norm(const T *__restrict__ x, float *__restrict__ inv, int
 }
 
 hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, hipStream_t st) {
+    StageScope _stage(st, "inv_norm");
     const int n_items = p.kind == KIND_BLOCK ? p.N : p.F * p.N;
     const int n_sub = p.kind == KIND_BLOCK ? p.F : 1;
     const long sub = (long)p.N * p.C;
     const int blocks = cdiv(n_items, 4);
     if (p.bf16)
-        {
-            StageScope _stage(st, "inv_norm");
-            k_inv_norm<uint16_t><<<blocks, 256, 0, st>>>((const uint16_t *)x, inv, n_items, n_sub, sub, p.C);
-        }
+        k_inv_norm<uint16_t><<<blocks, 256, 0, st>>>((const uint16_t *)x, inv, n_items, n_sub, sub, p.C);
     else
-        {
-            StageScope _stage(st, "inv_norm");
-            k_inv_norm<float><<<blocks, 256, 0, st>>>((const float *)x, inv, n_items, n_sub, sub, p.C);
-        }
+        k_inv_norm<float><<<blocks, 256, 0, st>>>((const float *)x, inv, n_items, n_sub, sub, p.C);
     return hipGetLastError();
 }
 
 // ----------------------------------------------------------------------------
 // similarity + arg-max, bf16 MFMA
 // ----------------------------------------------------------------------------
-// Block (bt, at, g): candidates b in [bt*BB, +BB) x representatives a in
-// [at*BA, +BA) of group g.  t = dot(src_b, dst_a) * inv(dst_a); per candidate
-// the largest t over this block's representatives (smallest position on
-// ties) goes to part[at][g][b].  The representative norm is applied before
-// the arg-max, the candidate's own norm (a positive constant per row) after.
+// Block (candidate tile bt, representative tile at, group g), in an
+// XCD-aware order: t = dot(src_b, dst_a) * inv(dst_a); per candidate the
+// largest t over this block's representatives (smallest position on ties)
+// goes to part[at][g][b].  The representative norm is applied before the
+// arg-max, the candidate's own norm (a positive constant per row) after.
 template <int BA, int BB, int WA, int WB>
 __global__ __launch_bounds__(256) void k_match_mfma(const uint16_t *__restrict__ x, const float *__restrict__ inv,
                                                      const int32_t *__restrict__ src_ids,
                                                      const int32_t *__restrict__ dst_ids, int G, int S, int D,
                                                      int K, int seg_len, long sub_stride, long item_stride,
-                                                     float *__restrict__ part_max, int32_t *__restrict__ part_idx) {
+                                                     int n_bt, int n_at, float *__restrict__ part_max,
+                                                     int32_t *__restrict__ part_idx) {
     using T = MfmaTile<BA, BB, WA, WB>;
     extern __shared__ __align__(16) uint16_t lds[];
-    const int bt = blockIdx.x, at = blockIdx.y, g = blockIdx.z;
+    const int total = n_bt * n_at * G;
+    const int lid = xcd_remap(blockIdx.x, total);
+    // consecutive logical blocks: the representative tiles of one candidate tile
+    const int at = lid % n_at, bt = (lid / n_at) % n_bt, g = lid / (n_at * n_bt);
     const int32_t *src = src_ids + (long)g * S;
     const int32_t *dst = dst_ids + (long)g * D;
     const uint16_t *rowsA[T::CA], *rowsB[T::CB];
@@ -171,45 +166,43 @@ __global__ __launch_bounds__(256) void k_match_mfma(const uint16_t *__restrict__
     T tile;
     tile.run(lds, rowsA, rowsB, K, seg_len, sub_stride);
 
-    // epilogue: per-lane arg-max over this lane's representatives
+    // representative norms of this tile (0 for padding, which never wins)
+    float *sinv = reinterpret_cast<float *>(lds);
+    float *sv = sinv + BA;
+    int *si = reinterpret_cast<int *>(sv + WA * BB);
+    for (int a = threadIdx.x; a < BA; a += 256) {
+        const int ga = at * BA + a;
+        const int id = ga < D ? dst[ga] : -1;
+        sinv[a] = id >= 0 ? inv[id] : -1.f;
+    }
+    __syncthreads();
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wa = wave / WB;
-    float bv[T::TB];
-    int bi[T::TB];
 #pragma unroll
     for (int j = 0; j < T::TB; ++j) {
-        bv[j] = -INFINITY;
-        bi[j] = -1;
+        float bv = -INFINITY;
+        int bi = -1;
 #pragma unroll
         for (int i = 0; i < T::TA; ++i)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int a = at * BA + T::a_of(i, e);
-                if (a < D) {
-                    const int id = dst[a];
-                    if (id >= 0) argmax_merge(bv[j], bi[j], tile.acc[i][j][e] * inv[id], a);
+            for (int g4 = 0; g4 < 4; ++g4)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int al = T::a_of(i, g4) + e;
+                    const float w = sinv[al];
+                    if (w >= 0.f) argmax_merge(bv, bi, tile.acc[i][j][4 * g4 + e] * w, at * BA + al);
                 }
-            }
-#pragma unroll
-        for (int o = 16; o < 64; o <<= 1) {
-            const float v2 = __shfl_xor(bv[j], o, WAVE);
-            const int i2 = __shfl_xor(bi[j], o, WAVE);
-            argmax_merge(bv[j], bi[j], v2, i2);
-        }
-    }
-    // merge the WA waves that share a candidate range, in ascending a order
-    __syncthreads();
-    float *sv = reinterpret_cast<float *>(lds);
-    int *si = reinterpret_cast<int *>(lds) + WA * BB;
-    if (lane < 16) {
-#pragma unroll
-        for (int j = 0; j < T::TB; ++j) {
+        const float v2 = __shfl_xor(bv, 32, WAVE);
+        const int i2 = __shfl_xor(bi, 32, WAVE);
+        argmax_merge(bv, bi, v2, i2);
+        if (lane < 32) {
             const int bl = T::b_of(j);
-            sv[wa * BB + bl] = bv[j];
-            si[wa * BB + bl] = bi[j];
+            sv[wa * BB + bl] = bv;
+            si[wa * BB + bl] = bi;
         }
     }
     __syncthreads();
+    // merge the WA waves that share a candidate range, in ascending a order
     for (int bl = threadIdx.x; bl < BB; bl += 256) {
         float v = sv[bl];
         int ix = si[bl];
@@ -275,6 +268,19 @@ __global__ void k_match_reduce(const float *__restrict__ part_max, const int32_t
     node_idx[i] = ix >= 0 ? dst_ids[(long)g * D + ix] : -1;
 }
 
+template <int BA, int BB, int WA, int WB>
+static void go_match(const Plan &p, const uint16_t *x, const float *inv, const int32_t *src_ids,
+                     const int32_t *dst_ids, int K, int seg_len, long sub_stride, long item_stride, float *part_max,
+                     int32_t *part_idx, hipStream_t st) {
+    using T = MfmaTile<BA, BB, WA, WB>;
+    const int G = p.n_groups, S = p.n_src_max, D = p.n_dst_max;
+    const int n_bt = cdiv(S, BB), n_at = cdiv(D, BA);
+    const size_t lds = T::LDS_BYTES;
+    k_match_mfma<BA, BB, WA, WB><<<n_bt * n_at * G, 256, lds, st>>>(x, inv, src_ids, dst_ids, G, S, D, K, seg_len,
+                                                                     sub_stride, item_stride, n_bt, n_at, part_max,
+                                                                     part_idx);
+}
+
 hipError_t launch_match(const Plan &p, const Layout &L, const void *x, const float *inv, const int32_t *src_ids,
                         const int32_t *dst_ids, float *part_max, int32_t *part_idx, float *node_max,
                         int32_t *node_idx, hipStream_t st) {
@@ -285,43 +291,22 @@ hipError_t launch_match(const Plan &p, const Layout &L, const void *x, const flo
     const long sub_stride = (long)p.N * p.C;
     const long item_stride = p.C;
     const int n_split = match_split(p);
-    if (p.bf16) {
-        const uint16_t *xb = (const uint16_t *)x;
-        if (D > 64) {
-            constexpr int BA = 128, BB = 128;
-            using T = MfmaTile<BA, BB, 2, 2>;
-            dim3 grid(cdiv(S, BB), n_split, G);
-            const size_t lds = T::LDS_BYTES;
-            {
-                StageScope _stage(st, "match");
-                k_match_mfma<BA, BB, 2, 2><<<grid, 256, lds, st>>>(xb, inv, src_ids, dst_ids, G, S, D, K, seg_len,
-                                                                  sub_stride, item_stride, part_max, part_idx);
-            }
-        } else if (D > 32) {
-            constexpr int BA = 64, BB = 64;
-            using T = MfmaTile<BA, BB, 2, 2>;
-            dim3 grid(cdiv(S, BB), n_split, G);
-            {
-                StageScope _stage(st, "match");
-                k_match_mfma<BA, BB, 2, 2><<<grid, 256, T::LDS_BYTES, st>>>(xb, inv, src_ids, dst_ids, G, S, D, K,
-                                                                           seg_len, sub_stride, item_stride,
-                                                                           part_max, part_idx);
-            }
+    {
+        StageScope _stage(st, "match");
+        if (p.bf16) {
+            const uint16_t *xb = (const uint16_t *)x;
+            // representative tile height as in match_split(): 128, 64 or 32
+            if (D > 64)
+                go_match<128, 64, 2, 2>(p, xb, inv, src_ids, dst_ids, K, seg_len, sub_stride, item_stride, part_max,
+                                        part_idx, st);
+            else if (D > 32)
+                go_match<64, 64, 2, 2>(p, xb, inv, src_ids, dst_ids, K, seg_len, sub_stride, item_stride, part_max,
+                                       part_idx, st);
+            else
+                go_match<32, 128, 1, 4>(p, xb, inv, src_ids, dst_ids, K, seg_len, sub_stride, item_stride, part_max,
+                                        part_idx, st);
         } else {
-            constexpr int BA = 32, BB = 64;
-            using T = MfmaTile<BA, BB, 2, 2>;
-            dim3 grid(cdiv(S, BB), n_split, G);
-            {
-                StageScope _stage(st, "match");
-                k_match_mfma<BA, BB, 2, 2><<<grid, 256, T::LDS_BYTES, st>>>(xb, inv, src_ids, dst_ids, G, S, D, K,
-                                                                           seg_len, sub_stride, item_stride,
-                                                                           part_max, part_idx);
-            }
-        }
-    } else {
-        dim3 grid(cdiv(S, 64), G);
-        {
-            StageScope _stage(st, "match");
+            dim3 grid(cdiv(S, 64), G);
             k_match_f32<<<grid, 64, 0, st>>>((const float *)x, inv, src_ids, dst_ids, G, S, D, K, seg_len, sub_stride,
                                              item_stride, part_max, part_idx);
         }
@@ -331,8 +316,8 @@ hipError_t launch_match(const Plan &p, const Layout &L, const void *x, const flo
     const long n = (long)G * S;
     {
         StageScope _stage(st, "match_reduce");
-        k_match_reduce<<<(unsigned)cdiv((int)n, 256), 256, 0, st>>>(part_max, part_idx, n_split, G, S, D, inv, src_ids,
-                                                                     dst_ids, node_max, node_idx);
+        k_match_reduce<<<(unsigned)cdiv((int)n, 256), 256, 0, st>>>(part_max, part_idx, n_split, G, S, D, inv,
+                                                                     src_ids, dst_ids, node_max, node_idx);
     }
     return hipGetLastError();
 }

@@ -12,6 +12,10 @@
 //               context output
 // Rows r < n_main come from x (through row_idx when given); rows after them
 // are the uncached context tokens of a single sequence.
+//
+// Tile order: blocks are remapped so that each XCD runs a contiguous range
+// of logical tiles, and logical tiles are grouped GA weight tiles wide, so
+// one XCD's L2 sees a few weight tiles and a few token tiles instead of all.
 #include "oc_internal.h"
 #include "oc_device.h"
 #include "oc_mfma_tile.h"
@@ -21,15 +25,26 @@ namespace oc {
 
 constexpr int PBA = 128, PBB = 128;
 using PTile = MfmaTile<PBA, PBB, 2, 2>;
-// output projection: O rows are fp16, wo (bf16) is converted to fp16 as it is staged
-using OTile = MfmaTile<PBA, PBB, 2, 2, true, true>;
+// output projection: O rows and wo (converted once per call) are fp16
+using OTile = MfmaTile<PBA, PBB, 2, 2, true, false>;
+constexpr int GA = 6;
+
+// logical tile lid -> (a tile, b tile), GA a-tiles per group, b fastest inside
+__device__ __forceinline__ void tile_order(int lid, int n_at, int n_bt, int &at, int &bt) {
+    const int per = GA * n_bt;
+    const int grp = lid / per, idx = lid - grp * per;
+    const int ga = min(GA, n_at - grp * GA);
+    at = grp * GA + idx % ga;
+    bt = idx / ga;
+}
 
 // a in [0, 2*hd): rows of wq then wk; b = batch rows.  Q/K[b][a % hd].
 __global__ __launch_bounds__(256) void k_proj_qk(RowMap rm, const uint16_t *__restrict__ wq,
-                                                 const uint16_t *__restrict__ wk, int hd, float qscale,
-                                                 uint16_t *__restrict__ Q, uint16_t *__restrict__ K) {
+                                                 const uint16_t *__restrict__ wk, int hd, float qscale, int n_at,
+                                                 int n_bt, uint16_t *__restrict__ Q, uint16_t *__restrict__ K) {
     extern __shared__ __align__(16) uint16_t lds[];
-    const int at = blockIdx.y, bt = blockIdx.x;
+    int at, bt;
+    tile_order(xcd_remap(blockIdx.x, n_at * n_bt), n_at, n_bt, at, bt);
     const uint16_t *rowsA[PTile::CA], *rowsB[PTile::CB];
 #pragma unroll
     for (int i = 0; i < PTile::CA; ++i) {
@@ -45,17 +60,19 @@ __global__ __launch_bounds__(256) void k_proj_qk(RowMap rm, const uint16_t *__re
         const int b = bt * PBB + PTile::b_of(j);
         if (b >= rm.n_rows) continue;
 #pragma unroll
-        for (int i = 0; i < PTile::TA; ++i) {
-            const int a = at * PBA + PTile::a_of(i, 0);
-            if (a >= 2 * hd) continue;
-            const bool isq = a < hd;
-            uint16_t *dst = isq ? Q + (long)b * hd + a : K + (long)b * hd + (a - hd);
-            const float sc = isq ? qscale : 1.f;
-            u16x4 v;
+        for (int i = 0; i < PTile::TA; ++i)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = f2h_bits(t.acc[i][j][e] * sc);
-            *reinterpret_cast<u16x4 *>(dst) = v;
-        }
+            for (int g = 0; g < 4; ++g) {
+                const int a = at * PBA + PTile::a_of(i, g);
+                if (a >= 2 * hd) continue;
+                const bool isq = a < hd;
+                uint16_t *dst = isq ? Q + (long)b * hd + a : K + (long)b * hd + (a - hd);
+                const float sc = isq ? qscale : 1.f;
+                u16x4 v;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = f2h_bits(t.acc[i][j][4 * g + e] * sc);
+                *reinterpret_cast<u16x4 *>(dst) = v;
+            }
     }
 }
 
@@ -63,9 +80,11 @@ __global__ __launch_bounds__(256) void k_proj_qk(RowMap rm, const uint16_t *__re
 // four consecutive rows of one feature: one 8-byte store when they are
 // consecutive positions of one sequence.
 __global__ __launch_bounds__(256) void k_proj_v(RowMap rm, const uint16_t *__restrict__ wv, int hd, int dh,
-                                                int n_seq, int L, int lpad, uint16_t *__restrict__ Vt) {
+                                                int n_seq, int L, int lpad, int n_at, int n_bt,
+                                                uint16_t *__restrict__ Vt) {
     extern __shared__ __align__(16) uint16_t lds[];
-    const int at = blockIdx.y, bt = blockIdx.x;
+    int at, bt;
+    tile_order(xcd_remap(blockIdx.x, n_at * n_bt), n_at, n_bt, at, bt);
     const uint16_t *rowsA[PTile::CA], *rowsB[PTile::CB];
 #pragma unroll
     for (int i = 0; i < PTile::CA; ++i) rowsA[i] = rm.row(at * PBA + PTile::chunk_row(i));
@@ -82,38 +101,41 @@ __global__ __launch_bounds__(256) void k_proj_v(RowMap rm, const uint16_t *__res
         if (f >= hd) continue;
         const int h = f / dh, d = f - h * dh;
 #pragma unroll
-        for (int i = 0; i < PTile::TA; ++i) {
-            const int r0 = at * PBA + PTile::a_of(i, 0);
-            if (r0 >= rm.n_rows) continue;
-            int s0, j0, s3, j3;
-            seq_pos(r0, n_seq, L, s0, j0);
-            seq_pos(r0 + 3, n_seq, L, s3, j3);
-            if (r0 + 3 < rm.n_rows && s0 == s3 && (j0 & 3) == 0) {
-                u16x4 v;
+        for (int i = 0; i < PTile::TA; ++i)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] = f2h_bits(t.acc[i][j][e]);
-                *reinterpret_cast<u16x4 *>(Vt + (((long)h * n_seq + s0) * dh + d) * lpad + j0) = v;
-            } else {
+            for (int g = 0; g < 4; ++g) {
+                const int r0 = at * PBA + PTile::a_of(i, g);
+                if (r0 >= rm.n_rows) continue;
+                int s0, j0, s3, j3;
+                seq_pos(r0, n_seq, L, s0, j0);
+                seq_pos(r0 + 3, n_seq, L, s3, j3);
+                if (r0 + 3 < rm.n_rows && s0 == s3 && (j0 & 3) == 0) {
+                    u16x4 v;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int r = r0 + e;
-                    if (r >= rm.n_rows) continue;
-                    int s, jj;
-                    seq_pos(r, n_seq, L, s, jj);
-                    Vt[(((long)h * n_seq + s) * dh + d) * lpad + jj] = f2h_bits(t.acc[i][j][e]);
+                    for (int e = 0; e < 4; ++e) v[e] = f2h_bits(t.acc[i][j][4 * g + e]);
+                    *reinterpret_cast<u16x4 *>(Vt + (((long)h * n_seq + s0) * dh + d) * lpad + j0) = v;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int r = r0 + e;
+                        if (r >= rm.n_rows) continue;
+                        int s, jj;
+                        seq_pos(r, n_seq, L, s, jj);
+                        Vt[(((long)h * n_seq + s) * dh + d) * lpad + jj] = f2h_bits(t.acc[i][j][4 * g + e]);
+                    }
                 }
             }
-        }
     }
 }
 
 // a in [0, C): rows of wo; b = batch rows of O.  y[out row][a].
 __global__ __launch_bounds__(256) void k_proj_out(const uint16_t *__restrict__ O, int n_rows, int hd,
                                                   const uint16_t *__restrict__ wo, int C, int n_main,
-                                                  const int32_t *__restrict__ out_idx, uint16_t *__restrict__ y,
-                                                  uint16_t *__restrict__ y_ctx) {
+                                                  const int32_t *__restrict__ out_idx, int n_at, int n_bt,
+                                                  uint16_t *__restrict__ y, uint16_t *__restrict__ y_ctx) {
     extern __shared__ __align__(16) uint16_t lds[];
-    const int at = blockIdx.y, bt = blockIdx.x;
+    int at, bt;
+    tile_order(xcd_remap(blockIdx.x, n_at * n_bt), n_at, n_bt, at, bt);
     const uint16_t *rowsA[OTile::CA], *rowsB[OTile::CB];
 #pragma unroll
     for (int i = 0; i < OTile::CA; ++i) {
@@ -133,14 +155,16 @@ __global__ __launch_bounds__(256) void k_proj_out(const uint16_t *__restrict__ O
         if (b >= n_rows) continue;
         uint16_t *yrow = b < n_main ? y + (long)(out_idx ? out_idx[b] : b) * C : y_ctx + (long)(b - n_main) * C;
 #pragma unroll
-        for (int i = 0; i < OTile::TA; ++i) {
-            const int a = at * PBA + OTile::a_of(i, 0);
-            if (a >= C) continue;
-            u16x4 v;
+        for (int i = 0; i < OTile::TA; ++i)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = f2bf(t.acc[i][j][e]);
-            *reinterpret_cast<u16x4 *>(yrow + a) = v;
-        }
+            for (int g = 0; g < 4; ++g) {
+                const int a = at * PBA + OTile::a_of(i, g);
+                if (a >= C) continue;
+                u16x4 v;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = f2bf(t.acc[i][j][4 * g + e]);
+                *reinterpret_cast<u16x4 *>(yrow + a) = v;
+            }
     }
 }
 
@@ -149,22 +173,38 @@ hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, h
     const float qscale = (float)(1.4426950408889634 / sqrt((double)p.dh));
     {
         StageScope _stage(st, "proj_qk");
-        k_proj_qk<<<dim3(cdiv(rm.n_rows, PBB), cdiv(2 * p.hd, PBA)), 256, lds, st>>>(
-            rm, (const uint16_t *)a.wq, (const uint16_t *)a.wk, p.hd, qscale, (uint16_t *)a.q, (uint16_t *)a.k);
+        const int n_at = cdiv(2 * p.hd, PBA), n_bt = cdiv(rm.n_rows, PBB);
+        k_proj_qk<<<n_at * n_bt, 256, lds, st>>>(rm, (const uint16_t *)a.wq, (const uint16_t *)a.wk, p.hd, qscale,
+                                                 n_at, n_bt, (uint16_t *)a.q, (uint16_t *)a.k);
     }
     {
         StageScope _stage(st, "proj_v");
-        k_proj_v<<<dim3(cdiv(p.hd, PBB), cdiv(rm.n_rows, PBA)), 256, lds, st>>>(
-            rm, (const uint16_t *)a.wv, p.hd, p.dh, a.n_seq, a.L, a.lpad, (uint16_t *)a.vt);
+        const int n_at = cdiv(rm.n_rows, PBA), n_bt = cdiv(p.hd, PBB);
+        k_proj_v<<<n_at * n_bt, 256, lds, st>>>(rm, (const uint16_t *)a.wv, p.hd, p.dh, a.n_seq, a.L, a.lpad, n_at,
+                                                n_bt, (uint16_t *)a.vt);
     }
     return hipGetLastError();
 }
 
+// bf16 -> fp16 (exact in the fp16 normal range, saturating outside), 8 per thread
+__global__ void k_to_f16(const uint4 *__restrict__ src, long n8, uint4 *__restrict__ dst) {
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += (long)gridDim.x * blockDim.x)
+        dst[i] = bf16x8_to_f16x8(src[i]);
+}
+
 hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStream_t st) {
+    const long n8 = (long)p.C * p.hd / 8;
+    {
+        StageScope _stage(st, "wo_f16");
+        const long blocks = (n8 + 255) / 256;
+        k_to_f16<<<(unsigned)(blocks < 2048 ? blocks : 2048), 256, 0, st>>>((const uint4 *)a.wo, n8,
+                                                                            (uint4 *)a.wo16);
+    }
     StageScope _stage(st, "proj_out");
-    k_proj_out<<<dim3(cdiv(n_rows, PBB), cdiv(p.C, PBA)), 256, OTile::LDS_BYTES, st>>>(
-        (const uint16_t *)a.o, n_rows, p.hd, (const uint16_t *)a.wo, p.C, a.n_main, a.out_idx, (uint16_t *)a.y,
-        (uint16_t *)a.y_ctx);
+    const int n_at = cdiv(p.C, PBA), n_bt = cdiv(n_rows, PBB);
+    k_proj_out<<<n_at * n_bt, 256, OTile::LDS_BYTES, st>>>((const uint16_t *)a.o, n_rows, p.hd,
+                                                           (const uint16_t *)a.wo16, p.C, a.n_main, a.out_idx, n_at,
+                                                           n_bt, (uint16_t *)a.y, (uint16_t *)a.y_ctx);
     return hipGetLastError();
 }
 

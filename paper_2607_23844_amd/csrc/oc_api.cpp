@@ -404,6 +404,7 @@ oc_status oc_attn_reduced(const oc_shape *shape, const void *x_kept, int32_t n_s
     a.y = y_kept; a.out_idx = nullptr; a.y_ctx = y_ctx;
     a.q = at<char>(ws, aw.q); a.k = at<char>(ws, aw.k); a.o = at<char>(ws, aw.o); a.vt = at<char>(ws, aw.v);
     a.lpad = aw.lpad;
+    a.wo16 = at<char>(ws, aw.wo16);
     HIP_TRY(launch_attention(p, a, stream), "attention");
     return ok();
 }
@@ -460,6 +461,7 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
     a.y = cache->y; a.out_idx = kept; a.y_ctx = y_ctx;
     a.q = at<char>(ws, aw.q); a.k = at<char>(ws, aw.k); a.o = at<char>(ws, aw.o); a.vt = at<char>(ws, aw.v);
     a.lpad = aw.lpad;
+    a.wo16 = at<char>(ws, aw.wo16);
     HIP_TRY(launch_attention(p, a, stream), "attention");
     if (map_matched) HIP_TRY(launch_copy_matched(p, cached, p.n_cached, rmap, kept, cache->y, stream), "copy matched");
 
@@ -511,6 +513,7 @@ oc_status oc_attn_full(const oc_shape *shape, const oc_cfg *cfg, const void *x, 
     a.y = y; a.out_idx = kept; a.y_ctx = y_ctx;
     a.q = at<char>(ws, aw.q); a.k = at<char>(ws, aw.k); a.o = at<char>(ws, aw.o); a.vt = at<char>(ws, aw.v);
     a.lpad = aw.lpad;
+    a.wo16 = at<char>(ws, aw.wo16);
     HIP_TRY(launch_attention(p, a, stream), "attention");
     return ok();
 }

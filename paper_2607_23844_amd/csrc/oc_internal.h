@@ -43,7 +43,7 @@ struct Layout {
 
 // Attention workspace carved at `base`: Q, K, O [rows, H*dh] and V
 // (bf16: Vt [H][seq][dh][lpad]; fp32: [rows, H*dh]).
-struct AttnWs { size_t q, k, o, v, bytes; int lpad; };
+struct AttnWs { size_t q, k, o, v, wo16, bytes; int lpad; };
 AttnWs attn_ws(const Plan &p, int n_seq, int L, size_t base);
 int gram_blocks(const Plan &p);
 
@@ -102,6 +102,7 @@ struct AttnArgs {
     void *y; const int32_t *out_idx;  // main outputs
     void *y_ctx;
     void *q, *k, *vt, *o;             // workspace
+    void *wo16;                       // workspace: wo converted to fp16 (bf16 layers)
     int lpad;                         // padded keys per sequence in vt
 };
 hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st);
