@@ -1,75 +1,151 @@
 // Flash-style attention over the retained tokens (OmniCache §3.2.3: the
 // layer runs on the retained tokens only), fp16 MFMA with fp32 accumulation.
 //
-// One block = NW waves of one (sequence, head); a wave owns QB blocks of 32
-// queries.  Per 64-key tile:
+// One block = NW waves of one (sequence, head); a wave owns 32 queries.  Per
+// 64-key tile:
 //   S^T = K Q^T  on v_mfma_f32_32x32x16_f16: K rows from LDS are the A
 //                operand, the wave's Q fragments (registers) the B operand,
-//                so the result lane l holds query l%32 and 16 of the 32 keys
-//                of each key block (rows 8*(i/4) + 4*(l/32) + i%4);
-//   softmax in the log2 domain (Q is pre-scaled by log2(e)/sqrt(dh)) with a
-//                lazily rebased reference maximum m: the S accumulator starts
-//                at -m, so the MFMA itself yields s - m; only when a score
-//                exceeds m by more than REBASE (or on the first tile) is m
-//                raised and O and the running sum rescaled.  P = exp2(s - m)
-//                <= 2^REBASE stays well inside fp16.  One lane owns one query:
-//                the tile maximum needs a single exchange with lane l^32, the
-//                running sum none until the end;
+//                so lane l holds query l%32 and 16 of the 32 keys of each key
+//                block (rows 8*(i/4) + 4*(l/32) + i%4);
+//   softmax in the log2 domain (Q is pre-scaled by log2(e)/sqrt(dh)) against
+//                a lazily raised reference maximum m: the S accumulator starts
+//                at -m, so the MFMA itself yields s - m.  P = exp2(s - m) is
+//                rounded to fp16 for the PV product; the packed fp16 maximum
+//                of P tells whether any score exceeds m by more than REBASE
+//                (or overflowed fp16).  Only then (and on the first tile) does
+//                the wave take the slow path: the fp32 maximum t of both
+//                lane halves, m += t, O and the running sum scaled by
+//                exp2(-t), P recomputed.  The running sum adds the fp16 P that
+//                the PV product uses (v_dot2 with ones, fp32 accumulation);
 //   O^T += Vt P^T on the same MFMA: P leaves the score registers as the B
-//                operand directly (8 consecutive accumulator slots = 8 keys),
-//                and Vt rows are staged in LDS with the keys of each 16-key
-//                block permuted so that the matching A operand is one
-//                contiguous 16-byte read.
-// K and Vt tiles are double-buffered in LDS with a register prefetch of the
-// next tile and one barrier per tile; only the last tile is masked.  Blocks
-// of one head are kept on one XCD (xcd_remap) so its K/V stay in its L2.
+//                operand directly (8 consecutive accumulator slots = 8 keys).
+//                Vt is stored with the keys of each 16-key block permuted
+//                (quads 1 and 2 swapped, written so by the V projection), so
+//                the matching A operand is one contiguous 16-byte read.
+// K and Vt tiles go through a ring of LDS buffers with one barrier per tile;
+// the K fragments of tile kt+1 are read into registers while tile kt
+// finishes.  Two ways to fill the ring:
+//   DMA (head_dim a multiple of 64, long sequences): global_load_lds moves
+//     16 bytes per lane straight into LDS, three tiles ahead, into a ring of
+//     four unpadded buffers whose 16-byte chunks are XOR-swizzled by row
+//     (chunk c of row r at slot c ^ (r & 7)) so the fragment reads of 8
+//     consecutive rows hit distinct banks.  Key rows past the end are
+//     clamped to the last key (their scores are masked) and the V projection
+//     zeroes the padded key positions of Vt, so nothing needs masking in LDS;
+//   registers (other head dims, short sequences): global loads one tile
+//     ahead, masked, written to a ring of three padded buffers.
+// Only the last tile's scores are masked.  Blocks of one head are kept on one
+// XCD (xcd_remap) so its K/V stay in that XCD's L2.
 #include "oc_attn_common.h"
 #include "oc_mfma_tile.h"
 
 namespace oc {
 
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
-constexpr float REBASE = 8.f;
+constexpr float REBASE = 8.f;   // P = exp2(s - m) stays below 2^REBASE on the fast path
 
-template <int DH, int QB, int NW>
+typedef __attribute__((address_space(3))) void *lds_vp;
+typedef __attribute__((address_space(1))) void *glb_vp;
+
+// s_waitcnt vmcnt(n) leaving the other counters alone (gfx9 encoding)
+#define OC_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8))
+
+template <int DH, bool DMA>
+struct FlashCfg {
+    static constexpr int DK = (DH + 15) / 16 * 16;   // S^T k-loop (16 per MFMA)
+    static constexpr int NKS = DK / 16;
+    static constexpr int DV = (DH + 31) / 32 * 32;   // O^T row blocks of 32
+    static constexpr int NDB = DV / 32;
+    static constexpr int KT = 64;                    // keys per tile
+    static constexpr int NBUF = DMA ? 4 : 3;
+    // LDS rows (halves): unpadded and swizzled for DMA, padded by 16 bytes otherwise
+    static constexpr int LDK = DMA ? DK : DK + 8, LDV = DMA ? KT : KT + 8;
+    static constexpr int KBUF = KT * LDK, VBUF = DV * LDV;
+    static constexpr size_t LDS_BYTES = (size_t)NBUF * (KBUF + VBUF) * 2;
+    static_assert(!DMA || (DK == DH && DV == DH && DH % 64 == 0), "DMA staging needs head_dim % 64 == 0");
+};
+
+// LDS offset (halves) of the 8-element chunk c of row r in a buffer of rows of LD halves
+template <bool DMA, int LD>
+__device__ __forceinline__ int lds_chunk(int r, int c) {
+    return DMA ? r * LD + ((c ^ (r & 7)) << 3) : r * LD + (c << 3);
+}
+
+template <int DH, int NW, bool DMA>
 __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                                                     const uint16_t *__restrict__ Vt, uint16_t *__restrict__ O,
                                                     int hd, int heads, int n_seq, int L, int Lk, int lpad,
                                                     int n_qt) {
-    constexpr int DK = (DH + 15) / 16 * 16;     // S^T k-loop (16 per MFMA)
-    constexpr int DV = (DH + 31) / 32 * 32;     // O^T row blocks of 32
-    constexpr int KT = 64;                      // keys per tile
-    constexpr int LDK = DK + 8, LDV = KT + 8;   // padded LDS rows (halves)
-    constexpr int NT = NW * 64, QW = 32 * QB, QT = QW * NW;
+    using C = FlashCfg<DH, DMA>;
+    constexpr int DK = C::DK, NKS = C::NKS, DV = C::DV, NDB = C::NDB, KT = C::KT, LDK = C::LDK, LDV = C::LDV;
+    constexpr int NT = NW * 64, QT = 32 * NW;
     constexpr int KCH = KT * (DK / 8), VCH = DV * (KT / 8);
     constexpr int KPT = (KCH + NT - 1) / NT, VPT = (VCH + NT - 1) / NT;
-    __shared__ __align__(16) uint16_t Ks[2][KT * LDK];
-    __shared__ __align__(16) uint16_t Vs[2][DV * LDV];
+    extern __shared__ __align__(16) uint16_t lds[];
+    uint16_t *const Ks = lds;                       // [NBUF][KT][LDK]
+    uint16_t *const Vs = lds + C::NBUF * C::KBUF;   // [NBUF][DV][LDV]
 
     const int total = n_qt * heads * n_seq;
     const int lid = xcd_remap(blockIdx.x, total);
     const int qt = lid % n_qt, hs = lid / n_qt, h = hs % heads, s = hs / heads;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, ln = lane & 31, lg = lane >> 5;
     const long row0 = (long)s * L;
-    const int q_base = qt * QT + wave * QW;
+    const int q_base = qt * QT + wave * 32;
     const uint16_t *kbase = K + row0 * hd + h * DH;
     const uint16_t *vbase = Vt + ((long)h * n_seq + s) * DH * lpad;
 
-    f16x8 qf[QB][DK / 16];
+    f16x8 qf[NKS];
+    {
+        const int q = q_base + ln;
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-        const int q = q_base + qb * 32 + ln;
-#pragma unroll
-        for (int ks = 0; ks < DK / 16; ++ks) {
+        for (int ks = 0; ks < NKS; ++ks) {
             const int d0 = ks * 16 + lg * 8;
             uint4 v = make_uint4(0, 0, 0, 0);
             if (q < Lk && d0 < DH) v = *reinterpret_cast<const uint4 *>(Q + (row0 + q) * hd + h * DH + d0);
-            qf[qb][ks] = *reinterpret_cast<f16x8 *>(&v);
+            qf[ks] = __builtin_bit_cast(f16x8, v);
         }
     }
 
-    // this thread's staging slots (fixed across tiles)
+    // DMA: instruction j of this wave fills LDS chunks q = (wave*I + j)*64 + lane
+    // of a buffer (row q / chunks-per-row, slot q % chunks-per-row); the lane
+    // fetches the chunk that the swizzle puts in that slot
+    constexpr int IK = DMA ? KCH / NT : 1, IV = DMA ? VCH / NT : 1;
+    static_assert(!DMA || (KCH % NT == 0 && VCH % NT == 0), "DMA tile split");
+    const uint16_t *kd[IK];
+    int kdrow[IK];
+    const uint16_t *vd[IV];
+    if constexpr (DMA) {
+#pragma unroll
+        for (int j = 0; j < IK; ++j) {
+            const int q = (wave * IK + j) * 64 + lane;
+            const int r = q / (DK / 8), c = (q % (DK / 8)) ^ (r & 7);
+            kdrow[j] = r;
+            kd[j] = kbase + c * 8;
+        }
+#pragma unroll
+        for (int j = 0; j < IV; ++j) {
+            const int q = (wave * IV + j) * 64 + lane;
+            const int d = q / (KT / 8), c = (q % (KT / 8)) ^ (d & 7);
+            vd[j] = vbase + (long)d * lpad + c * 8;
+        }
+    }
+    auto issue = [&](int kt) {
+        const int k0 = kt * KT, buf = kt & 3;
+        uint16_t *kb = Ks + buf * C::KBUF;
+        uint16_t *vb = Vs + buf * C::VBUF;
+#pragma unroll
+        for (int j = 0; j < IK; ++j) {
+            const int row = min(k0 + kdrow[j], Lk - 1);
+            __builtin_amdgcn_global_load_lds((glb_vp)(kd[j] + (long)row * hd), (lds_vp)(kb + (wave * IK + j) * 512),
+                                             16, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < IV; ++j)
+            __builtin_amdgcn_global_load_lds((glb_vp)(vd[j] + k0), (lds_vp)(vb + (wave * IV + j) * 512), 16, 0, 0);
+    };
+
+    // this thread's staging chunks (fixed across tiles)
     const uint16_t *kp[KPT];
     int kkey[KPT], klds[KPT];
     bool kok[KPT];
@@ -77,31 +153,32 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
     for (int i = 0; i < KPT; ++i) {
         const int c = threadIdx.x + i * NT;
         const int key = c / (DK / 8), d0 = (c % (DK / 8)) * 8;
-        kok[i] = c < KCH && d0 < DH;
+        kok[i] = (KCH % NT == 0 || c < KCH) && (DK == DH || d0 < DH);
         kkey[i] = key;
         kp[i] = kbase + (long)key * hd + d0;
         klds[i] = key * LDK + d0;
     }
     const uint16_t *vp[VPT];
-    int vkey[VPT], vlds[VPT];
+    int vpos[VPT], vlds[VPT];
     bool vok[VPT];
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
         const int c = threadIdx.x + i * NT;
         const int d = c >> 3, kc = c & 7;
-        vok[i] = c < VCH && d < DH;
-        vkey[i] = kc * 8;
+        vok[i] = (VCH % NT == 0 || c < VCH) && (DV == DH || d < DH);
+        vpos[i] = kc * 8;
         vp[i] = vbase + (long)d * lpad + kc * 8;
-        // keys 8kc..8kc+3 -> position off, keys 8kc+4..8kc+7 -> 8+off of their 16-key block
-        vlds[i] = d * LDV + (kc >> 1) * 16 + (kc & 1) * 4;
+        vlds[i] = d * LDV + kc * 8;
     }
-    uint4 kr0[KPT], vr0[VPT], kr1[KPT], vr1[VPT];
+    uint4 kr[KPT], vr[VPT];
     const long kstep = (long)KT * hd;
-    auto load = [&](int k0, bool tail, uint4 *kr, uint4 *vr) {
+    auto load = [&](int kt) {
+        const int k0 = kt * KT;
+        const bool tail = k0 + KT > Lk;
 #pragma unroll
         for (int i = 0; i < KPT; ++i) {
             uint4 v = make_uint4(0, 0, 0, 0);
-            if (kok[i] && (!tail || k0 + kkey[i] < Lk)) v = *reinterpret_cast<const uint4 *>(kp[i] + (k0 / KT) * kstep);
+            if (kok[i] && (!tail || k0 + kkey[i] < Lk)) v = *reinterpret_cast<const uint4 *>(kp[i] + kt * kstep);
             kr[i] = v;
         }
 #pragma unroll
@@ -110,177 +187,242 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
             if (vok[i]) {
                 v = *reinterpret_cast<const uint4 *>(vp[i] + k0);
                 if (tail) {
-                    const int valid = Lk - (k0 + vkey[i]);
+                    // zero the stored positions whose key is past the end
                     uint16_t *e = reinterpret_cast<uint16_t *>(&v);
+                    const int blk = vpos[i] & ~15, p0 = vpos[i] & 15;
 #pragma unroll
                     for (int t = 0; t < 8; ++t)
-                        if (t >= valid) e[t] = 0;
+                        if (k0 + blk + vt_key_of_pos(p0 + t) >= Lk) e[t] = 0;
                 }
             }
             vr[i] = v;
         }
     };
-    auto store = [&](int buf, const uint4 *kr, const uint4 *vr) {
+    auto store = [&](int buf) {
+        uint16_t *kb = Ks + buf * C::KBUF;
+        uint16_t *vb = Vs + buf * C::VBUF;
 #pragma unroll
         for (int i = 0; i < KPT; ++i)
-            if (threadIdx.x + i * NT < KCH) *reinterpret_cast<uint4 *>(&Ks[buf][klds[i]]) = kr[i];
+            if (KCH % NT == 0 || threadIdx.x + i * NT < KCH) *reinterpret_cast<uint4 *>(kb + klds[i]) = kr[i];
 #pragma unroll
         for (int i = 0; i < VPT; ++i)
-            if (threadIdx.x + i * NT < VCH) {
-                uint16_t *dst = &Vs[buf][vlds[i]];
-                *reinterpret_cast<uint2 *>(dst) = make_uint2(vr[i].x, vr[i].y);
-                *reinterpret_cast<uint2 *>(dst + 8) = make_uint2(vr[i].z, vr[i].w);
-            }
+            if (VCH % NT == 0 || threadIdx.x + i * NT < VCH) *reinterpret_cast<uint4 *>(vb + vlds[i]) = vr[i];
     };
 
-    f32x16 o[QB][DV / 32];
-    float m[QB], l[QB];
+    f16x8 kf[2][NKS];
+    auto read_k = [&](int buf) {
+        const uint16_t *kb = Ks + buf * C::KBUF;
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-        m[qb] = 0.f;
-        l[qb] = 0.f;
+        for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
-        for (int db = 0; db < DV / 32; ++db) o[qb][db] = f32x16{};
-    }
+            for (int kb2 = 0; kb2 < 2; ++kb2)
+                kf[kb2][ks] = *reinterpret_cast<const f16x8 *>(kb + lds_chunk<DMA, LDK>(kb2 * 32 + ln, ks * 2 + lg));
+    };
 
-    // tile kt lives in LDS buffer kt&1; global loads run two tiles ahead of
-    // the buffer they fill, through two register sets
-    const int n_kt = cdiv(Lk, KT);
-    load(0, KT > Lk, kr0, vr0);
-    store(0, kr0, vr0);
-    if (n_kt > 1) load(KT, 2 * KT > Lk, kr1, vr1);
-    if (n_kt > 2) load(2 * KT, 3 * KT > Lk, kr0, vr0);
-    __syncthreads();
-    auto tile = [&](int kt, int buf) {
-        const int k0 = kt * KT;
-        f32x16 sc[QB][2];
+    // output accumulator o (MFMA) and the part saved at the last rebase osv;
+    // the attention output is (osv + o) / l
+    f32x16 o[NDB], osv[NDB];
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
+    for (int db = 0; db < NDB; ++db) o[db] = osv[db] = f32x16{};
+    float m = 0.f, l0 = 0.f, l1 = 0.f;
+
+    const int n_kt = cdiv(Lk, KT);
+    constexpr int IPT = IK + IV;   // DMA instructions per wave and tile
+    if constexpr (DMA) {
+        issue(0);
+        if (n_kt > 1) issue(1);
+        if (n_kt > 2) {
+            issue(2);
+            OC_WAIT_VMCNT(IPT);   // Q and tiles 0, 1 landed; tile 2 may be in flight
+        } else {
+            OC_WAIT_VMCNT(0);
+        }
+    } else {
+        load(0);
+        store(0);
+        if (n_kt > 1) {
+            load(1);
+            store(1);
+        }
+        if (n_kt > 2) load(2);
+        // the Q fragments and tile 2 must have landed before the loop: its
+        // first MFMA then never waits on the loads a previous tile left in flight
+        OC_WAIT_VMCNT(0);
+    }
+    __syncthreads();
+    read_k(0);
+
+    const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
+    const _Float16 big = (_Float16)(float)(1 << (int)REBASE);
+    int b0 = 0;
+    for (int kt = 0; kt < n_kt; ++kt) {
+        const int b1 = DMA ? (kt + 1) & 3 : (b0 == 2 ? 0 : b0 + 1), b2 = b1 == 2 ? 0 : b1 + 1;
+        const int k0 = kt * KT;
+        // DMA: tile kt+3 into the buffer that tile kt-1 left (free since the last barrier)
+        if (DMA && kt + 3 < n_kt) issue(kt + 3);
+        // S^T - m
+        f32x16 sc[2];
+        {
             f32x16 init;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) init[i] = -m[qb];
-            sc[qb][0] = sc[qb][1] = init;
+            for (int i = 0; i < 16; ++i) init[i] = -m;
+            sc[0] = sc[1] = init;
         }
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
-            for (int ks = 0; ks < DK / 16; ++ks) {
-                const f16x8 kf = *reinterpret_cast<const f16x8 *>(&Ks[buf][(kb * 32 + ln) * LDK + ks * 16 + lg * 8]);
+            for (int kb2 = 0; kb2 < 2; ++kb2)
+                sc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf[kb2][ks], qf[ks], sc[kb2], 0, 0, 0);
+        // V fragments of this tile
+        f16x8 vf[NDB][4];
+        {
+            const uint16_t *vb = Vs + b0 * C::VBUF;
 #pragma unroll
-                for (int qb = 0; qb < QB; ++qb)
-                    sc[qb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[qb][ks], sc[qb][kb], 0, 0, 0);
-            }
+            for (int k4 = 0; k4 < 4; ++k4)
+#pragma unroll
+                for (int db = 0; db < NDB; ++db)
+                    vf[db][k4] = *reinterpret_cast<const f16x8 *>(vb + lds_chunk<DMA, LDV>(db * 32 + ln, k4 * 2 + lg));
+        }
+        // registers: tile kt+2 into the free buffer, then the global loads of tile kt+3
+        if (!DMA && kt + 2 < n_kt) {
+            store(b2);
+            if (kt + 3 < n_kt) load(kt + 3);
+        }
         if (k0 + KT > Lk) {
 #pragma unroll
-            for (int qb = 0; qb < QB; ++qb)
+            for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i)
-                        if (k0 + kb * 32 + 8 * (i >> 2) + 4 * lg + (i & 3) >= Lk) sc[qb][kb][i] = -INFINITY;
+                for (int i = 0; i < 16; ++i)
+                    if (k0 + kb2 * 32 + 8 * (i >> 2) + 4 * lg + (i & 3) >= Lk) sc[kb2][i] = -INFINITY;
         }
-        f16x8 pf[QB][4];
+        f16x8 pf[4];
+        auto exps = [&]() {
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-            float t = -INFINITY;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) t = fmaxf(t, sc[qb][kb][i]);
-            t = fmaxf(t, __shfl_xor(t, 32, 64));
-            if (kt == 0 || t > REBASE) {
-                // raise the reference maximum by t: rescale what was accumulated
-                // (nothing yet on the first tile, where t may be of any sign)
-                if (kt > 0) {
-                    const float alpha = __builtin_amdgcn_exp2f(-t);
-                    l[qb] *= alpha;
-#pragma unroll
-                    for (int db = 0; db < DV / 32; ++db) o[qb][db] *= alpha;
-                }
-#pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) sc[qb][kb][i] -= t;
-                m[qb] += t;
-            }
-            float ls = 0.f;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
+            for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
                 for (int hf = 0; hf < 2; ++hf) {
                     f16x8 f;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const float p = __builtin_amdgcn_exp2f(sc[qb][kb][8 * hf + e]);
-                        ls += p;
-                        f[e] = (_Float16)p;
-                    }
-                    pf[qb][kb * 2 + hf] = f;
+                    for (int e = 0; e < 8; ++e) f[e] = (_Float16)__builtin_amdgcn_exp2f(sc[kb2][8 * hf + e]);
+                    pf[kb2 * 2 + hf] = f;
                 }
-            l[qb] += ls;
+        };
+        exps();
+        // largest P of this lane (packed fp16; overflow gives +inf)
+        f16x2 mx = __builtin_elementwise_maximum(pf[0].s01, pf[0].s23);
+        mx = __builtin_elementwise_maximum(__builtin_elementwise_maximum(mx, pf[0].s45), pf[0].s67);
+#pragma unroll
+        for (int j = 1; j < 4; ++j) {
+            mx = __builtin_elementwise_maximum(__builtin_elementwise_maximum(mx, pf[j].s01), pf[j].s23);
+            mx = __builtin_elementwise_maximum(__builtin_elementwise_maximum(mx, pf[j].s45), pf[j].s67);
         }
+        const bool over = mx[0] > big || mx[1] > big;
+        if (kt == 0 || __builtin_amdgcn_ballot_w64(over) != 0) {
+            // raise the reference maximum of the queries that need it by the
+            // tile maximum t of both lane halves (any sign on the first tile)
+            float t = -INFINITY;
 #pragma unroll
-        for (int db = 0; db < DV / 32; ++db)
+            for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
-            for (int kstep4 = 0; kstep4 < 4; ++kstep4) {
-                const f16x8 vf =
-                    *reinterpret_cast<const f16x8 *>(&Vs[buf][(db * 32 + ln) * LDV + kstep4 * 16 + lg * 8]);
+                for (int i = 0; i < 16; ++i) t = fmaxf(t, sc[kb2][i]);
+            t = fmaxf(t, __shfl_xor(t, 32, 64));
+            const float tt = (kt == 0 || t > REBASE) ? t : 0.f;
+            float alpha = 1.f;
+            if (kt > 0) alpha = __builtin_amdgcn_exp2f(-tt);
+            l0 *= alpha;
+            l1 *= alpha;
+            // fold the MFMA accumulator into the rescaled saved sum and
+            // restart it at zero: O itself is never scaled element-wise,
+            // which keeps it in the same registers on both paths
 #pragma unroll
-                for (int qb = 0; qb < QB; ++qb)
-                    o[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf[qb][kstep4], o[qb][db], 0, 0, 0);
+            for (int db = 0; db < NDB; ++db) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) osv[db][i] = (osv[db][i] + o[db][i]) * alpha;
+                o[db] = f32x16{};
             }
-    };
-    for (int kt = 0; kt < n_kt; kt += 2) {
-        tile(kt, 0);
-        if (kt + 1 < n_kt) store(1, kr1, vr1);
-        if (kt + 3 < n_kt) load((kt + 3) * KT, (kt + 4) * KT > Lk, kr1, vr1);
+#pragma unroll
+            for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) sc[kb2][i] -= tt;
+            m += tt;
+            exps();
+        }
+        // running sum of the fp16 P, fp32 accumulation
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            l0 = __builtin_amdgcn_fdot2(pf[j].s01, ones, l0, false);
+            l1 = __builtin_amdgcn_fdot2(pf[j].s23, ones, l1, false);
+            l0 = __builtin_amdgcn_fdot2(pf[j].s45, ones, l0, false);
+            l1 = __builtin_amdgcn_fdot2(pf[j].s67, ones, l1, false);
+        }
+        // K fragments of the next tile (its buffer was filled before the last barrier)
+        if (kt + 1 < n_kt) read_k(b1);
+#pragma unroll
+        for (int k4 = 0; k4 < 4; ++k4)
+#pragma unroll
+            for (int db = 0; db < NDB; ++db)
+                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[db][k4], pf[k4], o[db], 0, 0, 0);
+        // DMA: this wave's part of tile kt+2 must have landed before the
+        // barrier that publishes it (only tile kt+3 may still be in flight)
+        if (DMA && kt + 2 < n_kt) {
+            if (kt + 3 < n_kt) {
+                OC_WAIT_VMCNT(IPT);
+            } else {
+                OC_WAIT_VMCNT(0);
+            }
+        }
         __syncthreads();
-        if (kt + 1 >= n_kt) break;
-        tile(kt + 1, 1);
-        if (kt + 2 < n_kt) store(0, kr0, vr0);
-        if (kt + 4 < n_kt) load((kt + 4) * KT, (kt + 5) * KT > Lk, kr0, vr0);
-        __syncthreads();
+        b0 = b1;
     }
     // normalise and store: lane holds query ln, d = db*32 + 8*g4 + 4*lg + e
+    float lt = l0 + l1;
+    lt += __shfl_xor(lt, 32, 64);
+    const float inv = 1.f / lt;
+    const int q = q_base + ln;
+    if (q >= Lk) return;
+    uint16_t *orow = O + (row0 + q) * hd + h * DH;
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-        const float lt = l[qb] + __shfl_xor(l[qb], 32, 64);
-        const float inv = 1.f / lt;
-        const int q = q_base + qb * 32 + ln;
-        if (q >= Lk) continue;
-        uint16_t *orow = O + (row0 + q) * hd + h * DH;
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
-        for (int db = 0; db < DV / 32; ++db)
+        for (int g4 = 0; g4 < 4; ++g4) {
+            const int d = db * 32 + 8 * g4 + 4 * lg;
+            if (d >= DH) continue;
+            u16x4 v;
 #pragma unroll
-            for (int g4 = 0; g4 < 4; ++g4) {
-                const int d = db * 32 + 8 * g4 + 4 * lg;
-                if (d >= DH) continue;
-                u16x4 v;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] = f2h_bits(o[qb][db][4 * g4 + e] * inv);
-                *reinterpret_cast<u16x4 *>(orow + d) = v;
-            }
-    }
+            for (int e = 0; e < 4; ++e) v[e] = f2h_bits((osv[db][4 * g4 + e] + o[db][4 * g4 + e]) * inv);
+            *reinterpret_cast<u16x4 *>(orow + d) = v;
+        }
 }
 
-template <int DH, int QB, int NW>
+template <int DH, int NW, bool DMA>
 static hipError_t go(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
-    const int n_qt = cdiv(Lk, 32 * QB * NW);
+    const int n_qt = cdiv(Lk, 32 * NW);
     const int total = n_qt * p.heads * a.n_seq;
-    k_flash<DH, QB, NW><<<total, NW * 64, 0, st>>>((const uint16_t *)a.q, (const uint16_t *)a.k,
-                                                    (const uint16_t *)a.vt, (uint16_t *)a.o, p.hd, p.heads, a.n_seq,
-                                                    a.L, Lk, a.lpad, n_qt);
+    const size_t lds = FlashCfg<DH, DMA>::LDS_BYTES;
+    static bool attr = false;   // one attribute call per instantiation (idempotent)
+    if (!attr) {
+        const hipError_t e = hipFuncSetAttribute((const void *)k_flash<DH, NW, DMA>,
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        attr = true;
+    }
+    k_flash<DH, NW, DMA><<<total, NW * 64, lds, st>>>((const uint16_t *)a.q, (const uint16_t *)a.k,
+                                                      (const uint16_t *)a.vt, (uint16_t *)a.o, p.hd, p.heads,
+                                                      a.n_seq, a.L, Lk, a.lpad, n_qt);
     return hipGetLastError();
 }
 
-// Query-tile shape by sequence length (measured on MI355X: 4 waves of 32
-// queries beat 2 and beat two 32-query blocks per wave at every length of
-// the SD3-like layer): a short sequence gets one or two waves per block.
+// Waves per block by sequence length: a short sequence gets one or two
+// waves (32 queries each) per block, a long one four (DMA-staged when the
+// head dim allows it).
 template <int DH>
 static hipError_t go_dh(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
-    if (Lk <= 32) return go<DH, 1, 1>(p, a, Lk, st);
-    if (Lk <= 64) return go<DH, 1, 2>(p, a, Lk, st);
-    return go<DH, 1, 4>(p, a, Lk, st);
+    if (Lk <= 32) return go<DH, 1, false>(p, a, Lk, st);
+    if (Lk <= 64) return go<DH, 2, false>(p, a, Lk, st);
+    if constexpr (DH % 64 == 0) {
+        if (flash_uses_dma(DH, Lk)) return go<DH, 4, true>(p, a, Lk, st);
+    }
+    return go<DH, 4, false>(p, a, Lk, st);
 }
 
 hipError_t launch_flash(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {

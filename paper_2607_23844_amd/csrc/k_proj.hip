@@ -6,7 +6,8 @@
 // pre-multiplied by log2(e)/sqrt(head_dim) so that the attention kernel's
 // scores are already in the log2 domain.
 //   k_proj_qk : [rows, C] x [2*H*dh, C]^T -> Q, K [rows, H*dh]
-//   k_proj_v  : -> Vt [H][seq][dh][Lpad], keys contiguous per (head, d)
+//   k_proj_v  : -> Vt [H][seq][dh][Lpad], keys contiguous per (head, d),
+//               quads 1 and 2 of every 16-key block swapped (vt_key_of_pos)
 //   k_proj_out: O [rows, H*dh] (fp16) x wo [C, H*dh] -> y rows, written
 //               straight to their positions (row -> out_idx[row]) or to the
 //               context output
@@ -80,7 +81,7 @@ __global__ __launch_bounds__(256) void k_proj_qk(RowMap rm, const uint16_t *__re
 // four consecutive rows of one feature: one 8-byte store when they are
 // consecutive positions of one sequence.
 __global__ __launch_bounds__(256) void k_proj_v(RowMap rm, const uint16_t *__restrict__ wv, int hd, int dh,
-                                                int n_seq, int L, int lpad, int n_at, int n_bt,
+                                                int n_seq, int L, int lpad, int n_at, int n_bt, int zero_pad,
                                                 uint16_t *__restrict__ Vt) {
     extern __shared__ __align__(16) uint16_t lds[];
     int at, bt;
@@ -113,7 +114,7 @@ __global__ __launch_bounds__(256) void k_proj_v(RowMap rm, const uint16_t *__res
                     u16x4 v;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) v[e] = f2h_bits(t.acc[i][j][4 * g + e]);
-                    *reinterpret_cast<u16x4 *>(Vt + (((long)h * n_seq + s0) * dh + d) * lpad + j0) = v;
+                    *reinterpret_cast<u16x4 *>(Vt + (((long)h * n_seq + s0) * dh + d) * lpad + vt_key_of_pos(j0)) = v;
                 } else {
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
@@ -121,9 +122,21 @@ __global__ __launch_bounds__(256) void k_proj_v(RowMap rm, const uint16_t *__res
                         if (r >= rm.n_rows) continue;
                         int s, jj;
                         seq_pos(r, n_seq, L, s, jj);
-                        Vt[(((long)h * n_seq + s) * dh + d) * lpad + jj] = f2h_bits(t.acc[i][j][4 * g + e]);
+                        Vt[(((long)h * n_seq + s) * dh + d) * lpad + vt_key_of_pos(jj)] = f2h_bits(t.acc[i][j][4 * g + e]);
                     }
                 }
+            }
+    }
+    // zero the padded key positions [Lk, lpad) of this block's features, for
+    // the sequences s = at, at + n_at, ... (the DMA-staged attention reads them)
+    const int Lk = n_seq == 1 ? rm.n_rows : L, npad = lpad - Lk;
+    if (zero_pad && npad > 0) {
+        for (int sq = at; sq < n_seq; sq += n_at)
+            for (int idx = threadIdx.x; idx < PBB * npad; idx += blockDim.x) {
+                const int f = bt * PBB + idx / npad, jj = Lk + idx % npad;
+                if (f >= hd) continue;
+                const int h = f / dh, d = f - h * dh;
+                Vt[(((long)h * n_seq + sq) * dh + d) * lpad + vt_key_of_pos(jj)] = 0;
             }
     }
 }
@@ -180,8 +193,9 @@ hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, h
     {
         StageScope _stage(st, "proj_v");
         const int n_at = cdiv(rm.n_rows, PBA), n_bt = cdiv(p.hd, PBB);
+        const int Lk = a.n_seq == 1 ? rm.n_rows : a.L;
         k_proj_v<<<n_at * n_bt, 256, lds, st>>>(rm, (const uint16_t *)a.wv, p.hd, p.dh, a.n_seq, a.L, a.lpad, n_at,
-                                                n_bt, (uint16_t *)a.vt);
+                                                n_bt, flash_uses_dma(p.dh, Lk) ? 1 : 0, (uint16_t *)a.vt);
     }
     return hipGetLastError();
 }

@@ -37,6 +37,16 @@ __device__ __forceinline__ int xcd_remap(int id, int total) {
     return start + k;
 }
 
+// Vt rows store the keys of each 16-key block with quads 1 and 2 swapped:
+// the key held at position p (and the position of key p; the map is its own
+// inverse).  The attention kernel's PV operand is then one 16-byte read.
+__device__ __forceinline__ int vt_key_of_pos(int p) { return (p & ~12) | ((p & 4) << 1) | ((p & 8) >> 1); }
+
+// Whether the attention kernel stages K/V by DMA for this head dim and key
+// count.  The DMA path relies on the V projection having zeroed the padded
+// key positions [Lk, lpad) of every Vt row.
+inline bool flash_uses_dma(int dh, int Lk) { return dh % 64 == 0 && dh <= 128 && Lk >= 256; }
+
 hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, hipStream_t st);
 hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStream_t st);
 hipError_t launch_flash(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st);
