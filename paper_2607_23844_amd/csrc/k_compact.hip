@@ -27,10 +27,13 @@ __global__ void k_frame_counts(const int32_t *__restrict__ flag, int N, int32_t 
 
 // One block per attention unit (a frame, or a frame pair s, d): retained
 // tokens of the unit's frames in ascending id become rows [u*L, u*L+L).
+// fcnt == nullptr: every frame caches static_cnt tokens (token groups of
+// plain frames, a fixed budget per group).
 __global__ __launch_bounds__(CMP_THREADS) void k_compact_units(const int32_t *__restrict__ units, int F,
                                                                const int32_t *__restrict__ flag,
-                                                               const int32_t *__restrict__ fcnt, int N, int L,
-                                                               int n_cached, int32_t *__restrict__ kept_idx,
+                                                               const int32_t *__restrict__ fcnt, int static_cnt,
+                                                               int N, int L, int n_cached,
+                                                               int32_t *__restrict__ kept_idx,
                                                                int32_t *__restrict__ cached_idx,
                                                                int32_t *__restrict__ rmap) {
     __shared__ int sh[17];
@@ -44,12 +47,18 @@ __global__ __launch_bounds__(CMP_THREADS) void k_compact_units(const int32_t *__
     }
     if (fa < 0 || fa >= F || fb >= F) return;   // malformed unit table
     if (threadIdx.x == 0) {
-        int ca = 0, cb = 0;
-        for (int f = 0; f < fa; ++f) ca += fcnt[f];
-        if (fb >= 0) for (int f = 0; f < fb; ++f) cb += fcnt[f];
-        base[0] = ca;          // cached tokens before frame fa
-        base[1] = cb;          // cached tokens before frame fb
-        base[2] = fcnt[fa];    // cached tokens in frame fa
+        if (fcnt == nullptr) {
+            base[0] = fa * static_cnt;
+            base[1] = fb >= 0 ? fb * static_cnt : 0;
+            base[2] = static_cnt;
+        } else {
+            int ca = 0, cb = 0;
+            for (int f = 0; f < fa; ++f) ca += fcnt[f];
+            if (fb >= 0) for (int f = 0; f < fb; ++f) cb += fcnt[f];
+            base[0] = ca;          // cached tokens before frame fa
+            base[1] = cb;          // cached tokens before frame fb
+            base[2] = fcnt[fa];    // cached tokens in frame fa
+        }
     }
     __syncthreads();
     const int n_u = fb >= 0 ? 2 * N : N;
@@ -177,13 +186,17 @@ hipError_t launch_compact(const Plan &p, const int32_t *units, const int32_t *fl
     const long total = (long)p.F * p.N;
     const unsigned grid = (unsigned)std::min<long>((total + 255) / 256, 4096);
     if (p.kind == KIND_TOKEN) {
-        {
+        // frame pairs split their budget between two frames in a data-dependent
+        // way: count per frame; plain frames cache k*k*R_tok tokens each
+        const bool pairs = p.gran == 3;
+        if (pairs) {
             StageScope _stage(st, "frame_counts");
             k_frame_counts<<<p.F, 1024, 0, st>>>(flag, p.N, fcnt);
         }
         {
             StageScope _stage(st, "compact");
-            k_compact_units<<<p.n_units, CMP_THREADS, 0, st>>>(p.gran == 3 ? units : nullptr, p.F, flag, fcnt, p.N,
+            k_compact_units<<<p.n_units, CMP_THREADS, 0, st>>>(pairs ? units : nullptr, p.F, flag,
+                                                                pairs ? fcnt : nullptr, p.k * p.k * p.R_tok, p.N,
                                                                 p.seq_len, p.n_cached, kept_idx, cached_idx, rmap);
         }
     } else if (p.kind == KIND_BLOCK) {
@@ -199,6 +212,13 @@ hipError_t launch_compact(const Plan &p, const int32_t *units, const int32_t *fl
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !map_matched) return e;
+    return launch_map_matched(p, flag, mtok, rmap, st);
+}
+
+hipError_t launch_map_matched(const Plan &p, const int32_t *flag, const int32_t *mtok, int32_t *rmap,
+                              hipStream_t st) {
+    const long total = (long)p.F * p.N;
+    const unsigned grid = (unsigned)std::min<long>((total + 255) / 256, 4096);
     {
         StageScope _stage(st, "map_matched");
         k_map_matched<<<grid, 256, 0, st>>>(p.kind, flag, mtok, p.F, p.N, rmap);

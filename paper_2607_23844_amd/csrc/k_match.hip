@@ -1,98 +1,32 @@
-// Matching kernels: group id lists, descriptor inverse norms, and the
-// similarity tile GEMM with a fused row arg-max (OmniCache §3.2.1-§3.2.3
-// cosine-similarity matching, patch-local per §3.3).
+// Matching kernels: descriptor inverse norms and the similarity tile GEMM
+// with a fused row arg-max (OmniCache §3.2.1-§3.2.3 cosine-similarity
+// matching, patch-local per §3.3).  Group members come from GroupMap.
 #include "oc_internal.h"
+#include "oc_groups.h"
 #include "oc_device.h"
 #include "oc_mfma_tile.h"
 #include "oc_attn_common.h"
+#include <algorithm>
 
 namespace oc {
 
 // ----------------------------------------------------------------------------
-// group id lists
-// ----------------------------------------------------------------------------
-// Unit u covers frame s (and frame d for a frame pair, d = -1 otherwise);
-// group g = u * k*k + patch.  Candidates are listed in ascending global id,
-// representatives (top-left token of each 2x2 window, in frame d for a pair)
-// likewise.  BLOCK groups use spatial positions as ids (frame term 0).
-
-__device__ __forceinline__ void patch_tok(int i, int pw, int &y, int &x) { y = i / pw; x = i - y * pw; }
-__device__ __forceinline__ void patch_nonrep(int i, int pw, int &y, int &x) {
-    const int per2 = 3 * pw / 2, q = i / per2, rem = i - q * per2;
-    if (rem < pw / 2) { y = 2 * q; x = 2 * rem + 1; }
-    else { y = 2 * q + 1; x = rem - pw / 2; }
-}
-__device__ __forceinline__ void patch_rep(int i, int pw, int &y, int &x) {
-    const int h = pw / 2, q = i / h;
-    y = 2 * q; x = 2 * (i - q * h);
-}
-
-__global__ void k_group_ids(int kind, int F, int N, int W, int k, int ph, int pw, int np, int np_src, int np_dst,
-                            int S, int D, int R_tok, int R_pair, const int32_t *__restrict__ units,
-                            int32_t *__restrict__ src_ids, int32_t *__restrict__ dst_ids,
-                            int32_t *__restrict__ grp_R) {
-    const int g = blockIdx.x;
-    const int kk = k * k;
-    const int u = g / kk, patch = g - u * kk;
-    const int oy = (patch / k) * ph, ox = (patch % k) * pw;
-    int s = u, d = -1;
-    if (units != nullptr) { s = units[2 * u]; d = units[2 * u + 1]; }
-    const long fbase = (kind == KIND_BLOCK) ? 0 : (long)N;
-    const bool bad = units != nullptr && (s < 0 || s >= F || d >= F || s == d);   // malformed unit table
-    if (bad) { s = 0; d = -1; }
-    const bool pair = d >= 0;
-    const int a = pair ? min(s, d) : s, b = pair ? max(s, d) : -1;
-    const int n_a = (pair && a == d) ? np_src : np;   // tokens of frame a in the list
-    const int nsrc = pair ? np + np_src : np_src;
-    for (int i = threadIdx.x; i < S; i += blockDim.x) {
-        int id = -1;
-        if (i < nsrc) {
-            int f, y, x;
-            if (!pair) { f = s; patch_nonrep(i, pw, y, x); }
-            else if (i < n_a) { f = a; if (a == d) patch_nonrep(i, pw, y, x); else patch_tok(i, pw, y, x); }
-            else { f = b; const int j = i - n_a; if (b == d) patch_nonrep(j, pw, y, x); else patch_tok(j, pw, y, x); }
-            id = (int)(f * fbase + (long)(oy + y) * W + (ox + x));
-        }
-        src_ids[(long)g * S + i] = id;
-    }
-    const int rf = pair ? d : s;
-    for (int i = threadIdx.x; i < D; i += blockDim.x) {
-        int id = -1;
-        if (i < np_dst) {
-            int y, x;
-            patch_rep(i, pw, y, x);
-            id = (int)(rf * fbase + (long)(oy + y) * W + (ox + x));
-        }
-        dst_ids[(long)g * D + i] = id;
-    }
-    if (threadIdx.x == 0) grp_R[g] = pair ? R_pair : R_tok;
-}
-
-__global__ void k_frame_ids(int F, int S, int D, int R, int32_t *src_ids, int32_t *dst_ids, int32_t *grp_R) {
-    for (int i = threadIdx.x; i < S; i += blockDim.x) src_ids[i] = 2 * i + 1 < F ? 2 * i + 1 : -1;
-    for (int i = threadIdx.x; i < D; i += blockDim.x) dst_ids[i] = 2 * i < F ? 2 * i : -1;
-    if (threadIdx.x == 0) grp_R[0] = R;
-}
-
-hipError_t launch_group_ids(const Plan &p, const int32_t *units, int32_t *src_ids, int32_t *dst_ids,
-                            int32_t *grp_R, hipStream_t st) {
-    StageScope _stage(st, "group_ids");
-    if (p.kind == KIND_FRAME) {
-        k_frame_ids<<<1, 64, 0, st>>>(p.F, p.n_src_max, p.n_dst_max, p.R_f, src_ids, dst_ids, grp_R);
-    } else {
-        k_group_ids<<<p.n_groups, 256, 0, st>>>(p.kind, p.F, p.N, p.W, p.k, p.ph, p.pw, p.np, p.np_src, p.np_dst,
-                                                p.n_src_max, p.n_dst_max, p.R_tok, p.R_pair, units, src_ids,
-                                                dst_ids, grp_R);
-    }
-    return hipGetLastError();
-}
-
-// ----------------------------------------------------------------------------
-// inverse L2 norms of item descriptors (one wave per item)
+// inverse L2 norms of item descriptors (one wave per item); blocks past the
+// norm blocks convert the output-projection weights bf16 -> fp16 (exact in
+// the fp16 normal range, saturating outside), 8 elements per thread
 // ----------------------------------------------------------------------------
 template <typename T>
 __global__ void k_inv_norm(const T *__restrict__ x, float *__restrict__ inv, int n_items, int n_sub,
-                           long sub_stride, int C) {
+                           long sub_stride, int C, int norm_blocks, unsigned long long *__restrict__ pack,
+                           long n_pack, const uint4 *__restrict__ wo, long n8, uint4 *__restrict__ wo16) {
+    if ((int)blockIdx.x >= norm_blocks) {
+        const long nb = gridDim.x - norm_blocks;
+        for (long i = (long)(blockIdx.x - norm_blocks) * blockDim.x + threadIdx.x; i < n8; i += nb * blockDim.x)
+            wo16[i] = bf16x8_to_f16x8(wo[i]);
+        return;
+    }
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n_pack; i += (long)norm_blocks * blockDim.x)
+        pack[i] = 0ull;
     constexpr int VEC = 16 / sizeof(T);
     const int item = blockIdx.x * (blockDim.x / WAVE) + (threadIdx.x / WAVE);
     const int lane = threadIdx.x & (WAVE - 1);
@@ -114,16 +48,22 @@ __global__ void k_inv_norm(const T *__restrict__ x, float *__restrict__ inv, int
     if (lane == 0) inv[item] = ss > 0.f ? (float)(1.0 / sqrt((double)ss)) : 0.f;
 }
 
-hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, hipStream_t st) {
+hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, unsigned long long *node_pack, long n_pack,
+                           const void *wo, void *wo16, long n_wo, hipStream_t st) {
     StageScope _stage(st, "inv_norm");
     const int n_items = p.kind == KIND_BLOCK ? p.N : p.F * p.N;
     const int n_sub = p.kind == KIND_BLOCK ? p.F : 1;
     const long sub = (long)p.N * p.C;
     const int blocks = cdiv(n_items, 4);
+    const long n8 = (wo && wo16 && p.bf16) ? n_wo / 8 : 0;
+    const int cvt_blocks = n8 > 0 ? (int)std::min<long>((n8 + 255) / 256, 1024) : 0;
     if (p.bf16)
-        k_inv_norm<uint16_t><<<blocks, 256, 0, st>>>((const uint16_t *)x, inv, n_items, n_sub, sub, p.C);
+        k_inv_norm<uint16_t><<<blocks + cvt_blocks, 256, 0, st>>>((const uint16_t *)x, inv, n_items, n_sub, sub, p.C,
+                                                                 blocks, node_pack, n_pack, (const uint4 *)wo, n8,
+                                                                 (uint4 *)wo16);
     else
-        k_inv_norm<float><<<blocks, 256, 0, st>>>((const float *)x, inv, n_items, n_sub, sub, p.C);
+        k_inv_norm<float><<<blocks, 256, 0, st>>>((const float *)x, inv, n_items, n_sub, sub, p.C, blocks, node_pack,
+                                                  n_pack, nullptr, 0, nullptr);
     return hipGetLastError();
 }
 
@@ -133,34 +73,34 @@ hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, hipStream_t
 // Block (candidate tile bt, representative tile at, group g), in an
 // XCD-aware order: t = dot(src_b, dst_a) * inv(dst_a); per candidate the
 // largest t over this block's representatives (smallest position on ties)
-// goes to part[at][g][b].  The representative norm is applied before the
-// arg-max, the candidate's own norm (a positive constant per row) after.
+// is merged into node_pack[g][b] with one 64-bit atomic maximum of the
+// packed pair, so the representative tiles need no second pass.  The
+// representative norm is applied before the arg-max, the candidate's own
+// norm (a positive constant per row) when unpacking.
 template <int BA, int BB, int WA, int WB>
 __global__ __launch_bounds__(256) void k_match_mfma(const uint16_t *__restrict__ x, const float *__restrict__ inv,
-                                                     const int32_t *__restrict__ src_ids,
-                                                     const int32_t *__restrict__ dst_ids, int G, int S, int D,
+                                                     GroupMap gm, int G, int S, int D,
                                                      int K, int seg_len, long sub_stride, long item_stride,
-                                                     int n_bt, int n_at, float *__restrict__ part_max,
-                                                     int32_t *__restrict__ part_idx) {
+                                                     int n_bt, int n_at,
+                                                     unsigned long long *__restrict__ node_pack) {
     using T = MfmaTile<BA, BB, WA, WB>;
     extern __shared__ __align__(16) uint16_t lds[];
     const int total = n_bt * n_at * G;
     const int lid = xcd_remap(blockIdx.x, total);
     // consecutive logical blocks: the representative tiles of one candidate tile
     const int at = lid % n_at, bt = (lid / n_at) % n_bt, g = lid / (n_at * n_bt);
-    const int32_t *src = src_ids + (long)g * S;
-    const int32_t *dst = dst_ids + (long)g * D;
+    const GroupMap::Grp gr = gm.group(g);
     const uint16_t *rowsA[T::CA], *rowsB[T::CB];
 #pragma unroll
     for (int i = 0; i < T::CA; ++i) {
         const int a = at * BA + T::chunk_row(i);
-        const int id = a < D ? dst[a] : -1;
+        const int id = a < D ? gm.dst_id(gr, a) : -1;
         rowsA[i] = id >= 0 ? x + (long)id * item_stride : nullptr;
     }
 #pragma unroll
     for (int i = 0; i < T::CB; ++i) {
         const int b = bt * BB + T::chunk_row(i);
-        const int id = b < S ? src[b] : -1;
+        const int id = b < S ? gm.src_id(gr, b) : -1;
         rowsB[i] = id >= 0 ? x + (long)id * item_stride : nullptr;
     }
     T tile;
@@ -172,7 +112,7 @@ __global__ __launch_bounds__(256) void k_match_mfma(const uint16_t *__restrict__
     int *si = reinterpret_cast<int *>(sv + WA * BB);
     for (int a = threadIdx.x; a < BA; a += 256) {
         const int ga = at * BA + a;
-        const int id = ga < D ? dst[ga] : -1;
+        const int id = ga < D ? gm.dst_id(gr, ga) : -1;
         sinv[a] = id >= 0 ? inv[id] : -1.f;
     }
     __syncthreads();
@@ -208,29 +148,25 @@ __global__ __launch_bounds__(256) void k_match_mfma(const uint16_t *__restrict__
         int ix = si[bl];
         for (int w = 1; w < WA; ++w) argmax_merge(v, ix, sv[w * BB + bl], si[w * BB + bl]);
         const int b = bt * BB + bl;
-        if (b < S) {
-            const long o = ((long)at * G + g) * S + b;
-            part_max[o] = v;
-            part_idx[o] = ix;
-        }
+        if (b < S && ix >= 0) atomicMax(&node_pack[(long)g * S + b], pack_argmax(v, ix));
     }
 }
 
 // fp32 similarity + arg-max (small fp32 layers): one thread per candidate.
-__global__ void k_match_f32(const float *__restrict__ x, const float *__restrict__ inv,
-                            const int32_t *__restrict__ src_ids, const int32_t *__restrict__ dst_ids, int G, int S,
+__global__ void k_match_f32(const float *__restrict__ x, const float *__restrict__ inv, GroupMap gm, int G, int S,
                             int D, int K, int seg_len, long sub_stride, long item_stride,
-                            float *__restrict__ part_max, int32_t *__restrict__ part_idx) {
+                            unsigned long long *__restrict__ node_pack) {
     const int g = blockIdx.y;
     const int b = blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= S) return;
-    const int sid = src_ids[(long)g * S + b];
+    const GroupMap::Grp gr = gm.group(g);
+    const int sid = gm.src_id(gr, b);
     float bv = -INFINITY;
     int bi = -1;
     if (sid >= 0) {
         const float *u = x + (long)sid * item_stride;
         for (int a = 0; a < D; ++a) {
-            const int did = dst_ids[(long)g * D + a];
+            const int did = gm.dst_id(gr, a);
             if (did < 0) continue;
             const float *v = x + (long)did * item_stride;
             float dot = 0.f;
@@ -242,82 +178,74 @@ __global__ void k_match_f32(const float *__restrict__ x, const float *__restrict
             argmax_merge(bv, bi, dot * inv[did], a);
         }
     }
-    part_max[(long)g * S + b] = bv;
-    part_idx[(long)g * S + b] = bi;
+    node_pack[(long)g * S + b] = bi >= 0 ? pack_argmax(bv, bi) : 0ull;
 }
 
-// Merge the rep-range partials in ascending order, convert the winning
-// position to a global id and apply the candidate's norm.
-__global__ void k_match_reduce(const float *__restrict__ part_max, const int32_t *__restrict__ part_idx,
-                               int n_split, int G, int S, int D, const float *__restrict__ inv,
-                               const int32_t *__restrict__ src_ids, const int32_t *__restrict__ dst_ids,
-                               float *__restrict__ node_max, int32_t *__restrict__ node_idx) {
+// Unpack the best pair, convert the winning position to a global id and
+// apply the candidate's norm.
+__global__ void k_match_unpack(const unsigned long long *__restrict__ node_pack, int G, int S,
+                               const float *__restrict__ inv, GroupMap gm, float *__restrict__ node_max,
+                               int32_t *__restrict__ node_idx) {
     const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (long)G * S) return;
     const int g = (int)(i / S);
-    const int sid = src_ids[i];
+    const GroupMap::Grp gr = gm.group(g);
+    const int sid = gm.src_id(gr, (int)(i - (long)g * S));
     if (sid < 0) {
         node_max[i] = -INFINITY;
         node_idx[i] = -1;
         return;
     }
-    float v = part_max[i];
-    int ix = part_idx[i];
-    for (int s = 1; s < n_split; ++s) argmax_merge(v, ix, part_max[(long)s * G * S + i], part_idx[(long)s * G * S + i]);
+    float v;
+    int ix;
+    unpack_argmax(node_pack[i], v, ix);
     node_max[i] = v * inv[sid];
-    node_idx[i] = ix >= 0 ? dst_ids[(long)g * D + ix] : -1;
+    node_idx[i] = ix >= 0 ? gm.dst_id(gr, ix) : -1;
 }
 
 template <int BA, int BB, int WA, int WB>
-static void go_match(const Plan &p, const uint16_t *x, const float *inv, const int32_t *src_ids,
-                     const int32_t *dst_ids, int K, int seg_len, long sub_stride, long item_stride, float *part_max,
-                     int32_t *part_idx, hipStream_t st) {
+static void go_match(const Plan &p, const uint16_t *x, const float *inv, const GroupMap &gm, int K, int seg_len,
+                     long sub_stride, long item_stride, unsigned long long *node_pack, hipStream_t st) {
     using T = MfmaTile<BA, BB, WA, WB>;
     const int G = p.n_groups, S = p.n_src_max, D = p.n_dst_max;
     const int n_bt = cdiv(S, BB), n_at = cdiv(D, BA);
     const size_t lds = T::LDS_BYTES;
-    k_match_mfma<BA, BB, WA, WB><<<n_bt * n_at * G, 256, lds, st>>>(x, inv, src_ids, dst_ids, G, S, D, K, seg_len,
-                                                                     sub_stride, item_stride, n_bt, n_at, part_max,
-                                                                     part_idx);
+    k_match_mfma<BA, BB, WA, WB><<<n_bt * n_at * G, 256, lds, st>>>(x, inv, gm, G, S, D, K, seg_len,
+                                                                     sub_stride, item_stride, n_bt, n_at, node_pack);
 }
 
-hipError_t launch_match(const Plan &p, const Layout &L, const void *x, const float *inv, const int32_t *src_ids,
-                        const int32_t *dst_ids, float *part_max, int32_t *part_idx, float *node_max,
-                        int32_t *node_idx, hipStream_t st) {
+hipError_t launch_match(const Plan &p, const void *x, const float *inv, const int32_t *units,
+                        unsigned long long *node_pack, float *node_max, int32_t *node_idx, hipStream_t st) {
+    const GroupMap gm = group_map(p, units);
     const int G = p.n_groups, S = p.n_src_max, D = p.n_dst_max;
     const bool block = p.kind == KIND_BLOCK;
     const int K = block ? p.F * p.C : p.C;
     const int seg_len = block ? p.C : 0;
     const long sub_stride = (long)p.N * p.C;
     const long item_stride = p.C;
-    const int n_split = match_split(p);
     {
         StageScope _stage(st, "match");
         if (p.bf16) {
             const uint16_t *xb = (const uint16_t *)x;
-            // representative tile height as in match_split(): 128, 64 or 32
+            // representative tile height by group size: 128, 64 or 32
             if (D > 64)
-                go_match<128, 64, 2, 2>(p, xb, inv, src_ids, dst_ids, K, seg_len, sub_stride, item_stride, part_max,
-                                        part_idx, st);
+                go_match<128, 64, 2, 2>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride, node_pack, st);
             else if (D > 32)
-                go_match<64, 64, 2, 2>(p, xb, inv, src_ids, dst_ids, K, seg_len, sub_stride, item_stride, part_max,
-                                       part_idx, st);
+                go_match<64, 64, 2, 2>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride, node_pack, st);
             else
-                go_match<32, 128, 1, 4>(p, xb, inv, src_ids, dst_ids, K, seg_len, sub_stride, item_stride, part_max,
-                                        part_idx, st);
+                go_match<32, 128, 1, 4>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride, node_pack, st);
         } else {
             dim3 grid(cdiv(S, 64), G);
-            k_match_f32<<<grid, 64, 0, st>>>((const float *)x, inv, src_ids, dst_ids, G, S, D, K, seg_len, sub_stride,
-                                             item_stride, part_max, part_idx);
+            k_match_f32<<<grid, 64, 0, st>>>((const float *)x, inv, gm, G, S, D, K, seg_len, sub_stride,
+                                             item_stride, node_pack);
         }
     }
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if (e != hipSuccess || node_max == nullptr) return e;   // no outputs: the selection unpacks node_pack
     const long n = (long)G * S;
     {
-        StageScope _stage(st, "match_reduce");
-        k_match_reduce<<<(unsigned)cdiv((int)n, 256), 256, 0, st>>>(part_max, part_idx, n_split, G, S, D, inv,
-                                                                     src_ids, dst_ids, node_max, node_idx);
+        StageScope _stage(st, "match_unpack");
+        k_match_unpack<<<(unsigned)cdiv((int)n, 256), 256, 0, st>>>(node_pack, G, S, inv, gm, node_max, node_idx);
     }
     return hipGetLastError();
 }

@@ -208,7 +208,7 @@ __global__ void k_to_f16(const uint4 *__restrict__ src, long n8, uint4 *__restri
 
 hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStream_t st) {
     const long n8 = (long)p.C * p.hd / 8;
-    {
+    if (!a.wo16_ready) {
         StageScope _stage(st, "wo_f16");
         const long blocks = (n8 + 255) / 256;
         k_to_f16<<<(unsigned)(blocks < 2048 ? blocks : 2048), 256, 0, st>>>((const uint4 *)a.wo, n8,

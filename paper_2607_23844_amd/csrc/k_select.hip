@@ -10,51 +10,108 @@
 #include "oc_internal.h"
 #include "oc_device.h"
 #include "oc_block.h"
+#include "oc_groups.h"
 #include <algorithm>
 
 namespace oc {
 
 constexpr int SEL_THREADS = 1024;
+constexpr int SEL_WAVES = SEL_THREADS / 64;
 constexpr int SEL_IPT = 16;            // candidates per thread: groups up to 16384
-constexpr int CMP_THREADS = 1024;
 
-__global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict__ node_max,
-                                                        const int32_t *__restrict__ node_idx,
-                                                        const int32_t *__restrict__ src_ids,
-                                                        const int32_t *__restrict__ dst_ids,
-                                                        const int32_t *__restrict__ grp_R, int S, int D,
-                                                        int32_t *__restrict__ flag, int32_t *__restrict__ mtok) {
-    __shared__ int hist[256];
+
+// One block per group.  PACKED: node_max / node_idx are unpacked from the
+// similarity kernel's packed arg-max (the candidate's inverse norm applied
+// last) and written out when node_max_out is given; otherwise they are read.
+// With kept_idx (one group per plain frame) the block then compacts its
+// frame: retained tokens in ascending id become rows [g*L, g*L+L), cached
+// ones go to cached_idx[g*Rc...] (Rc = the frame's static budget).
+template <bool PACKED>
+__global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict__ node_max_in,
+                                                        const int32_t *__restrict__ node_idx_in,
+                                                        const unsigned long long *__restrict__ node_pack,
+                                                        const float *__restrict__ inv,
+                                                        float *__restrict__ node_max_out,
+                                                        int32_t *__restrict__ node_idx_out, GroupMap gm, int G,
+                                                        int S, int D, int32_t *__restrict__ flag,
+                                                        int32_t *__restrict__ mtok, int32_t *__restrict__ kept_idx,
+                                                        int32_t *__restrict__ cached_idx,
+                                                        int32_t *__restrict__ rmap, int N, int L) {
+    // per-wave digit histograms, double-buffered across radix passes
+    __shared__ int hist[2][SEL_WAVES][256];
+    __shared__ uint32_t red[3][SEL_WAVES];
     __shared__ int sh[17];
-    __shared__ uint32_t shu[16];
     __shared__ int sel_info[2];
     const int g = blockIdx.x;
-    const int t = threadIdx.x;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int ipt = cdiv(S, SEL_THREADS);
-    const float *nm = node_max + (long)g * S;
-    const int32_t *src = src_ids + (long)g * S;
-    const int R = grp_R[g];
+    const GroupMap::Grp gr = gm.group(g);
+    const int R = gr.R;
 
     uint32_t key[SEL_IPT];
+    int32_t nid[SEL_IPT];
     uint32_t vmask = 0;
     int nvalid_local = 0;
     uint32_t lo = 0xFFFFFFFFu, hi = 0u;
 #pragma unroll
     for (int j = 0; j < SEL_IPT; ++j) {
         key[j] = 0;
+        nid[j] = -1;
         const int i = t * ipt + j;
-        if (j < ipt && i < S && src[i] >= 0) {
-            key[j] = float_key(nm[i]);
-            vmask |= 1u << j;
-            ++nvalid_local;
-            lo = min(lo, key[j]);
-            hi = max(hi, key[j]);
+        if (j >= ipt || i >= S) continue;
+        const long gi = (long)g * S + i;
+        const int sid = gm.src_id(gr, i);
+        if (sid < 0) {
+            if (PACKED && node_max_out != nullptr) {
+                node_max_out[gi] = -INFINITY;
+                node_idx_out[gi] = -1;
+            }
+            continue;
         }
+        float v;
+        if constexpr (PACKED) {
+            int ix;
+            unpack_argmax(node_pack[gi], v, ix);
+            v *= inv[sid];
+            nid[j] = ix >= 0 ? gm.dst_id(gr, ix) : -1;
+            if (node_max_out != nullptr) {
+                node_max_out[gi] = v;
+                node_idx_out[gi] = nid[j];
+            }
+        } else {
+            v = node_max_in[gi];
+            nid[j] = node_idx_in[gi];
+        }
+        key[j] = float_key(v);
+        vmask |= 1u << j;
+        ++nvalid_local;
+        lo = min(lo, key[j]);
+        hi = max(hi, key[j]);
     }
-    int n_valid;
-    (void)block_exclusive_scan(nvalid_local, sh, n_valid);
-    const uint32_t kmin = block_reduce_u32(lo, false, shu);
-    const uint32_t kmax = block_reduce_u32(hi, true, shu);
+    // valid count, smallest and largest key: one combined block reduction
+    uint32_t cnt = (uint32_t)nvalid_local;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        cnt += __shfl_xor(cnt, o, 64);
+        lo = min(lo, (uint32_t)__shfl_xor(lo, o, 64));
+        hi = max(hi, (uint32_t)__shfl_xor(hi, o, 64));
+    }
+    if (lane == 0) {
+        red[0][wave] = cnt;
+        red[1][wave] = lo;
+        red[2][wave] = hi;
+    }
+    // clear both histogram buffers meanwhile
+    for (int e = t; e < 2 * SEL_WAVES * 256; e += SEL_THREADS) (&hist[0][0][0])[e] = 0;
+    __syncthreads();
+    int n_valid = 0;
+    uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+#pragma unroll
+    for (int w = 0; w < SEL_WAVES; ++w) {
+        n_valid += (int)red[0][w];
+        kmin = min(kmin, red[1][w]);
+        kmax = max(kmax, red[2][w]);
+    }
 
     // threshold key tau (the R-th largest) and how many keys equal to tau are taken
     uint32_t tau = 0;
@@ -62,42 +119,42 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
     const bool none = R <= 0;
     const bool all = R >= n_valid;
     if (!none && !all) {
+        // keys share every bit above the highest bit where kmin and kmax
+        // differ (bit_hi = -1: all keys equal).  The mask is one 64-bit shift:
+        // a nested select here was compiled with the wrong condition.
         const uint32_t diff = kmin ^ kmax;
+        int bit_hi = diff == 0 ? -1 : 31 - __clz((int)diff);
+        uint32_t mask = (uint32_t)(0xFFFFFFFFull << (bit_hi + 1));
+        uint32_t prefix = kmax & mask;
         int remaining = R;
-        uint32_t prefix, mask;
-        int bit_hi;
-        if (diff == 0) {
-            prefix = kmax;
-            mask = 0xFFFFFFFFu;
-            bit_hi = -1;
-        } else {
-            const int top = 31 - __clz(diff);
-            mask = top == 31 ? 0u : ~((2u << top) - 1u);
-            prefix = kmax & mask;
-            bit_hi = top;
-        }
+        int buf = 0;
         while (bit_hi >= 0) {
             const int bit_lo = max(bit_hi - 7, 0);
             const int nbits = bit_hi - bit_lo + 1;
             const uint32_t dmask = (1u << nbits) - 1u;
-            if (t < 256) hist[t] = 0;
-            __syncthreads();
+            int *hw = hist[buf][wave];
 #pragma unroll
             for (int j = 0; j < SEL_IPT; ++j)
-                if (((vmask >> j) & 1u) && (key[j] & mask) == prefix) atomicAdd(&hist[(key[j] >> bit_lo) & dmask], 1);
+                if (((vmask >> j) & 1u) && (key[j] & mask) == prefix) atomicAdd(&hw[(key[j] >> bit_lo) & dmask], 1);
             __syncthreads();
             if (t < 64) {
                 // lane covers bins [4*t, 4*t+4); suffix sums from the top bin down
-                int c[4], s = 0;
+                int c[4], sum = 0;
 #pragma unroll
-                for (int q = 0; q < 4; ++q) { c[q] = hist[4 * t + q]; s += c[q]; }
-                int incl = s;   // inclusive suffix over lanes >= t
+                for (int q = 0; q < 4; ++q) {
+                    int cq = 0;
+#pragma unroll
+                    for (int w = 0; w < SEL_WAVES; ++w) cq += hist[buf][w][4 * t + q];
+                    c[q] = cq;
+                    sum += cq;
+                }
+                int incl = sum;   // inclusive suffix over lanes >= t
 #pragma unroll
                 for (int o = 1; o < 64; o <<= 1) {
                     const int y = __shfl_down(incl, o, 64);
                     if (t + o < 64) incl += y;
                 }
-                int above = incl - s;   // count in bins above this lane's bins
+                int above = incl - sum;   // count in bins above this lane's bins
 #pragma unroll
                 for (int q = 3; q >= 0; --q) {
                     if (above < remaining && remaining <= above + c[q]) {
@@ -107,13 +164,15 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
                     above += c[q];
                 }
             }
+            // the other buffer, used by the next pass, was last read a pass ago
+            for (int e = t; e < SEL_WAVES * 256; e += SEL_THREADS) (&hist[buf ^ 1][0][0])[e] = 0;
             __syncthreads();
             const int sel = sel_info[0];
             remaining -= sel_info[1];
             prefix |= (uint32_t)sel << bit_lo;
             mask |= dmask << bit_lo;
             bit_hi = bit_lo - 1;
-            __syncthreads();
+            buf ^= 1;
         }
         tau = prefix;
         need = remaining;
@@ -126,6 +185,10 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
         if (((vmask >> j) & 1u) && key[j] == tau) ++eq_local;
     int eq_total;
     int eq_rank = block_exclusive_scan((!none && !all) ? eq_local : 0, sh, eq_total);
+    // frame compaction (kept_idx given): flags of the frame's N tokens in LDS
+    __shared__ uint8_t fl[SEL_COMPACT_MAX_N];
+    const bool compact = kept_idx != nullptr;
+    const long fbase = (long)g * N;
 #pragma unroll
     for (int j = 0; j < SEL_IPT; ++j) {
         if (!((vmask >> j) & 1u)) continue;
@@ -136,24 +199,72 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
         else if (key[j] > tau) c = true;
         else if (key[j] == tau) { c = eq_rank < need; ++eq_rank; }
         else c = false;
-        const int id = src[i];
+        const int id = gm.src_id(gr, i);
         flag[id] = c ? 1 : 0;
-        mtok[id] = c ? node_idx[(long)g * S + i] : -1;
+        mtok[id] = c ? nid[j] : -1;
+        if (compact) fl[id - fbase] = c ? 1 : 0;
     }
-    const int32_t *dst = dst_ids + (long)g * D;
     for (int i = t; i < D; i += SEL_THREADS) {
-        const int id = dst[i];
-        if (id >= 0) { flag[id] = 0; mtok[id] = -1; }
+        const int id = gm.dst_id(gr, i);
+        if (id >= 0) {
+            flag[id] = 0;
+            mtok[id] = -1;
+            if (compact) fl[id - fbase] = 0;
+        }
+    }
+    if (!compact) return;
+    __syncthreads();
+    // one scan over the frame's tokens in id order gives both ranks: kept
+    // count in the low 16 bits, cached count in the high 16 (N < 32768)
+    const int cpt = cdiv(N, SEL_THREADS), p0 = t * cpt;
+    int packed = 0;
+    for (int j = 0; j < cpt; ++j) {
+        const int n = p0 + j;
+        if (n < N) packed += fl[n] ? (1 << 16) : 1;
+    }
+    int tot;
+    const int pre = block_exclusive_scan(packed, sh, tot);
+    int krank = pre & 0xFFFF, crank = pre >> 16;
+    const int n_c = gr.R;   // every frame caches exactly its budget
+    for (int j = 0; j < cpt; ++j) {
+        const int n = p0 + j;
+        if (n >= N) break;
+        const int pid = (int)(fbase + n);
+        if (fl[n]) {
+            if (crank < n_c) cached_idx[(long)g * n_c + crank] = pid;
+            rmap[pid] = -1;
+            ++crank;
+        } else {
+            const int row = g * L + krank;
+            if (krank < L) kept_idx[row] = pid;
+            rmap[pid] = krank < L ? row : -2;
+            ++krank;
+        }
     }
 }
 
-hipError_t launch_select(const Plan &p, const float *node_max, const int32_t *node_idx, const int32_t *src_ids,
-                         const int32_t *dst_ids, const int32_t *grp_R, int32_t *flag, int32_t *mtok,
-                         hipStream_t st) {
+hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_max, const int32_t *node_idx,
+                         int32_t *flag, int32_t *mtok, hipStream_t st) {
     {
         StageScope _stage(st, "select");
-        k_select<<<p.n_groups, SEL_THREADS, 0, st>>>(node_max, node_idx, src_ids, dst_ids, grp_R, p.n_src_max,
-                                                     p.n_dst_max, flag, mtok);
+        k_select<false><<<p.n_groups, SEL_THREADS, 0, st>>>(node_max, node_idx, nullptr, nullptr, nullptr, nullptr,
+                                                            group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max,
+                                                            flag, mtok, nullptr, nullptr, nullptr, p.N, p.seq_len);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_select_packed(const Plan &p, const int32_t *units, const unsigned long long *node_pack,
+                                const float *inv, float *node_max, int32_t *node_idx, int32_t *flag, int32_t *mtok,
+                                int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap, hipStream_t st) {
+    const bool compact = kept_idx != nullptr;
+    if (compact && !select_compacts(p)) return hipErrorInvalidValue;
+    {
+        StageScope _stage(st, "select");
+        k_select<true><<<p.n_groups, SEL_THREADS, 0, st>>>(nullptr, nullptr, node_pack, inv, node_max, node_idx,
+                                                           group_map(p, units), p.n_groups, p.n_src_max,
+                                                           p.n_dst_max, flag, mtok, kept_idx, cached_idx, rmap, p.N,
+                                                           p.seq_len);
     }
     return hipGetLastError();
 }

@@ -163,16 +163,10 @@ Layout make_layout(const Plan &p) {
     auto take = [&o](size_t bytes) { const size_t at = o; o += al(bytes); return at; };
     const size_t FN = (size_t)p.F * p.N;
     const size_t GS = (size_t)p.n_groups * p.n_src_max;
-    const int ns = match_split(p);
     L.inv = take(FN * 4);
-    L.part_max = take(ns * GS * 4);
-    L.part_idx = take(ns * GS * 4);
+    L.node_pack = take(GS * 8);
     L.node_max = take(GS * 4);
     L.node_idx = take(GS * 4);
-    // group lists sized for the largest group shape of this granularity
-    L.src_ids = take(GS * 4);
-    L.dst_ids = take((size_t)p.n_groups * p.n_dst_max * 4);
-    L.grp_R = take((size_t)p.n_groups * 4);
     const bool frames = p.gran == OC_GRAN_FRAME || p.gran == OC_GRAN_FRAME_TOKEN;
     L.gram_part = take(frames ? (size_t)gram_blocks(p) * 1024 * 4 : 0);
     L.fsim = take(frames ? 1024 * 8 : 0);
@@ -229,10 +223,16 @@ oc_status check_ws(void *ws, size_t ws_bytes, size_t need) {
 
 template <typename T> T *at(void *ws, size_t off) { return reinterpret_cast<T *>((char *)ws + off); }
 
-// match stage into (node_max, node_idx); leaves group ids, frame stage and
-// norms in ws
-oc_status run_match(const Plan &p, const Layout &L, const void *x, float *node_max, int32_t *node_idx, void *ws,
-                    hipStream_t st) {
+const int32_t *units_of(const Plan &p, const Layout &L, void *ws) {
+    return p.gran == OC_GRAN_FRAME_TOKEN ? at<int32_t>(ws, L.units) : nullptr;
+}
+
+// Match stage.  With reduce, (node_max, node_idx) are produced; without,
+// only the packed arg-max is left in ws for launch_select_packed (frame
+// granularity always produces node_max / node_idx).  Leaves the frame stage
+// and norms in ws; wo / wo16, when given, are converted in the norm launch.
+oc_status run_match(const Plan &p, const Layout &L, const void *x, float *node_max, int32_t *node_idx, bool reduce,
+                    void *ws, hipStream_t st, const void *wo = nullptr, void *wo16 = nullptr) {
     char *w = (char *)ws;
     const bool frames = p.gran == OC_GRAN_FRAME || p.gran == OC_GRAN_FRAME_TOKEN;
     if (frames) {
@@ -240,22 +240,38 @@ oc_status run_match(const Plan &p, const Layout &L, const void *x, float *node_m
         int32_t *fi = p.gran == OC_GRAN_FRAME ? node_idx : at<int32_t>(ws, L.fidx);
         HIP_TRY(launch_frame_stage(p, L, x, w, fm, fi, st), "frame stage");
     }
-    const int32_t *units = p.gran == OC_GRAN_FRAME_TOKEN ? at<int32_t>(ws, L.units) : nullptr;
-    HIP_TRY(launch_group_ids(p, units, at<int32_t>(ws, L.src_ids), at<int32_t>(ws, L.dst_ids),
-                             at<int32_t>(ws, L.grp_R), st), "group ids");
     if (p.kind == KIND_FRAME) return OC_OK;
-    HIP_TRY(launch_inv_norm(p, x, at<float>(ws, L.inv), st), "inv_norm");
-    HIP_TRY(launch_match(p, L, x, at<float>(ws, L.inv), at<int32_t>(ws, L.src_ids), at<int32_t>(ws, L.dst_ids),
-                         at<float>(ws, L.part_max), at<int32_t>(ws, L.part_idx), node_max, node_idx, st),
+    unsigned long long *pack = at<unsigned long long>(ws, L.node_pack);
+    HIP_TRY(launch_inv_norm(p, x, at<float>(ws, L.inv), pack, (long)p.n_groups * p.n_src_max, wo, wo16,
+                            (long)p.C * p.hd, st), "inv_norm");
+    HIP_TRY(launch_match(p, x, at<float>(ws, L.inv), units_of(p, L, ws), pack, reduce ? node_max : nullptr,
+                         reduce ? node_idx : nullptr, st),
             "match");
     return OC_OK;
 }
 
-oc_status run_select(const Plan &p, const Layout &L, const float *node_max, const int32_t *node_idx,
+// Selection and compaction.  from_pack: unpack the similarity arg-max in
+// the selection kernel (writing node_max / node_idx too), and compact there
+// as well when every frame is one group.
+oc_status run_select(const Plan &p, const Layout &L, float *node_max, int32_t *node_idx, bool from_pack,
                      int32_t *kept, int32_t *cached, int32_t *rmap, int map_matched, void *ws, hipStream_t st) {
-    HIP_TRY(launch_select(p, node_max, node_idx, at<int32_t>(ws, L.src_ids), at<int32_t>(ws, L.dst_ids),
-                          at<int32_t>(ws, L.grp_R), at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok), st),
-            "select");
+    const int32_t *units = units_of(p, L, ws);
+    if (from_pack && p.kind != KIND_FRAME) {
+        const bool fused = select_compacts(p);
+        HIP_TRY(launch_select_packed(p, units, at<unsigned long long>(ws, L.node_pack), at<float>(ws, L.inv),
+                                     node_max, node_idx, at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok),
+                                     fused ? kept : nullptr, fused ? cached : nullptr, fused ? rmap : nullptr, st),
+                "select");
+        if (fused) {
+            if (map_matched)
+                HIP_TRY(launch_map_matched(p, at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok), rmap, st),
+                        "map matched");
+            return OC_OK;
+        }
+    } else {
+        HIP_TRY(launch_select(p, units, node_max, node_idx, at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok), st),
+                "select");
+    }
     HIP_TRY(launch_compact(p, at<int32_t>(ws, L.units), at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok),
                            at<int32_t>(ws, L.fcnt), kept, cached, rmap, map_matched, st),
             "compact");
@@ -331,7 +347,7 @@ oc_status oc_match(const oc_shape *shape, const oc_cfg *cfg, const void *x, floa
     if (!aligned16(x)) return fail(OC_ERR_INVALID_ARG, "x must be 16-byte aligned");
     const Layout L = make_layout(p);
     if ((s = check_ws(ws, ws_bytes, workspace_for(shape, cfg))) != OC_OK) return s;
-    if ((s = run_match(p, L, x, node_max, node_idx, ws, stream)) != OC_OK) return s;
+    if ((s = run_match(p, L, x, node_max, node_idx, true, ws, stream)) != OC_OK) return s;
     if (frames && p.gran == OC_GRAN_FRAME_TOKEN) {
         if ((s = copy_d2d(frames->frame_max, at<float>(ws, L.fmax), (size_t)p.n_fsrc * 4, stream)) != OC_OK) return s;
         if ((s = copy_d2d(frames->frame_idx, at<int32_t>(ws, L.fidx), (size_t)p.n_fsrc * 4, stream)) != OC_OK) return s;
@@ -351,11 +367,9 @@ oc_status oc_select(const oc_shape *shape, const oc_cfg *cfg, const float *node_
     if (map_matched != 0 && map_matched != 1) return fail(OC_ERR_INVALID_ARG, "map_matched must be 0 or 1");
     const Layout L = make_layout(p);
     if ((s = check_ws(ws, ws_bytes, workspace_for(shape, cfg))) != OC_OK) return s;
-    // group lists (FRAME_TOKEN: from the unit table oc_match left in ws)
-    const int32_t *units = p.gran == OC_GRAN_FRAME_TOKEN ? at<int32_t>(ws, L.units) : nullptr;
-    HIP_TRY(launch_group_ids(p, units, at<int32_t>(ws, L.src_ids), at<int32_t>(ws, L.dst_ids),
-                             at<int32_t>(ws, L.grp_R), stream), "group ids");
-    if ((s = run_select(p, L, node_max, node_idx, kept_idx, cached_idx, restore_map, map_matched, ws, stream)) != OC_OK)
+    // FRAME_TOKEN groups follow the unit table oc_match left in ws
+    if ((s = run_select(p, L, const_cast<float *>(node_max), const_cast<int32_t *>(node_idx), false, kept_idx,
+                        cached_idx, restore_map, map_matched, ws, stream)) != OC_OK)
         return s;
     return ok();
 }
@@ -447,11 +461,15 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
 
     float *nm = at<float>(ws, L.node_max);
     int32_t *ni = at<int32_t>(ws, L.node_idx);
-    if ((s = run_match(p, L, x, nm, ni, ws, stream)) != OC_OK) return s;
-    int32_t *kept = at<int32_t>(ws, L.kept), *cached = at<int32_t>(ws, L.cached), *rmap = at<int32_t>(ws, L.rmap);
-    if ((s = run_select(p, L, nm, ni, kept, cached, rmap, map_matched, ws, stream)) != OC_OK) return s;
-
     const AttnWs aw = attn_ws(p, p.n_seq, p.seq_len, L.attn);
+    // bf16 layers: the fp16 copy of wo is made in the norm launch of the match stage
+    const bool wo_early = p.bf16 && p.kind != KIND_FRAME;
+    if ((s = run_match(p, L, x, nm, ni, false, ws, stream, wo_early ? w->wo : nullptr,
+                       wo_early ? at<char>(ws, aw.wo16) : nullptr)) != OC_OK)
+        return s;
+    int32_t *kept = at<int32_t>(ws, L.kept), *cached = at<int32_t>(ws, L.cached), *rmap = at<int32_t>(ws, L.rmap);
+    if ((s = run_select(p, L, nm, ni, true, kept, cached, rmap, map_matched, ws, stream)) != OC_OK) return s;
+
     AttnArgs a;
     std::memset(&a, 0, sizeof(a));
     a.x = x; a.row_idx = kept; a.n_main = p.n_kept;
@@ -462,6 +480,7 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
     a.q = at<char>(ws, aw.q); a.k = at<char>(ws, aw.k); a.o = at<char>(ws, aw.o); a.vt = at<char>(ws, aw.v);
     a.lpad = aw.lpad;
     a.wo16 = at<char>(ws, aw.wo16);
+    a.wo16_ready = wo_early ? 1 : 0;
     HIP_TRY(launch_attention(p, a, stream), "attention");
     if (map_matched) HIP_TRY(launch_copy_matched(p, cached, p.n_cached, rmap, kept, cache->y, stream), "copy matched");
 
@@ -500,17 +519,22 @@ oc_status oc_attn_full(const oc_shape *shape, const oc_cfg *cfg, const void *x, 
     if ((s = check_ws(ws, ws_bytes, workspace_for(shape, cfg))) != OC_OK) return s;
     int32_t *flag = at<int32_t>(ws, L.flag);
     int32_t *kept = at<int32_t>(ws, L.kept), *cached = at<int32_t>(ws, L.cached), *rmap = at<int32_t>(ws, L.rmap);
-    HIP_TRY(launch_fill_i32(flag, (long)p.F * p.N, 0, stream), "fill");
-    HIP_TRY(launch_compact(p, nullptr, flag, at<int32_t>(ws, L.mtok), at<int32_t>(ws, L.fcnt), kept, cached, rmap, 0,
-                           stream), "compact");
+    // spatial layers keep every token in place (the identity row map needs
+    // no index list); temporal layers gather one sequence per position
+    const bool identity = p.kind == KIND_TOKEN;
+    if (!identity) {
+        HIP_TRY(launch_fill_i32(flag, (long)p.F * p.N, 0, stream), "fill");
+        HIP_TRY(launch_compact(p, nullptr, flag, at<int32_t>(ws, L.mtok), at<int32_t>(ws, L.fcnt), kept, cached,
+                               rmap, 0, stream), "compact");
+    }
     const AttnWs aw = attn_ws(p, p.n_seq, p.seq_len, L.attn);
     AttnArgs a;
     std::memset(&a, 0, sizeof(a));
-    a.x = x; a.row_idx = kept; a.n_main = p.n_kept;
+    a.x = x; a.row_idx = identity ? nullptr : kept; a.n_main = p.n_kept;
     a.ctx = shape->n_ctx > 0 ? ctx : nullptr; a.n_ctx = shape->n_ctx;
     a.n_seq = p.n_seq; a.L = p.seq_len;
     a.wq = w->wq; a.wk = w->wk; a.wv = w->wv; a.wo = w->wo;
-    a.y = y; a.out_idx = kept; a.y_ctx = y_ctx;
+    a.y = y; a.out_idx = identity ? nullptr : kept; a.y_ctx = y_ctx;
     a.q = at<char>(ws, aw.q); a.k = at<char>(ws, aw.k); a.o = at<char>(ws, aw.o); a.vt = at<char>(ws, aw.v);
     a.lpad = aw.lpad;
     a.wo16 = at<char>(ws, aw.wo16);

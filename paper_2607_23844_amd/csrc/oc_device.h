@@ -55,6 +55,27 @@ __device__ __forceinline__ uint32_t float_key(float f) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Inverse of float_key (-0 comes back as +0).
+__device__ __forceinline__ float key_float(uint32_t k) {
+    return __uint_as_float((k & 0x80000000u) ? (k ^ 0x80000000u) : ~k);
+}
+
+// (value, index) packed into 64 bits so that the unsigned maximum is the
+// arg-max with the smallest index on ties: order-preserving value key high,
+// inverted index low.  0 is below every packed pair and means "none".
+__device__ __forceinline__ unsigned long long pack_argmax(float v, int i) {
+    return ((unsigned long long)float_key(v) << 32) | (unsigned long long)(~(uint32_t)i);
+}
+__device__ __forceinline__ void unpack_argmax(unsigned long long p, float &v, int &i) {
+    if (p == 0ull) {
+        v = -INFINITY;
+        i = -1;
+        return;
+    }
+    v = key_float((uint32_t)(p >> 32));
+    i = (int)~(uint32_t)p;
+}
+
 __host__ __device__ __forceinline__ int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace oc

@@ -34,7 +34,7 @@ struct Plan {
 
 // Workspace carve-up (byte offsets from the caller's ws base).
 struct Layout {
-    size_t inv, part_max, part_idx, node_max, node_idx, src_ids, dst_ids, grp_R;
+    size_t inv, node_pack, node_max, node_idx;
     size_t gram_part, fsim, fmax, fidx, forder, pairs, units;
     size_t flag, mtok, fcnt, kept, cached, rmap;
     size_t attn;             // start of the attention workspace (Q, K, O, V)
@@ -47,15 +47,6 @@ struct AttnWs { size_t q, k, o, v, wo16, bytes; int lpad; };
 AttnWs attn_ws(const Plan &p, int n_seq, int L, size_t base);
 int gram_blocks(const Plan &p);
 
-// Representative-range splits of the similarity GEMM (its tile height in
-// representatives is 128, 64 or 32 by group size; bf16 only).
-inline int match_split(const Plan &p) {
-    if (!p.bf16) return 1;
-    const int D = p.n_dst_max;
-    const int BA = D > 64 ? 128 : (D > 32 ? 64 : 32);
-    return (D + BA - 1) / BA;
-}
-
 // Stage timing: when a timer is attached to the calling thread, the kernels
 // launched between stage_begin and stage_end are bracketed by HIP events on
 // the launch stream (oc_timer.cpp).
@@ -67,21 +58,41 @@ struct StageScope {
 };
 
 // ---- launchers (k_*.hip) ---------------------------------------------------
-// group id lists: src_ids [G, S] / dst_ids [G, D] (-1 padded), grp_R [G]
-hipError_t launch_group_ids(const Plan &p, const int32_t *units, int32_t *src_ids, int32_t *dst_ids,
-                            int32_t *grp_R, hipStream_t st);
-hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, hipStream_t st);
-hipError_t launch_match(const Plan &p, const Layout &L, const void *x, const float *inv,
-                        const int32_t *src_ids, const int32_t *dst_ids, float *part_max,
-                        int32_t *part_idx, float *node_max, int32_t *node_idx, hipStream_t st);
+// Group members are computed from the plan (GroupMap, oc_groups.h); units is
+// the frame-token unit table in the workspace (nullptr for other kinds).
+// node_pack [G, S] holds each candidate's best (similarity, representative
+// position) packed for a 64-bit atomic maximum (pack_argmax).
+// launch_inv_norm also clears node_pack (n_pack entries) and, with wo / wo16
+// given, converts the output-projection weights wo (bf16, n_wo elements) to
+// fp16 into wo16, all in one launch.
+hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, unsigned long long *node_pack, long n_pack,
+                           const void *wo, void *wo16, long n_wo, hipStream_t st);
+// node_max == nullptr: node_pack only (the selection unpacks it)
+hipError_t launch_match(const Plan &p, const void *x, const float *inv, const int32_t *units,
+                        unsigned long long *node_pack, float *node_max, int32_t *node_idx, hipStream_t st);
 hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, char *ws,
                               float *node_max, int32_t *node_idx, hipStream_t st);
-hipError_t launch_select(const Plan &p, const float *node_max, const int32_t *node_idx,
-                         const int32_t *src_ids, const int32_t *dst_ids, const int32_t *grp_R,
+hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_max, const int32_t *node_idx,
                          int32_t *flag, int32_t *mtok, hipStream_t st);
+// selection straight from node_pack; node_max / node_idx are written as
+// well when non-null.  With kept_idx given (plain frames, patch_k == 1: one
+// group per frame) the same launch also compacts the frame into kept_idx,
+// cached_idx and rmap, as launch_compact would.
+hipError_t launch_select_packed(const Plan &p, const int32_t *units, const unsigned long long *node_pack,
+                                const float *inv, float *node_max, int32_t *node_idx, int32_t *flag, int32_t *mtok,
+                                int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap, hipStream_t st);
+// whether launch_select_packed can compact in the same launch (the frame's
+// flags are staged in LDS: N below SEL_COMPACT_MAX_N)
+constexpr int SEL_COMPACT_MAX_N = 24576;
+inline bool select_compacts(const Plan &p) {
+    return p.kind == KIND_TOKEN && p.gran != 3 && p.k == 1 && p.N < SEL_COMPACT_MAX_N;
+}
 hipError_t launch_compact(const Plan &p, const int32_t *units, const int32_t *flag, const int32_t *mtok,
                           int32_t *fcnt, int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap,
                           int map_matched, hipStream_t st);
+// cold "matched" restore map: cached positions point at their matched row
+hipError_t launch_map_matched(const Plan &p, const int32_t *flag, const int32_t *mtok, int32_t *rmap,
+                              hipStream_t st);
 hipError_t launch_gather(const Plan &p, const void *x, const int32_t *kept_idx, int n_rows, void *x_kept,
                          hipStream_t st);
 hipError_t launch_restore(const Plan &p, const void *y_kept, int n_rows, const int32_t *rmap,
@@ -103,6 +114,7 @@ struct AttnArgs {
     void *y_ctx;
     void *q, *k, *vt, *o;             // workspace
     void *wo16;                       // workspace: wo converted to fp16 (bf16 layers)
+    int wo16_ready;                   // wo16 already converted by an earlier launch of this call
     int lpad;                         // padded keys per sequence in vt
 };
 hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st);
