@@ -45,12 +45,6 @@ typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 constexpr float REBASE = 8.f;   // P = exp2(s - m) stays below 2^REBASE on the fast path
 
-typedef __attribute__((address_space(3))) void *lds_vp;
-typedef __attribute__((address_space(1))) void *glb_vp;
-
-// s_waitcnt vmcnt(n) leaving the other counters alone (gfx9 encoding)
-#define OC_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8))
-
 template <int DH, bool DMA>
 struct FlashCfg {
     static constexpr int DK = (DH + 15) / 16 * 16;   // S^T k-loop (16 per MFMA)
@@ -249,7 +243,7 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
         // first MFMA then never waits on the loads a previous tile left in flight
         OC_WAIT_VMCNT(0);
     }
-    __syncthreads();
+    if constexpr (DMA) barrier_lds(); else __syncthreads();
     read_k(0);
 
     const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
@@ -364,14 +358,18 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
                 o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[db][k4], pf[k4], o[db], 0, 0, 0);
         // DMA: this wave's part of tile kt+2 must have landed before the
         // barrier that publishes it (only tile kt+3 may still be in flight)
-        if (DMA && kt + 2 < n_kt) {
-            if (kt + 3 < n_kt) {
-                OC_WAIT_VMCNT(IPT);
-            } else {
-                OC_WAIT_VMCNT(0);
+        if constexpr (DMA) {
+            if (kt + 2 < n_kt) {
+                if (kt + 3 < n_kt) {
+                    OC_WAIT_VMCNT(IPT);
+                } else {
+                    OC_WAIT_VMCNT(0);
+                }
             }
+            barrier_lds();
+        } else {
+            __syncthreads();
         }
-        __syncthreads();
         b0 = b1;
     }
     // normalise and store: lane holds query ln, d = db*32 + 8*g4 + 4*lg + e

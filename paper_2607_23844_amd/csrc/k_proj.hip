@@ -1,4 +1,4 @@
-// Projections of the reduced attention layer on the MFMA tile engine.
+// Projections of the reduced attention layer on the MFMA tile engines.
 //
 // x, weights and y are bf16; products of bf16 inputs are exact and
 // accumulate in fp32.  The attention intermediates Q, K, V and O are stored
@@ -14,20 +14,24 @@
 // Rows r < n_main come from x (through row_idx when given); rows after them
 // are the uncached context tokens of a single sequence.
 //
+// Engines: the V and output projections use the LDS-DMA tile (128 x 64)
+// when their K is a multiple of 64, the register-staged tile (128 x 128)
+// otherwise; the Q/K projection uses the register-staged tile (measured
+// faster at its shape).  Epilogues go through LDS: the tile is staged as
+// whole output rows and written in 16-byte chunks, so every store is a
+// contiguous run of a row (Vt rows included).
+//
 // Tile order: blocks are remapped so that each XCD runs a contiguous range
 // of logical tiles, and logical tiles are grouped GA weight tiles wide, so
 // one XCD's L2 sees a few weight tiles and a few token tiles instead of all.
 #include "oc_internal.h"
 #include "oc_device.h"
 #include "oc_mfma_tile.h"
+#include "oc_dma_tile.h"
 #include "oc_attn_common.h"
 
 namespace oc {
 
-constexpr int PBA = 128, PBB = 128;
-using PTile = MfmaTile<PBA, PBB, 2, 2>;
-// output projection: O rows and wo (converted once per call) are fp16
-using OTile = MfmaTile<PBA, PBB, 2, 2, true, false>;
 constexpr int GA = 6;
 
 // logical tile lid -> (a tile, b tile), GA a-tiles per group, b fastest inside
@@ -39,101 +43,164 @@ __device__ __forceinline__ void tile_order(int lid, int n_at, int n_bt, int &at,
     bt = idx / ga;
 }
 
-// a in [0, 2*hd): rows of wq then wk; b = batch rows.  Q/K[b][a % hd].
-__global__ __launch_bounds__(256) void k_proj_qk(RowMap rm, const uint16_t *__restrict__ wq,
-                                                 const uint16_t *__restrict__ wk, int hd, float qscale, int n_at,
-                                                 int n_bt, uint16_t *__restrict__ Q, uint16_t *__restrict__ K) {
-    extern __shared__ __align__(16) uint16_t lds[];
-    int at, bt;
-    tile_order(xcd_remap(blockIdx.x, n_at * n_bt), n_at, n_bt, at, bt);
-    const uint16_t *rowsA[PTile::CA], *rowsB[PTile::CB];
+// Stage the block's results as rows of b with the a values contiguous:
+// S[b][col(a)], row stride BA + 8 halves.  cvt(value, a) gives the 16-bit
+// pattern of element (a, b); col maps an aligned quad of a to an aligned
+// quad of columns.
+template <int BA, typename T, typename Cvt, typename Col>
+__device__ __forceinline__ void stage_rows(const T &t, uint16_t *S, Cvt cvt, Col col) {
+    constexpr int SROW = BA + 8;
 #pragma unroll
-    for (int i = 0; i < PTile::CA; ++i) {
-        const int a = at * PBA + PTile::chunk_row(i);
-        rowsA[i] = a < hd ? wq + (long)a * rm.C : (a < 2 * hd ? wk + (long)(a - hd) * rm.C : nullptr);
-    }
+    for (int j = 0; j < T::TB; ++j) {
+        const int b = T::b_of(j);
 #pragma unroll
-    for (int i = 0; i < PTile::CB; ++i) rowsB[i] = rm.row(bt * PBB + PTile::chunk_row(i));
-    PTile t;
-    t.run(lds, rowsA, rowsB, rm.C, 0, 0);
-#pragma unroll
-    for (int j = 0; j < PTile::TB; ++j) {
-        const int b = bt * PBB + PTile::b_of(j);
-        if (b >= rm.n_rows) continue;
-#pragma unroll
-        for (int i = 0; i < PTile::TA; ++i)
+        for (int i = 0; i < T::TA; ++i)
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                const int a = at * PBA + PTile::a_of(i, g);
-                if (a >= 2 * hd) continue;
-                const bool isq = a < hd;
-                uint16_t *dst = isq ? Q + (long)b * hd + a : K + (long)b * hd + (a - hd);
-                const float sc = isq ? qscale : 1.f;
+                const int a = T::a_of(i, g);
                 u16x4 v;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] = f2h_bits(t.acc[i][j][4 * g + e] * sc);
-                *reinterpret_cast<u16x4 *>(dst) = v;
+                for (int e = 0; e < 4; ++e) v[e] = cvt(t.acc[i][j][4 * g + e], a + e);
+                *reinterpret_cast<u16x4 *>(S + b * SROW + col(a)) = v;
             }
     }
 }
 
-// a = batch rows, b in [0, hd): rows of wv.  Vt[h][s][d][j].  A lane holds
-// four consecutive rows of one feature: one 8-byte store when they are
-// consecutive positions of one sequence.
-__global__ __launch_bounds__(256) void k_proj_v(RowMap rm, const uint16_t *__restrict__ wv, int hd, int dh,
-                                                int n_seq, int L, int lpad, int n_at, int n_bt, int zero_pad,
-                                                uint16_t *__restrict__ Vt) {
+// Write the staged rows in 16-byte chunks: chunk (b, c0) (columns c0..c0+7,
+// c0 < ncol) goes to dst(b, c0); nullptr skips it.
+template <int BA, int BB, typename Dst>
+__device__ __forceinline__ void write_rows(const uint16_t *S, int ncol, Dst dst) {
+    constexpr int SROW = BA + 8, CPR = BA / 8;
+    for (int c = threadIdx.x; c < BB * CPR; c += 256) {
+        const int b = c / CPR, c0 = (c - b * CPR) * 8;
+        if (c0 >= ncol) continue;
+        uint16_t *d = dst(b, c0);
+        if (d != nullptr) *reinterpret_cast<uint4 *>(d) = *reinterpret_cast<const uint4 *>(S + b * SROW + c0);
+    }
+}
+
+struct RegRows { static constexpr bool dma = false; };
+struct DmaRows { static constexpr bool dma = true; };
+template <typename T, typename Rows>
+__device__ __forceinline__ void run_tile(T &t, uint16_t *lds, const uint16_t *const *rowsA,
+                                         const uint16_t *const *rowsB, const uint16_t *fbA, const uint16_t *fbB, int K,
+                                         Rows) {
+    if constexpr (Rows::dma) t.run(lds, rowsA, rowsB, fbA, fbB, K, 0, 0);
+    else t.run(lds, rowsA, rowsB, K, 0, 0);
+}
+
+template <typename KernelPtr>
+static hipError_t allow_lds(KernelPtr k, size_t bytes, bool &done) {
+    if (done || bytes <= 65536) return hipSuccess;
+    const hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e == hipSuccess) done = true;
+    return e;
+}
+
+// ---------------------------------------------------------------------------
+// Q, K: a in [0, 2*hd) are rows of wq then wk; b = batch rows.
+// ---------------------------------------------------------------------------
+using QKTile = MfmaTile<128, 128, 2, 2>;
+
+__global__ __launch_bounds__(256) void k_proj_qk(RowMap rm, const uint16_t *__restrict__ wq,
+                                                 const uint16_t *__restrict__ wk, int hd, float qscale, int n_at,
+                                                 int n_bt, uint16_t *__restrict__ Q, uint16_t *__restrict__ K) {
+    using T = QKTile;
+    constexpr int BA = 128, BB = 128;
     extern __shared__ __align__(16) uint16_t lds[];
     int at, bt;
     tile_order(xcd_remap(blockIdx.x, n_at * n_bt), n_at, n_bt, at, bt);
-    const uint16_t *rowsA[PTile::CA], *rowsB[PTile::CB];
+    const uint16_t *rowsA[T::CA], *rowsB[T::CB];
 #pragma unroll
-    for (int i = 0; i < PTile::CA; ++i) rowsA[i] = rm.row(at * PBA + PTile::chunk_row(i));
+    for (int i = 0; i < T::CA; ++i) {
+        const int a = at * BA + T::chunk_row(i);
+        rowsA[i] = a < hd ? wq + (long)a * rm.C : (a < 2 * hd ? wk + (long)(a - hd) * rm.C : nullptr);
+    }
 #pragma unroll
-    for (int i = 0; i < PTile::CB; ++i) {
-        const int b = bt * PBB + PTile::chunk_row(i);
+    for (int i = 0; i < T::CB; ++i) rowsB[i] = rm.row(bt * BB + T::chunk_row(i));
+    T t;
+    t.run(lds, rowsA, rowsB, rm.C, 0, 0);
+    const int a0 = at * BA, b0 = bt * BB;
+    stage_rows<BA>(t, lds, [&](float v, int a) { return f2h_bits(a0 + a < hd ? v * qscale : v); },
+                   [](int a) { return a; });
+    __syncthreads();
+    write_rows<BA, BB>(lds, min(BA, 2 * hd - a0), [&](int b, int c0) -> uint16_t * {
+        const int r = b0 + b, a = a0 + c0;
+        if (r >= rm.n_rows) return nullptr;
+        return a < hd ? Q + (long)r * hd + a : K + (long)r * hd + (a - hd);
+    });
+}
+
+// ---------------------------------------------------------------------------
+// V: a = batch rows, b in [0, hd) = rows of wv.  Vt[h][s][d][pos].  Tiles
+// whose rows are a 16-aligned run of one sequence (a single sequence, or
+// L % 128 == 0) are staged as Vt rows: the positions of the tile's tokens,
+// zero for positions past the end (the key padding up to lpad), written
+// as whole chunks.  Otherwise elements are stored one by one and, when the
+// attention kernel needs it, the key padding is zeroed separately.
+// ---------------------------------------------------------------------------
+template <bool DMA>
+using VTile = typename std::conditional<DMA, DmaTile<128, 64, 2, 2>, MfmaTile<128, 128, 2, 2>>::type;
+
+template <bool DMA>
+__global__ __launch_bounds__(256) void k_proj_v(RowMap rm, const uint16_t *__restrict__ wv, int hd, int dh,
+                                                int n_seq, int L, int lpad, int n_at, int n_bt, int zero_pad,
+                                                uint16_t *__restrict__ Vt) {
+    using T = VTile<DMA>;
+    constexpr int BA = 128, BB = DMA ? 64 : 128;
+    extern __shared__ __align__(16) uint16_t lds[];
+    int at, bt;
+    tile_order(xcd_remap(blockIdx.x, n_at * n_bt), n_at, n_bt, at, bt);
+    const uint16_t *rowsA[T::CA], *rowsB[T::CB];
+#pragma unroll
+    for (int i = 0; i < T::CA; ++i) rowsA[i] = rm.row(at * BA + T::chunk_row(i));
+#pragma unroll
+    for (int i = 0; i < T::CB; ++i) {
+        const int b = bt * BB + T::chunk_row(i);
         rowsB[i] = b < hd ? wv + (long)b * rm.C : nullptr;
     }
-    PTile t;
-    t.run(lds, rowsA, rowsB, rm.C, 0, 0);
+    T t;
+    run_tile(t, lds, rowsA, rowsB, rm.row(0), wv, rm.C, typename std::conditional<DMA, DmaRows, RegRows>::type{});
+    const int Lk = n_seq == 1 ? rm.n_rows : L;
+    const int r0 = at * BA, f0 = bt * BB;
+    if (n_seq == 1 || L % BA == 0) {
+        const int s = n_seq == 1 ? 0 : r0 / L, j0 = r0 - s * L;   // j0 is a multiple of BA
+        stage_rows<BA>(t, lds, [&](float v, int a) { return (uint16_t)(j0 + a < Lk ? f2h_bits(v) : 0); },
+                       [](int a) { return vt_key_of_pos(a); });
+        __syncthreads();
+        write_rows<BA, BB>(lds, min(BA, lpad - j0), [&](int b, int c0) -> uint16_t * {
+            const int f = f0 + b;
+            if (f >= hd) return nullptr;
+            const int h = f / dh, d = f - h * dh;
+            return Vt + (((long)h * n_seq + s) * dh + d) * lpad + j0 + c0;
+        });
+        return;
+    }
 #pragma unroll
-    for (int j = 0; j < PTile::TB; ++j) {
-        const int f = bt * PBB + PTile::b_of(j);
+    for (int j = 0; j < T::TB; ++j) {
+        const int f = f0 + T::b_of(j);
         if (f >= hd) continue;
         const int h = f / dh, d = f - h * dh;
 #pragma unroll
-        for (int i = 0; i < PTile::TA; ++i)
+        for (int i = 0; i < T::TA; ++i)
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int r0 = at * PBA + PTile::a_of(i, g);
-                if (r0 >= rm.n_rows) continue;
-                int s0, j0, s3, j3;
-                seq_pos(r0, n_seq, L, s0, j0);
-                seq_pos(r0 + 3, n_seq, L, s3, j3);
-                if (r0 + 3 < rm.n_rows && s0 == s3 && (j0 & 3) == 0) {
-                    u16x4 v;
+            for (int g = 0; g < 4; ++g)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] = f2h_bits(t.acc[i][j][4 * g + e]);
-                    *reinterpret_cast<u16x4 *>(Vt + (((long)h * n_seq + s0) * dh + d) * lpad + vt_key_of_pos(j0)) = v;
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int r = r0 + e;
-                        if (r >= rm.n_rows) continue;
-                        int s, jj;
-                        seq_pos(r, n_seq, L, s, jj);
-                        Vt[(((long)h * n_seq + s) * dh + d) * lpad + vt_key_of_pos(jj)] = f2h_bits(t.acc[i][j][4 * g + e]);
-                    }
+                for (int e = 0; e < 4; ++e) {
+                    const int r = r0 + T::a_of(i, g) + e;
+                    if (r >= rm.n_rows) continue;
+                    int s, jj;
+                    seq_pos(r, n_seq, L, s, jj);
+                    Vt[(((long)h * n_seq + s) * dh + d) * lpad + vt_key_of_pos(jj)] = f2h_bits(t.acc[i][j][4 * g + e]);
                 }
-            }
     }
     // zero the padded key positions [Lk, lpad) of this block's features, for
     // the sequences s = at, at + n_at, ... (the DMA-staged attention reads them)
-    const int Lk = n_seq == 1 ? rm.n_rows : L, npad = lpad - Lk;
+    const int npad = lpad - Lk;
     if (zero_pad && npad > 0) {
         for (int sq = at; sq < n_seq; sq += n_at)
-            for (int idx = threadIdx.x; idx < PBB * npad; idx += blockDim.x) {
-                const int f = bt * PBB + idx / npad, jj = Lk + idx % npad;
+            for (int idx = threadIdx.x; idx < BB * npad; idx += blockDim.x) {
+                const int f = f0 + idx / npad, jj = Lk + idx % npad;
                 if (f >= hd) continue;
                 const int h = f / dh, d = f - h * dh;
                 Vt[(((long)h * n_seq + sq) * dh + d) * lpad + vt_key_of_pos(jj)] = 0;
@@ -141,63 +208,76 @@ __global__ __launch_bounds__(256) void k_proj_v(RowMap rm, const uint16_t *__res
     }
 }
 
-// a in [0, C): rows of wo; b = batch rows of O.  y[out row][a].
+hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, hipStream_t st) {
+    const float qscale = (float)(1.4426950408889634 / sqrt((double)p.dh));
+    {
+        StageScope _stage(st, "proj_qk");
+        const int n_at = cdiv(2 * p.hd, 128), n_bt = cdiv(rm.n_rows, 128);
+        k_proj_qk<<<n_at * n_bt, 256, QKTile::LDS_BYTES, st>>>(rm, (const uint16_t *)a.wq, (const uint16_t *)a.wk,
+                                                               p.hd, qscale, n_at, n_bt, (uint16_t *)a.q,
+                                                               (uint16_t *)a.k);
+    }
+    {
+        StageScope _stage(st, "proj_v");
+        const int Lk = a.n_seq == 1 ? rm.n_rows : a.L;
+        const int zero_pad = flash_uses_dma(p.dh, Lk) ? 1 : 0;
+        const int n_at = cdiv(rm.n_rows, 128);
+        if (p.C % 64 == 0) {
+            static bool attr = false;
+            hipError_t e = allow_lds(k_proj_v<true>, VTile<true>::LDS_BYTES, attr);
+            if (e != hipSuccess) return e;
+            const int n_bt = cdiv(p.hd, 64);
+            k_proj_v<true><<<n_at * n_bt, 256, VTile<true>::LDS_BYTES, st>>>(
+                rm, (const uint16_t *)a.wv, p.hd, p.dh, a.n_seq, a.L, a.lpad, n_at, n_bt, zero_pad, (uint16_t *)a.vt);
+        } else {
+            const int n_bt = cdiv(p.hd, 128);
+            k_proj_v<false><<<n_at * n_bt, 256, VTile<false>::LDS_BYTES, st>>>(
+                rm, (const uint16_t *)a.wv, p.hd, p.dh, a.n_seq, a.L, a.lpad, n_at, n_bt, zero_pad, (uint16_t *)a.vt);
+        }
+    }
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Output projection: a in [0, C) = rows of wo (fp16); b = batch rows of O.
+// y[out row][a].
+// ---------------------------------------------------------------------------
+template <bool DMA>
+using OTile =
+    typename std::conditional<DMA, DmaTile<128, 64, 2, 2, true>, MfmaTile<128, 128, 2, 2, true, false>>::type;
+
+template <bool DMA>
 __global__ __launch_bounds__(256) void k_proj_out(const uint16_t *__restrict__ O, int n_rows, int hd,
                                                   const uint16_t *__restrict__ wo, int C, int n_main,
                                                   const int32_t *__restrict__ out_idx, int n_at, int n_bt,
                                                   uint16_t *__restrict__ y, uint16_t *__restrict__ y_ctx) {
+    using T = OTile<DMA>;
+    constexpr int BA = 128, BB = DMA ? 64 : 128;
     extern __shared__ __align__(16) uint16_t lds[];
     int at, bt;
     tile_order(xcd_remap(blockIdx.x, n_at * n_bt), n_at, n_bt, at, bt);
-    const uint16_t *rowsA[OTile::CA], *rowsB[OTile::CB];
+    const uint16_t *rowsA[T::CA], *rowsB[T::CB];
 #pragma unroll
-    for (int i = 0; i < OTile::CA; ++i) {
-        const int a = at * PBA + OTile::chunk_row(i);
+    for (int i = 0; i < T::CA; ++i) {
+        const int a = at * BA + T::chunk_row(i);
         rowsA[i] = a < C ? wo + (long)a * hd : nullptr;
     }
 #pragma unroll
-    for (int i = 0; i < OTile::CB; ++i) {
-        const int b = bt * PBB + OTile::chunk_row(i);
+    for (int i = 0; i < T::CB; ++i) {
+        const int b = bt * BB + T::chunk_row(i);
         rowsB[i] = b < n_rows ? O + (long)b * hd : nullptr;
     }
-    OTile t;
-    t.run(lds, rowsA, rowsB, hd, 0, 0);
-#pragma unroll
-    for (int j = 0; j < OTile::TB; ++j) {
-        const int b = bt * PBB + OTile::b_of(j);
-        if (b >= n_rows) continue;
-        uint16_t *yrow = b < n_main ? y + (long)(out_idx ? out_idx[b] : b) * C : y_ctx + (long)(b - n_main) * C;
-#pragma unroll
-        for (int i = 0; i < OTile::TA; ++i)
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int a = at * PBA + OTile::a_of(i, g);
-                if (a >= C) continue;
-                u16x4 v;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] = f2bf(t.acc[i][j][4 * g + e]);
-                *reinterpret_cast<u16x4 *>(yrow + a) = v;
-            }
-    }
-}
-
-hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, hipStream_t st) {
-    const size_t lds = PTile::LDS_BYTES;
-    const float qscale = (float)(1.4426950408889634 / sqrt((double)p.dh));
-    {
-        StageScope _stage(st, "proj_qk");
-        const int n_at = cdiv(2 * p.hd, PBA), n_bt = cdiv(rm.n_rows, PBB);
-        k_proj_qk<<<n_at * n_bt, 256, lds, st>>>(rm, (const uint16_t *)a.wq, (const uint16_t *)a.wk, p.hd, qscale,
-                                                 n_at, n_bt, (uint16_t *)a.q, (uint16_t *)a.k);
-    }
-    {
-        StageScope _stage(st, "proj_v");
-        const int n_at = cdiv(rm.n_rows, PBA), n_bt = cdiv(p.hd, PBB);
-        const int Lk = a.n_seq == 1 ? rm.n_rows : a.L;
-        k_proj_v<<<n_at * n_bt, 256, lds, st>>>(rm, (const uint16_t *)a.wv, p.hd, p.dh, a.n_seq, a.L, a.lpad, n_at,
-                                                n_bt, flash_uses_dma(p.dh, Lk) ? 1 : 0, (uint16_t *)a.vt);
-    }
-    return hipGetLastError();
+    T t;
+    run_tile(t, lds, rowsA, rowsB, wo, O, hd, typename std::conditional<DMA, DmaRows, RegRows>::type{});
+    const int a0 = at * BA, b0 = bt * BB;
+    stage_rows<BA>(t, lds, [](float v, int) { return f2bf(v); }, [](int a) { return a; });
+    __syncthreads();
+    write_rows<BA, BB>(lds, min(BA, C - a0), [&](int b, int c0) -> uint16_t * {
+        const int r = b0 + b;
+        if (r >= n_rows) return nullptr;
+        uint16_t *yrow = r < n_main ? y + (long)(out_idx ? out_idx[r] : r) * C : y_ctx + (long)(r - n_main) * C;
+        return yrow + a0 + c0;
+    });
 }
 
 // bf16 -> fp16 (exact in the fp16 normal range, saturating outside), 8 per thread
@@ -215,10 +295,21 @@ hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStre
                                                                             (uint4 *)a.wo16);
     }
     StageScope _stage(st, "proj_out");
-    const int n_at = cdiv(p.C, PBA), n_bt = cdiv(n_rows, PBB);
-    k_proj_out<<<n_at * n_bt, 256, OTile::LDS_BYTES, st>>>((const uint16_t *)a.o, n_rows, p.hd,
-                                                           (const uint16_t *)a.wo16, p.C, a.n_main, a.out_idx, n_at,
-                                                           n_bt, (uint16_t *)a.y, (uint16_t *)a.y_ctx);
+    const int n_at = cdiv(p.C, 128);
+    if (p.hd % 64 == 0) {
+        static bool attr = false;
+        hipError_t e = allow_lds(k_proj_out<true>, OTile<true>::LDS_BYTES, attr);
+        if (e != hipSuccess) return e;
+        const int n_bt = cdiv(n_rows, 64);
+        k_proj_out<true><<<n_at * n_bt, 256, OTile<true>::LDS_BYTES, st>>>(
+            (const uint16_t *)a.o, n_rows, p.hd, (const uint16_t *)a.wo16, p.C, a.n_main, a.out_idx, n_at, n_bt,
+            (uint16_t *)a.y, (uint16_t *)a.y_ctx);
+    } else {
+        const int n_bt = cdiv(n_rows, 128);
+        k_proj_out<false><<<n_at * n_bt, 256, OTile<false>::LDS_BYTES, st>>>(
+            (const uint16_t *)a.o, n_rows, p.hd, (const uint16_t *)a.wo16, p.C, a.n_main, a.out_idx, n_at, n_bt,
+            (uint16_t *)a.y, (uint16_t *)a.y_ctx);
+    }
     return hipGetLastError();
 }
 

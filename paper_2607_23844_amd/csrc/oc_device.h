@@ -12,6 +12,23 @@ typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int WAVE = 64;
 
+// address-space views for global_load_lds (global source, LDS destination)
+typedef __attribute__((address_space(3))) void *lds_vp;
+typedef __attribute__((address_space(1))) void *glb_vp;
+
+// s_waitcnt vmcnt(n) leaving the other counters alone (gfx9 encoding; n < 64)
+#define OC_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8))
+
+// Workgroup barrier for loops that stage operands with global_load_lds.
+// __syncthreads() is a release fence plus s_barrier, and the fence waits for
+// every outstanding LDS-DMA load (vmcnt(0)), which would drain the prefetch
+// ring at each step.  Here each wave has already waited (vmcnt) for its own
+// loads of the stage being published; the barrier only needs this wave's
+// LDS reads to have completed (lgkmcnt(0)) before other waves may overwrite
+// what they read.  The memory clobber keeps the compiler from moving memory
+// accesses across it.
+__device__ __forceinline__ void barrier_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 __device__ __forceinline__ float bf2f(uint16_t v) { return __uint_as_float((uint32_t)v << 16); }
 
 // fp32 -> bf16 bits, round to nearest even (inputs are finite).
