@@ -28,8 +28,9 @@
 //   DMA (head_dim a multiple of 64, long sequences): global_load_lds moves
 //     16 bytes per lane straight into LDS, three tiles ahead, into a ring of
 //     four unpadded buffers whose 16-byte chunks are XOR-swizzled by row
-//     (chunk c of row r at slot c ^ (r & 7)) so the fragment reads of 8
-//     consecutive rows hit distinct banks.  Key rows past the end are
+//     (chunk c of row r at slot c ^ ((r >> sh) & 7), sh = 1 for 128-byte
+//     rows, two of which fill the 64 LDS banks, 0 for 256-byte rows), so the
+//     fragment reads of 16 consecutive rows hit distinct banks.  Key rows past the end are
 //     clamped to the last key (their scores are masked) and the V projection
 //     zeroes the padded key positions of Vt, so nothing needs masking in LDS;
 //   registers (other head dims, short sequences): global loads one tile
@@ -60,10 +61,14 @@ struct FlashCfg {
     static_assert(!DMA || (DK == DH && DV == DH && DH % 64 == 0), "DMA staging needs head_dim % 64 == 0");
 };
 
+// XOR swizzle of the DMA layout: slot of chunk c in row r (rows of LD halves)
+template <int LD>
+__device__ __forceinline__ int dma_slot(int r, int c) { return c ^ ((r >> (LD * 2 >= 256 ? 0 : 1)) & 7); }
+
 // LDS offset (halves) of the 8-element chunk c of row r in a buffer of rows of LD halves
 template <bool DMA, int LD>
 __device__ __forceinline__ int lds_chunk(int r, int c) {
-    return DMA ? r * LD + ((c ^ (r & 7)) << 3) : r * LD + (c << 3);
+    return DMA ? r * LD + (dma_slot<LD>(r, c) << 3) : r * LD + (c << 3);
 }
 
 template <int DH, int NW, bool DMA>
@@ -113,14 +118,14 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
 #pragma unroll
         for (int j = 0; j < IK; ++j) {
             const int q = (wave * IK + j) * 64 + lane;
-            const int r = q / (DK / 8), c = (q % (DK / 8)) ^ (r & 7);
+            const int r = q / (DK / 8), c = dma_slot<LDK>(r, q % (DK / 8));
             kdrow[j] = r;
             kd[j] = kbase + c * 8;
         }
 #pragma unroll
         for (int j = 0; j < IV; ++j) {
             const int q = (wave * IV + j) * 64 + lane;
-            const int d = q / (KT / 8), c = (q % (KT / 8)) ^ (d & 7);
+            const int d = q / (KT / 8), c = dma_slot<LDV>(d, q % (KT / 8));
             vd[j] = vbase + (long)d * lpad + c * 8;
         }
     }

@@ -5,6 +5,7 @@
 #include "oc_groups.h"
 #include "oc_device.h"
 #include "oc_mfma_tile.h"
+#include "oc_dma_tile.h"
 #include "oc_attn_common.h"
 #include <algorithm>
 
@@ -77,13 +78,16 @@ hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, unsigned lo
 // packed pair, so the representative tiles need no second pass.  The
 // representative norm is applied before the arg-max, the candidate's own
 // norm (a positive constant per row) when unpacking.
-template <int BA, int BB, int WA, int WB>
+template <int BA, int BB, int WA, int WB, bool DMA>
+using MatchTile = typename std::conditional<DMA, DmaTile<BA, BB, WA, WB>, MfmaTile<BA, BB, WA, WB>>::type;
+
+template <int BA, int BB, int WA, int WB, bool DMA>
 __global__ __launch_bounds__(256) void k_match_mfma(const uint16_t *__restrict__ x, const float *__restrict__ inv,
                                                      GroupMap gm, int G, int S, int D,
                                                      int K, int seg_len, long sub_stride, long item_stride,
                                                      int n_bt, int n_at,
                                                      unsigned long long *__restrict__ node_pack) {
-    using T = MfmaTile<BA, BB, WA, WB>;
+    using T = MatchTile<BA, BB, WA, WB, DMA>;
     extern __shared__ __align__(16) uint16_t lds[];
     const int total = n_bt * n_at * G;
     const int lid = xcd_remap(blockIdx.x, total);
@@ -104,7 +108,10 @@ __global__ __launch_bounds__(256) void k_match_mfma(const uint16_t *__restrict__
         rowsB[i] = id >= 0 ? x + (long)id * item_stride : nullptr;
     }
     T tile;
-    tile.run(lds, rowsA, rowsB, K, seg_len, sub_stride);
+    // rows without an item read x's first row (DMA) or zeros; either way
+    // their results are discarded below
+    if constexpr (DMA) tile.run(lds, rowsA, rowsB, x, x, K, seg_len, sub_stride);
+    else tile.run(lds, rowsA, rowsB, K, seg_len, sub_stride);
 
     // representative norms of this tile (0 for padding, which never wins)
     float *sinv = reinterpret_cast<float *>(lds);
@@ -203,15 +210,27 @@ __global__ void k_match_unpack(const unsigned long long *__restrict__ node_pack,
     node_idx[i] = ix >= 0 ? gm.dst_id(gr, ix) : -1;
 }
 
-template <int BA, int BB, int WA, int WB>
-static void go_match(const Plan &p, const uint16_t *x, const float *inv, const GroupMap &gm, int K, int seg_len,
-                     long sub_stride, long item_stride, unsigned long long *node_pack, hipStream_t st) {
-    using T = MfmaTile<BA, BB, WA, WB>;
+template <int BA, int BB, int WA, int WB, bool DMA>
+static hipError_t go_match(const Plan &p, const uint16_t *x, const float *inv, const GroupMap &gm, int K,
+                           int seg_len, long sub_stride, long item_stride, unsigned long long *node_pack,
+                           hipStream_t st) {
+    using T = MatchTile<BA, BB, WA, WB, DMA>;
     const int G = p.n_groups, S = p.n_src_max, D = p.n_dst_max;
     const int n_bt = cdiv(S, BB), n_at = cdiv(D, BA);
     const size_t lds = T::LDS_BYTES;
-    k_match_mfma<BA, BB, WA, WB><<<n_bt * n_at * G, 256, lds, st>>>(x, inv, gm, G, S, D, K, seg_len,
-                                                                     sub_stride, item_stride, n_bt, n_at, node_pack);
+    if (lds > 65536) {
+        static bool attr = false;
+        if (!attr) {
+            const hipError_t e = hipFuncSetAttribute((const void *)k_match_mfma<BA, BB, WA, WB, DMA>,
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (e != hipSuccess) return e;
+            attr = true;
+        }
+    }
+    k_match_mfma<BA, BB, WA, WB, DMA><<<n_bt * n_at * G, 256, lds, st>>>(x, inv, gm, G, S, D, K, seg_len,
+                                                                          sub_stride, item_stride, n_bt, n_at,
+                                                                          node_pack);
+    return hipGetLastError();
 }
 
 hipError_t launch_match(const Plan &p, const void *x, const float *inv, const int32_t *units,
@@ -227,13 +246,22 @@ hipError_t launch_match(const Plan &p, const void *x, const float *inv, const in
         StageScope _stage(st, "match");
         if (p.bf16) {
             const uint16_t *xb = (const uint16_t *)x;
-            // representative tile height by group size: 128, 64 or 32
+            // representative tile height by group size: 128, 64 or 32; large
+            // groups stream by LDS DMA when the K steps allow it
+            const bool dma = K % 64 == 0 && (seg_len == 0 || seg_len % 64 == 0);
+            hipError_t e;
             if (D > 64)
-                go_match<128, 64, 2, 2>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride, node_pack, st);
+                e = dma ? go_match<128, 128, 2, 2, true>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride,
+                                                         node_pack, st)
+                        : go_match<128, 64, 2, 2, false>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride,
+                                                         node_pack, st);
             else if (D > 32)
-                go_match<64, 64, 2, 2>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride, node_pack, st);
+                e = go_match<64, 64, 2, 2, false>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride, node_pack,
+                                                  st);
             else
-                go_match<32, 128, 1, 4>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride, node_pack, st);
+                e = go_match<32, 128, 1, 4, false>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride, node_pack,
+                                                   st);
+            if (e != hipSuccess) return e;
         } else {
             dim3 grid(cdiv(S, 64), G);
             k_match_f32<<<grid, 64, 0, st>>>((const float *)x, inv, gm, G, S, D, K, seg_len, sub_stride,

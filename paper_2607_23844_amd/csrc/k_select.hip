@@ -41,7 +41,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
     __shared__ int hist[2][SEL_WAVES][256];
     __shared__ uint32_t red[3][SEL_WAVES];
     __shared__ int sh[17];
-    __shared__ int sel_info[2];
+    __shared__ int sel_info[3];
     const int g = blockIdx.x;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int ipt = cdiv(S, SEL_THREADS);
@@ -113,9 +113,11 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
         kmax = max(kmax, red[2][w]);
     }
 
-    // threshold key tau (the R-th largest) and how many keys equal to tau are taken
+    // threshold key tau (the R-th largest), how many keys equal to tau are
+    // taken (need) and how many there are (n_eq: the count of the last
+    // selected bin, which holds exactly the keys equal to tau)
     uint32_t tau = 0;
-    int need = 0;
+    int need = 0, n_eq = n_valid;
     const bool none = R <= 0;
     const bool all = R >= n_valid;
     if (!none && !all) {
@@ -160,6 +162,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
                     if (above < remaining && remaining <= above + c[q]) {
                         sel_info[0] = 4 * t + q;
                         sel_info[1] = above;
+                        sel_info[2] = c[q];
                     }
                     above += c[q];
                 }
@@ -169,6 +172,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
             __syncthreads();
             const int sel = sel_info[0];
             remaining -= sel_info[1];
+            n_eq = sel_info[2];
             prefix |= (uint32_t)sel << bit_lo;
             mask |= dmask << bit_lo;
             bit_hi = bit_lo - 1;
@@ -178,13 +182,19 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
         need = remaining;
     }
 
-    // exact selection: key > tau, or key == tau among the first `need` in index order
-    int eq_local = 0;
+    // exact selection: key > tau, or key == tau among the first `need` in
+    // index order; without a tie to break (every key equal to tau taken) no
+    // rank is needed
+    const bool tie = !none && !all && need < n_eq;
+    int eq_rank = 0;
+    if (tie) {
+        int eq_local = 0;
 #pragma unroll
-    for (int j = 0; j < SEL_IPT; ++j)
-        if (((vmask >> j) & 1u) && key[j] == tau) ++eq_local;
-    int eq_total;
-    int eq_rank = block_exclusive_scan((!none && !all) ? eq_local : 0, sh, eq_total);
+        for (int j = 0; j < SEL_IPT; ++j)
+            if (((vmask >> j) & 1u) && key[j] == tau) ++eq_local;
+        int eq_total;
+        eq_rank = block_exclusive_scan(eq_local, sh, eq_total);
+    }
     // frame compaction (kept_idx given): flags of the frame's N tokens in LDS
     __shared__ uint8_t fl[SEL_COMPACT_MAX_N];
     const bool compact = kept_idx != nullptr;
@@ -197,7 +207,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
         if (none) c = false;
         else if (all) c = true;
         else if (key[j] > tau) c = true;
-        else if (key[j] == tau) { c = eq_rank < need; ++eq_rank; }
+        else if (key[j] == tau) { c = !tie || eq_rank < need; ++eq_rank; }
         else c = false;
         const int id = gm.src_id(gr, i);
         flag[id] = c ? 1 : 0;

@@ -11,8 +11,9 @@
 // spare register set and then runs step kt's MFMAs from the fragments read
 // one iteration earlier: LDS latency hides behind the MFMAs and global
 // latency behind NST-1 steps.  An LDS row is the 128 bytes of one operand
-// row's step, unpadded; its 16-byte chunk c sits in slot c ^ (row & 7), so
-// the fragment reads of 8 consecutive rows hit distinct banks.  DMA
+// row's step, unpadded; its 16-byte chunk c sits in slot c ^ ((row >> 1) & 7):
+// two rows fill the 64 LDS banks, so the fragment reads of 16 consecutive
+// rows hit distinct banks.  DMA
 // instruction i of a wave fills the 64 slots (wave + 4i)*64 .. +63 of the
 // operand's stage, that is rows chunk_row(i) of MfmaTile: callers pass the
 // same per-thread row bases.  Rows without data (nullptr) read the fallback
@@ -42,7 +43,7 @@ struct DmaTile {
 
     f32x16 acc[TA][TB];
 
-    __device__ __forceinline__ static int slot(int r, int c) { return r * BK + ((c ^ (r & 7)) << 3); }
+    __device__ __forceinline__ static int slot(int r, int c) { return r * BK + ((c ^ ((r >> 1) & 7)) << 3); }
 
     // MFMA fragments of one step: [ks][i] for A, [ks][j] for B
     struct Frags {
@@ -93,12 +94,12 @@ struct DmaTile {
 #pragma unroll
         for (int i = 0; i < CA; ++i) {
             const int r = chunk_row(i);
-            pa[i] = (rowsA[i] ? rowsA[i] : fallbackA) + (((t & 7) ^ (r & 7)) << 3);
+            pa[i] = (rowsA[i] ? rowsA[i] : fallbackA) + (((t & 7) ^ ((r >> 1) & 7)) << 3);
         }
 #pragma unroll
         for (int i = 0; i < CB; ++i) {
             const int r = chunk_row(i);
-            pb[i] = (rowsB[i] ? rowsB[i] : fallbackB) + (((t & 7) ^ (r & 7)) << 3);
+            pb[i] = (rowsB[i] ? rowsB[i] : fallbackB) + (((t & 7) ^ ((r >> 1) & 7)) << 3);
         }
         const int nk = K / BK;
         constexpr int D = NST - 1;   // issue distance in steps
