@@ -27,6 +27,32 @@ sys.path.insert(0, ROOT)
 METRIC = "cached attn-layer tokens/sec & latency vs uncached at r; MFMA % / HBM GB/s"
 PEAK_MFMA_TFLOPS = 2516.6     # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+# Counter summary of the dominant kernel (rocprofv3 FETCH_SIZE / WRITE_SIZE
+# runs, scaled by a copy kernel of known size) and the sources it was taken on.
+PROFILE = os.path.join(ROOT, "profiles", "sd3_1024_r050_kernels.md")
+FLASH_SOURCES = ("k_flash.hip", "oc_attn_common.h", "oc_device.h")
+
+
+def flash_source_hash():
+    import hashlib
+    h = hashlib.sha1()
+    for f in FLASH_SOURCES:
+        with open(os.path.join(ROOT, "paper_2607_23844_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def flash_traffic():
+    """HBM bytes per flash launch from the committed counter summary, or None
+    when there is none or the kernel's sources changed since it was taken."""
+    try:
+        with open(PROFILE) as fh:
+            kv = dict(l.split(":", 1) for l in fh.read().splitlines() if l.startswith("flash_"))
+        if kv["flash_source_sha1"].strip() != flash_source_hash():
+            return None
+        return int(float(kv["flash_traffic_bytes_per_launch"]))
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def stage_work(shape, pl, n_ctx):
@@ -97,7 +123,7 @@ def run_gpu(args):
         if r == args.r:
             primary = (cfg, run, ms, wall)
     cfg, run, ms, wall = primary
-    # live per-stage timing: HIP events around each kernel on the launch stream
+    # live per-kernel timing: HIP events stamped by the runtime at each kernel's start and end
     timer = oc.StageTimer()
     with timer:
         for i in range(K):
@@ -122,17 +148,18 @@ def run_gpu(args):
     dom = max(stages, key=lambda s: stages[s][0])
     dom_avg_us = stages[dom][0] * 1e3 / stages[dom][1]
     roof = None
+    traffic = flash_traffic() if dom == "flash" else None
     if dom in work:
         kind, amount = work[dom]
         if kind == "mfma":
             ach = amount / (dom_avg_us * 1e-6) / 1e12
             roof = dict(kernel=dom, bound="mfma", achieved=round(ach, 2), peak=PEAK_MFMA_TFLOPS, unit="TFLOP/s",
-                        frac=round(ach / PEAK_MFMA_TFLOPS, 4), traffic=None, avg_us=round(dom_avg_us, 3),
+                        frac=round(ach / PEAK_MFMA_TFLOPS, 4), traffic=traffic, avg_us=round(dom_avg_us, 3),
                         algorithmic_per_launch=amount)
         else:
             ach = amount / (dom_avg_us * 1e-6) / 1e9
             roof = dict(kernel=dom, bound="hbm", achieved=round(ach, 1), peak=PEAK_HBM_GBS, unit="GB/s",
-                        frac=round(ach / PEAK_HBM_GBS, 4), traffic=None, avg_us=round(dom_avg_us, 3),
+                        frac=round(ach / PEAK_HBM_GBS, 4), traffic=traffic, avg_us=round(dom_avg_us, 3),
                         algorithmic_per_launch=amount)
     return dict(ms=ms, wall=wall, tokens=tokens, full_ms=full_ms, by_r=by_r, kernels=kernels, roofline=roof,
                 plan=dict(n_kept=pl.n_kept, n_cached=pl.n_cached, seq_len=pl.seq_len))

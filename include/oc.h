@@ -250,11 +250,11 @@ const char *oc_last_error(void);
  * Stage timing (a profiling aid, not part of the method).  A caller-owned
  * timer holds HIP events; while it is attached to a thread with
  * oc_timer_use, every kernel the library enqueues from that thread is
- * bracketed by a pair of events on the call's stream, tagged with its stage
- * name ("match", "select", "flash", ...).  oc_timer_collect waits for the
- * recorded events and adds each pair's elapsed time to its stage's total.
- * Event records add a small gap between kernels; time the unprofiled path
- * with the timer detached.  oc_timer_use(NULL) detaches.
+ * launched with a pair of the timer's events that the runtime stamps at the
+ * kernel's start and end (so a stage's time is its kernels' durations), tagged
+ * with its stage name ("match", "select", "flash", ...).  oc_timer_collect
+ * waits for the events and adds each kernel's duration to its stage's total
+ * and 1 to its stage's launch count.  oc_timer_use(NULL) detaches.
  */
 typedef struct oc_timer oc_timer;
 oc_status oc_timer_create(oc_timer **out);

@@ -6,6 +6,7 @@
 // -> output projection written straight to the output positions.
 // fp32 layers: the same dataflow with plain VALU kernels (below).
 #include "oc_attn_common.h"
+#include "oc_launch.h"
 
 namespace oc {
 
@@ -119,14 +120,14 @@ hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st) {
     const long nq = (long)n_rows * 3 * p.hd;
     {
         StageScope _stage(st, "proj_f32");
-        k_proj_f32<<<(unsigned)((nq + 255) / 256), 256, 0, st>>>(rm, (const float *)a.wq, (const float *)a.wk,
+        launch_k(k_proj_f32, (unsigned)((nq + 255) / 256), 256, 0, st, rm, (const float *)a.wq, (const float *)a.wk,
                                                                   (const float *)a.wv, p.hd, (float *)a.q,
                                                                   (float *)a.k, (float *)a.vt);
     }
     const long na = (long)n_rows * p.heads;
     {
         StageScope _stage(st, "attn_f32");
-        k_attn_f32<<<(unsigned)((na + 127) / 128), 128, 0, st>>>((const float *)a.q, (const float *)a.k,
+        launch_k(k_attn_f32, (unsigned)((na + 127) / 128), 128, 0, st, (const float *)a.q, (const float *)a.k,
                                                                   (const float *)a.vt, (float *)a.o, n_rows, p.heads,
                                                                   p.dh, a.n_seq, a.L, Lk,
                                                                   (float)(1.0 / sqrt((double)p.dh)));
@@ -134,7 +135,7 @@ hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st) {
     const long no = (long)n_rows * p.C;
     {
         StageScope _stage(st, "out_f32");
-        k_out_f32<<<(unsigned)((no + 255) / 256), 256, 0, st>>>((const float *)a.o, n_rows, p.hd,
+        launch_k(k_out_f32, (unsigned)((no + 255) / 256), 256, 0, st, (const float *)a.o, n_rows, p.hd,
                                                                  (const float *)a.wo, p.C, a.n_main, a.out_idx,
                                                                  (float *)a.y, (float *)a.y_ctx);
     }

@@ -6,6 +6,7 @@
 // Every write is bounded by the plan's static counts, so inconsistent flags
 // can produce wrong indices but never an out-of-range access.
 #include "oc_internal.h"
+#include "oc_launch.h"
 #include "oc_device.h"
 #include "oc_block.h"
 #include <algorithm>
@@ -191,23 +192,23 @@ hipError_t launch_compact(const Plan &p, const int32_t *units, const int32_t *fl
         const bool pairs = p.gran == 3;
         if (pairs) {
             StageScope _stage(st, "frame_counts");
-            k_frame_counts<<<p.F, 1024, 0, st>>>(flag, p.N, fcnt);
+            launch_k(k_frame_counts, p.F, 1024, 0, st, flag, p.N, fcnt);
         }
         {
             StageScope _stage(st, "compact");
-            k_compact_units<<<p.n_units, CMP_THREADS, 0, st>>>(pairs ? units : nullptr, p.F, flag,
+            launch_k(k_compact_units, p.n_units, CMP_THREADS, 0, st, pairs ? units : nullptr, p.F, flag,
                                                                 pairs ? fcnt : nullptr, p.k * p.k * p.R_tok, p.N,
                                                                 p.seq_len, p.n_cached, kept_idx, cached_idx, rmap);
         }
     } else if (p.kind == KIND_BLOCK) {
         {
             StageScope _stage(st, "compact");
-            k_compact_blocks<<<1, CMP_THREADS, 0, st>>>(flag, p.F, p.N, p.n_seq, kept_idx, cached_idx, rmap);
+            launch_k(k_compact_blocks, 1, CMP_THREADS, 0, st, flag, p.F, p.N, p.n_seq, kept_idx, cached_idx, rmap);
         }
     } else {
         {
             StageScope _stage(st, "compact");
-            k_compact_frames<<<grid, 256, 0, st>>>(flag, p.F, p.N, p.n_seq, kept_idx, cached_idx, rmap);
+            launch_k(k_compact_frames, grid, 256, 0, st, flag, p.F, p.N, p.n_seq, kept_idx, cached_idx, rmap);
         }
     }
     hipError_t e = hipGetLastError();
@@ -221,7 +222,7 @@ hipError_t launch_map_matched(const Plan &p, const int32_t *flag, const int32_t 
     const unsigned grid = (unsigned)std::min<long>((total + 255) / 256, 4096);
     {
         StageScope _stage(st, "map_matched");
-        k_map_matched<<<grid, 256, 0, st>>>(p.kind, flag, mtok, p.F, p.N, rmap);
+        launch_k(k_map_matched, grid, 256, 0, st, p.kind, flag, mtok, p.F, p.N, rmap);
     }
     return hipGetLastError();
 }

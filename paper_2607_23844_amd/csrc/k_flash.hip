@@ -38,6 +38,7 @@
 // Only the last tile's scores are masked.  Blocks of one head are kept on one
 // XCD (xcd_remap) so its K/V stay in that XCD's L2.
 #include "oc_attn_common.h"
+#include "oc_launch.h"
 #include "oc_mfma_tile.h"
 
 namespace oc {
@@ -409,7 +410,7 @@ static hipError_t go(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
         if (e != hipSuccess) return e;
         attr = true;
     }
-    k_flash<DH, NW, DMA><<<total, NW * 64, lds, st>>>((const uint16_t *)a.q, (const uint16_t *)a.k,
+    launch_k(k_flash<DH, NW, DMA>, total, NW * 64, lds, st, (const uint16_t *)a.q, (const uint16_t *)a.k,
                                                       (const uint16_t *)a.vt, (uint16_t *)a.o, p.hd, p.heads,
                                                       a.n_seq, a.L, Lk, a.lpad, n_qt);
     return hipGetLastError();

@@ -4,6 +4,7 @@
 // best matches, the selection of the most redundant odd frames and their
 // one-to-one pairing with even frames.
 #include "oc_internal.h"
+#include "oc_launch.h"
 #include "oc_device.h"
 
 namespace oc {
@@ -204,23 +205,23 @@ hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, cha
         nb = 1;
         {
             StageScope _stage(st, "frame_gram");
-            k_frame_gram_f32<<<p.F * p.F, 256, 0, st>>>((const float *)x, p.F, D, part);
+            launch_k(k_frame_gram_f32, p.F * p.F, 256, 0, st, (const float *)x, p.F, D, part);
         }
     } else if (p.F > 16)
         {
             StageScope _stage(st, "frame_gram");
-            k_frame_gram<true><<<nb, 256, 0, st>>>((const uint16_t *)x, p.F, D, gram_kw(p), part);
+            launch_k(k_frame_gram<true>, nb, 256, 0, st, (const uint16_t *)x, p.F, D, gram_kw(p), part);
         }
     else
         {
             StageScope _stage(st, "frame_gram");
-            k_frame_gram<false><<<nb, 256, 0, st>>>((const uint16_t *)x, p.F, D, gram_kw(p), part);
+            launch_k(k_frame_gram<false>, nb, 256, 0, st, (const uint16_t *)x, p.F, D, gram_kw(p), part);
         }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     {
         StageScope _stage(st, "frame_final");
-        k_frame_final<<<1, 1024, 0, st>>>(part, nb, p.F, p.R_f, p.gran == 3 ? 1 : 0, (double *)(ws + L.fsim), node_max,
+        launch_k(k_frame_final, 1, 1024, 0, st, part, nb, p.F, p.R_f, p.gran == 3 ? 1 : 0, (double *)(ws + L.fsim), node_max,
                                           node_idx, (int32_t *)(ws + L.forder), (int32_t *)(ws + L.pairs),
                                           (int32_t *)(ws + L.units));
     }

@@ -2,6 +2,7 @@
 // with a fused row arg-max (OmniCache §3.2.1-§3.2.3 cosine-similarity
 // matching, patch-local per §3.3).  Group members come from GroupMap.
 #include "oc_internal.h"
+#include "oc_launch.h"
 #include "oc_groups.h"
 #include "oc_device.h"
 #include "oc_mfma_tile.h"
@@ -59,11 +60,11 @@ hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, unsigned lo
     const long n8 = (wo && wo16 && p.bf16) ? n_wo / 8 : 0;
     const int cvt_blocks = n8 > 0 ? (int)std::min<long>((n8 + 255) / 256, 1024) : 0;
     if (p.bf16)
-        k_inv_norm<uint16_t><<<blocks + cvt_blocks, 256, 0, st>>>((const uint16_t *)x, inv, n_items, n_sub, sub, p.C,
+        launch_k(k_inv_norm<uint16_t>, blocks + cvt_blocks, 256, 0, st, (const uint16_t *)x, inv, n_items, n_sub, sub, p.C,
                                                                  blocks, node_pack, n_pack, (const uint4 *)wo, n8,
                                                                  (uint4 *)wo16);
     else
-        k_inv_norm<float><<<blocks, 256, 0, st>>>((const float *)x, inv, n_items, n_sub, sub, p.C, blocks, node_pack,
+        launch_k(k_inv_norm<float>, blocks, 256, 0, st, (const float *)x, inv, n_items, n_sub, sub, p.C, blocks, node_pack,
                                                   n_pack, nullptr, 0, nullptr);
     return hipGetLastError();
 }
@@ -227,7 +228,7 @@ static hipError_t go_match(const Plan &p, const uint16_t *x, const float *inv, c
             attr = true;
         }
     }
-    k_match_mfma<BA, BB, WA, WB, DMA><<<n_bt * n_at * G, 256, lds, st>>>(x, inv, gm, G, S, D, K, seg_len,
+    launch_k(k_match_mfma<BA, BB, WA, WB, DMA>, n_bt * n_at * G, 256, lds, st, x, inv, gm, G, S, D, K, seg_len,
                                                                           sub_stride, item_stride, n_bt, n_at,
                                                                           node_pack);
     return hipGetLastError();
@@ -264,7 +265,7 @@ hipError_t launch_match(const Plan &p, const void *x, const float *inv, const in
             if (e != hipSuccess) return e;
         } else {
             dim3 grid(cdiv(S, 64), G);
-            k_match_f32<<<grid, 64, 0, st>>>((const float *)x, inv, gm, G, S, D, K, seg_len, sub_stride,
+            launch_k(k_match_f32, grid, 64, 0, st, (const float *)x, inv, gm, G, S, D, K, seg_len, sub_stride,
                                              item_stride, node_pack);
         }
     }
@@ -273,7 +274,7 @@ hipError_t launch_match(const Plan &p, const void *x, const float *inv, const in
     const long n = (long)G * S;
     {
         StageScope _stage(st, "match_unpack");
-        k_match_unpack<<<(unsigned)cdiv((int)n, 256), 256, 0, st>>>(node_pack, G, S, inv, gm, node_max, node_idx);
+        launch_k(k_match_unpack, (unsigned)cdiv((int)n, 256), 256, 0, st, node_pack, G, S, inv, gm, node_max, node_idx);
     }
     return hipGetLastError();
 }

@@ -3,6 +3,7 @@
 // positions; App. A gather-scatter).  Each thread moves one 16-byte chunk of
 // a row; consecutive threads cover consecutive chunks of a row.
 #include "oc_internal.h"
+#include "oc_launch.h"
 #include "oc_device.h"
 
 namespace oc {
@@ -63,7 +64,7 @@ hipError_t launch_gather(const Plan &p, const void *x, const int32_t *kept_idx, 
     const int cpr = p.C * p.esz / 16;
     {
         StageScope _stage(st, "gather");
-        k_gather<<<grid_for((long)n_rows * cpr), 256, 0, st>>>((const uint4 *)x, kept_idx, n_rows, cpr,
+        launch_k(k_gather, grid_for((long)n_rows * cpr), 256, 0, st, (const uint4 *)x, kept_idx, n_rows, cpr,
                                                                (long)p.F * p.N, (uint4 *)x_kept);
     }
     return hipGetLastError();
@@ -75,7 +76,7 @@ hipError_t launch_restore(const Plan &p, const void *y_kept, int n_rows, const i
     const long n_pos = (long)p.F * p.N;
     {
         StageScope _stage(st, "restore");
-        k_restore<<<grid_for(n_pos * cpr), 256, 0, st>>>((const uint4 *)y_kept, n_rows, rmap, (const uint4 *)cache_y,
+        launch_k(k_restore, grid_for(n_pos * cpr), 256, 0, st, (const uint4 *)y_kept, n_rows, rmap, (const uint4 *)cache_y,
                                                          n_pos, cpr, (uint4 *)y);
     }
     return hipGetLastError();
@@ -87,7 +88,7 @@ hipError_t launch_copy_matched(const Plan &p, const int32_t *cached_idx, int n_c
     const int cpr = p.C * p.esz / 16;
     {
         StageScope _stage(st, "copy_matched");
-        k_copy_matched<<<grid_for((long)n_cached * cpr), 256, 0, st>>>(cached_idx, n_cached, rmap, kept_idx, p.n_kept,
+        launch_k(k_copy_matched, grid_for((long)n_cached * cpr), 256, 0, st, cached_idx, n_cached, rmap, kept_idx, p.n_kept,
                                                                        (long)p.F * p.N, cpr, (uint4 *)y);
     }
     return hipGetLastError();
@@ -100,7 +101,7 @@ hipError_t launch_fill_i32(int32_t *dst, long n, int32_t value, hipStream_t st) 
     if (n <= 0) return hipSuccess;
     {
         StageScope _stage(st, "fill");
-        k_fill_i32<<<grid_for(n), 256, 0, st>>>(dst, n, value);
+        launch_k(k_fill_i32, grid_for(n), 256, 0, st, dst, n, value);
     }
     return hipGetLastError();
 }

@@ -25,6 +25,7 @@
 // of logical tiles, and logical tiles are grouped GA weight tiles wide, so
 // one XCD's L2 sees a few weight tiles and a few token tiles instead of all.
 #include "oc_internal.h"
+#include "oc_launch.h"
 #include "oc_device.h"
 #include "oc_mfma_tile.h"
 #include "oc_dma_tile.h"
@@ -213,7 +214,7 @@ hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, h
     {
         StageScope _stage(st, "proj_qk");
         const int n_at = cdiv(2 * p.hd, 128), n_bt = cdiv(rm.n_rows, 128);
-        k_proj_qk<<<n_at * n_bt, 256, QKTile::LDS_BYTES, st>>>(rm, (const uint16_t *)a.wq, (const uint16_t *)a.wk,
+        launch_k(k_proj_qk, n_at * n_bt, 256, QKTile::LDS_BYTES, st, rm, (const uint16_t *)a.wq, (const uint16_t *)a.wk,
                                                                p.hd, qscale, n_at, n_bt, (uint16_t *)a.q,
                                                                (uint16_t *)a.k);
     }
@@ -227,11 +228,11 @@ hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, h
             hipError_t e = allow_lds(k_proj_v<true>, VTile<true>::LDS_BYTES, attr);
             if (e != hipSuccess) return e;
             const int n_bt = cdiv(p.hd, 64);
-            k_proj_v<true><<<n_at * n_bt, 256, VTile<true>::LDS_BYTES, st>>>(
+            launch_k(k_proj_v<true>, n_at * n_bt, 256, VTile<true>::LDS_BYTES, st, 
                 rm, (const uint16_t *)a.wv, p.hd, p.dh, a.n_seq, a.L, a.lpad, n_at, n_bt, zero_pad, (uint16_t *)a.vt);
         } else {
             const int n_bt = cdiv(p.hd, 128);
-            k_proj_v<false><<<n_at * n_bt, 256, VTile<false>::LDS_BYTES, st>>>(
+            launch_k(k_proj_v<false>, n_at * n_bt, 256, VTile<false>::LDS_BYTES, st, 
                 rm, (const uint16_t *)a.wv, p.hd, p.dh, a.n_seq, a.L, a.lpad, n_at, n_bt, zero_pad, (uint16_t *)a.vt);
         }
     }
@@ -291,7 +292,7 @@ hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStre
     if (!a.wo16_ready) {
         StageScope _stage(st, "wo_f16");
         const long blocks = (n8 + 255) / 256;
-        k_to_f16<<<(unsigned)(blocks < 2048 ? blocks : 2048), 256, 0, st>>>((const uint4 *)a.wo, n8,
+        launch_k(k_to_f16, (unsigned)(blocks < 2048 ? blocks : 2048), 256, 0, st, (const uint4 *)a.wo, n8,
                                                                             (uint4 *)a.wo16);
     }
     StageScope _stage(st, "proj_out");
@@ -301,12 +302,12 @@ hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStre
         hipError_t e = allow_lds(k_proj_out<true>, OTile<true>::LDS_BYTES, attr);
         if (e != hipSuccess) return e;
         const int n_bt = cdiv(n_rows, 64);
-        k_proj_out<true><<<n_at * n_bt, 256, OTile<true>::LDS_BYTES, st>>>(
+        launch_k(k_proj_out<true>, n_at * n_bt, 256, OTile<true>::LDS_BYTES, st, 
             (const uint16_t *)a.o, n_rows, p.hd, (const uint16_t *)a.wo16, p.C, a.n_main, a.out_idx, n_at, n_bt,
             (uint16_t *)a.y, (uint16_t *)a.y_ctx);
     } else {
         const int n_bt = cdiv(n_rows, 128);
-        k_proj_out<false><<<n_at * n_bt, 256, OTile<false>::LDS_BYTES, st>>>(
+        launch_k(k_proj_out<false>, n_at * n_bt, 256, OTile<false>::LDS_BYTES, st, 
             (const uint16_t *)a.o, n_rows, p.hd, (const uint16_t *)a.wo16, p.C, a.n_main, a.out_idx, n_at, n_bt,
             (uint16_t *)a.y, (uint16_t *)a.y_ctx);
     }

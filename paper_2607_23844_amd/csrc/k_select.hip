@@ -8,6 +8,7 @@
 // to the smallest candidate positions (ascending global id), so exactly R
 // are cached.  No floating-point atomics; integer LDS histograms only.
 #include "oc_internal.h"
+#include "oc_launch.h"
 #include "oc_device.h"
 #include "oc_block.h"
 #include "oc_groups.h"
@@ -257,7 +258,7 @@ hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_
                          int32_t *flag, int32_t *mtok, hipStream_t st) {
     {
         StageScope _stage(st, "select");
-        k_select<false><<<p.n_groups, SEL_THREADS, 0, st>>>(node_max, node_idx, nullptr, nullptr, nullptr, nullptr,
+        launch_k(k_select<false>, p.n_groups, SEL_THREADS, 0, st, node_max, node_idx, nullptr, nullptr, nullptr, nullptr,
                                                             group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max,
                                                             flag, mtok, nullptr, nullptr, nullptr, p.N, p.seq_len);
     }
@@ -271,7 +272,7 @@ hipError_t launch_select_packed(const Plan &p, const int32_t *units, const unsig
     if (compact && !select_compacts(p)) return hipErrorInvalidValue;
     {
         StageScope _stage(st, "select");
-        k_select<true><<<p.n_groups, SEL_THREADS, 0, st>>>(nullptr, nullptr, node_pack, inv, node_max, node_idx,
+        launch_k(k_select<true>, p.n_groups, SEL_THREADS, 0, st, nullptr, nullptr, node_pack, inv, node_max, node_idx,
                                                            group_map(p, units), p.n_groups, p.n_src_max,
                                                            p.n_dst_max, flag, mtok, kept_idx, cached_idx, rmap, p.N,
                                                            p.seq_len);

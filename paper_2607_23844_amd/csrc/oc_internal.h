@@ -47,14 +47,13 @@ struct AttnWs { size_t q, k, o, v, wo16, bytes; int lpad; };
 AttnWs attn_ws(const Plan &p, int n_seq, int L, size_t base);
 int gram_blocks(const Plan &p);
 
-// Stage timing: when a timer is attached to the calling thread, the kernels
-// launched between stage_begin and stage_end are bracketed by HIP events on
-// the launch stream (oc_timer.cpp).
+// Stage timing: while a timer is attached to the calling thread, the
+// kernels launched (launch_k, oc_launch.h) inside a StageScope are timed
+// under its name (oc_timer.cpp).
 struct StageScope {
     StageScope(hipStream_t st, const char *name);
     ~StageScope();
-    int slot;
-    hipStream_t st;
+    int prev;
 };
 
 // ---- launchers (k_*.hip) ---------------------------------------------------

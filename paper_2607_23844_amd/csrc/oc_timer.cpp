@@ -1,5 +1,7 @@
-// Stage timing: caller-owned HIP event pairs around each kernel launch
-// (see oc_timer_* in oc.h).  The attached timer is thread-local.
+// Stage timing (see oc_timer_* in oc.h): each kernel launched while a timer
+// is attached gets a pair of the timer's HIP events, which the runtime
+// stamps when the kernel starts and when it ends (oc_launch.h).  The
+// attached timer and the current stage are thread-local.
 #include "../../include/oc.h"
 #include "oc_internal.h"
 
@@ -31,31 +33,32 @@ int stage_index(oc_timer *t, const char *name) {
 
 namespace oc {
 
-StageScope::StageScope(hipStream_t stream, const char *name) : slot(-1), st(stream) {
+// A StageScope names the stage of the launches made inside it.
+thread_local int g_stage = -1;
+
+StageScope::StageScope(hipStream_t, const char *name) : prev(g_stage) {
     oc_timer *t = g_timer;
-    if (!t || t->failed) return;
+    if (t && !t->failed) g_stage = stage_index(t, name);
+}
+
+StageScope::~StageScope() { g_stage = prev; }
+
+bool timed_launch_events(hipStream_t, hipEvent_t *start, hipEvent_t *stop) {
+    oc_timer *t = g_timer;
+    if (!t || t->failed || g_stage < 0) return false;
     if (t->used == t->recs.size()) {
         oc_timer::Rec r{0, nullptr, nullptr};
         if (hipEventCreate(&r.a) != hipSuccess || hipEventCreate(&r.b) != hipSuccess) {
             t->failed = true;
-            return;
+            return false;
         }
         t->recs.push_back(r);
     }
-    oc_timer::Rec &r = t->recs[t->used];
-    r.stage = stage_index(t, name);
-    if (hipEventRecord(r.a, st) != hipSuccess) {
-        t->failed = true;
-        return;
-    }
-    slot = (int)t->used++;
-}
-
-StageScope::~StageScope() {
-    if (slot < 0) return;
-    oc_timer *t = g_timer;
-    if (!t || (size_t)slot >= t->recs.size()) return;
-    if (hipEventRecord(t->recs[slot].b, st) != hipSuccess) t->failed = true;
+    oc_timer::Rec &r = t->recs[t->used++];
+    r.stage = g_stage;
+    *start = r.a;
+    *stop = r.b;
+    return true;
 }
 
 }  // namespace oc
