@@ -386,23 +386,36 @@ def decide(x: np.ndarray, shape: LayerShape, cfg: CacheCfg, no_skip: bool = Fals
         raise ValueError(cfg.gran)
 
     node_max, node_idx, cached = [], [], []
-    fcached = forced.get("cached")
-    fmatch = forced.get("match", {})
     for g in groups:
         if len(g.src) == 0:
             nm, ni = np.zeros(0), np.zeros(0, dtype=np.int64)
         else:
             _, (nm, ni) = _match_group(x, g)
-        ni = np.array([fmatch.get(int(s), int(v)) for s, v in zip(g.src, ni)], dtype=np.int64)
         node_max.append(nm)
-        node_idx.append(ni)
-        if fcached is not None:
-            c = sorted(i for i in g.src if i in fcached)
+        node_idx.append(np.asarray(ni, dtype=np.int64))
+        cached.append(select_cached(nm, g.src, g.R))
+    dec = Decisions(groups, node_max, node_idx, cached, **dec_frame)
+    return force_decisions(dec, forced.get("cached"), forced.get("match"))
+
+
+def force_decisions(dec: Decisions, cached: Optional[set] = None, match: Optional[dict] = None) -> Decisions:
+    """The decisions with, for parity tests only, some candidates' matched
+    representative (``match``: item -> rep id) and the cached set of every
+    group (``cached``: item ids, the group's budget kept) replaced."""
+    if cached is None and not match:
+        return dec
+    match = match or {}
+    node_idx = [np.array([match.get(int(s), int(v)) for s, v in zip(g.src, ni)], dtype=np.int64)
+                for g, ni in zip(dec.groups, dec.node_idx)]
+    sel = dec.cached
+    if cached is not None:
+        sel = []
+        for g in dec.groups:
+            c = sorted(i for i in g.src if i in cached)
             assert len(c) == g.R, "forced selection must keep the group's budget"
-        else:
-            c = select_cached(nm, g.src, g.R)
-        cached.append(c)
-    return Decisions(groups, node_max, node_idx, cached, **dec_frame)
+            sel.append(c)
+    return Decisions(dec.groups, dec.node_max, node_idx, sel, dec.frame_group, dec.frame_max, dec.frame_idx,
+                     dec.frame_cached_order, dec.pairs, dec.frame_sim)
 
 
 # ----------------------------------------------------------------------------
@@ -483,6 +496,27 @@ def multi_head_attention(X: np.ndarray, wq: np.ndarray, wk: np.ndarray, wv: np.n
     heads concatenated, then the output projection Wo^T.  No bias,
     normalisation or positional term."""
     Q = X @ wq.T
+    K = X @ wk.T
+    V = X @ wv.T
+    O = np.empty_like(Q)
+    scale = 1.0 / math.sqrt(head_dim)
+    for h in range(heads):
+        sl = slice(h * head_dim, (h + 1) * head_dim)
+        s = (Q[:, sl] @ K[:, sl].T) * scale
+        s = s - s.max(axis=1, keepdims=True)
+        p = np.exp(s)
+        p = p / p.sum(axis=1, keepdims=True)
+        O[:, sl] = p @ V[:, sl]
+    return O @ wo.T
+
+
+def attention_rows(X: np.ndarray, wq: np.ndarray, wk: np.ndarray, wv: np.ndarray, wo: np.ndarray,
+                   heads: int, head_dim: int, rows: Sequence[int]) -> np.ndarray:
+    """The rows ``rows`` of multi_head_attention(X, ...): the same definition
+    with the queries restricted to those tokens, keys and values over all of
+    X.  Lets a check of a very long sequence compute a sample of outputs."""
+    rows = np.asarray(rows, dtype=np.int64)
+    Q = X[rows] @ wq.T
     K = X @ wk.T
     V = X @ wv.T
     O = np.empty_like(Q)

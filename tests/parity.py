@@ -150,6 +150,37 @@ def check_frame_stage(x64, osh, ocf, dec: O.Decisions, fmax, fidx, pairs):
     return dict(frame_order=g_order, pairs=[(int(s), int(dd)) for s, dd in pairs])
 
 
+def decision_parity(x64, osh, ocf, tr, valid):
+    """Matching and selection of one oc_layer_cached call (its trace) against
+    the oracle; returns the oracle's decisions with the library's in-band
+    choices forced on them, the forcing, and statistics."""
+    no_skip = (not valid) and ocf.cold == O.COLD_FULL
+    forced = {}
+    dec = O.decide(x64, osh, ocf, no_skip=no_skip)
+    if ocf.gran == O.FRAME_TOKEN and not no_skip:
+        forced.update(check_frame_stage(x64, osh, ocf, dec, tr["frame_max"].cpu().numpy(),
+                                        tr["frame_idx"].cpu().numpy(), tr["pairs"].cpu().numpy()))
+        if forced["frame_order"] != list(dec.frame_cached_order) or \
+                [tuple(p) for p in forced["pairs"]] != [tuple(p) for p in dec.pairs]:
+            dec = O.decide(x64, osh, ocf, no_skip=no_skip, forced=dict(forced))
+    kind = "block" if ocf.gran == O.BLOCK else ("frame" if ocf.gran == O.FRAME else "token")
+    nm = tr["node_max"].cpu().numpy()
+    ni = tr["node_idx"].cpu().numpy()
+    ov, worst_nm = check_match(x64, dec, nm, ni, kind)
+    cached_idx = tr["cached_idx"].cpu().numpy()
+    items = gpu_cached_items(ocf.gran, cached_idx, osh.N)
+    n_band = check_selection(dec, items)
+    forced.update(cached=items, match=ov)
+    dec = O.force_decisions(dec, items, ov)
+    return dec, forced, dict(node_max_err=worst_nm, in_band=n_band, idx_overrides=len(ov))
+
+
+def check_maps(tr, kept_idx, cached_idx, restore_map):
+    np.testing.assert_array_equal(tr["kept_idx"].cpu().numpy(), kept_idx)
+    np.testing.assert_array_equal(tr["cached_idx"].cpu().numpy(), cached_idx)
+    np.testing.assert_array_equal(tr["restore_map"].cpu().numpy(), restore_map)
+
+
 def layer_step_parity(wl, x_np, sh, cf, osh, ocf, cache, ws, ora_cache, valid, ctx_dev=None, ctx64=None,
                       W=None, W64=None):
     """One oc_layer_cached step against the oracle (with in-band forcing).
@@ -160,26 +191,9 @@ def layer_step_parity(wl, x_np, sh, cf, osh, ocf, cache, ws, ora_cache, valid, c
     y, y_ctx, tr = oc.layer_cached(x, W, cache, sh, cf, ctx=ctx_dev, ws=ws, trace=True)
     torch.cuda.synchronize()
     x64 = wl.f64(x_np).reshape(osh.F, osh.N, osh.C)
-    no_skip = (not valid) and ocf.cold == O.COLD_FULL
-    forced = {}
-    if ocf.gran == O.FRAME_TOKEN and not no_skip:
-        dec0 = O.decide(x64, osh, ocf)
-        forced.update(check_frame_stage(x64, osh, ocf, dec0, tr["frame_max"].cpu().numpy(),
-                                        tr["frame_idx"].cpu().numpy(), tr["pairs"].cpu().numpy()))
-    dec = O.decide(x64, osh, ocf, no_skip=no_skip, forced=dict(forced))
-    kind = "block" if ocf.gran == O.BLOCK else ("frame" if ocf.gran == O.FRAME else "token")
-    nm = tr["node_max"].cpu().numpy()
-    ni = tr["node_idx"].cpu().numpy()
-    ov, worst_nm = check_match(x64, dec, nm, ni, kind)
-    cached_idx = tr["cached_idx"].cpu().numpy()
-    items = gpu_cached_items(ocf.gran, cached_idx, osh.N)
-    n_band = check_selection(dec, items)
-    forced.update(cached=items, match=ov)
+    _, forced, st = decision_parity(x64, osh, ocf, tr, valid)
     res = O.layer_step(x64, ctx64, W64, osh, ocf, ora_cache, valid, forced=forced)
-    np.testing.assert_array_equal(tr["kept_idx"].cpu().numpy(), res.kept_idx)
-    np.testing.assert_array_equal(np.sort(cached_idx), res.cached_idx)
-    np.testing.assert_array_equal(cached_idx, res.cached_idx)
-    np.testing.assert_array_equal(tr["restore_map"].cpu().numpy(), res.restore_map)
+    check_maps(tr, res.kept_idx, res.cached_idx, res.restore_map)
     err = rel_err(to_f64(y).reshape(res.y.shape), res.y)
     tol = TOL[wl.dtype]
     assert err <= tol, f"layer output error {err:.3g} > {tol}"
@@ -187,4 +201,56 @@ def layer_step_parity(wl, x_np, sh, cf, osh, ocf, cache, ws, ora_cache, valid, c
         e2 = rel_err(to_f64(y_ctx), res.y_ctx)
         assert e2 <= tol, f"context output error {e2:.3g} > {tol}"
         err = max(err, e2)
-    return res, dict(err=err, node_max_err=worst_nm, in_band=n_band, idx_overrides=len(ov))
+    st.update(err=err)
+    return res, st
+
+
+def sampled_outputs(x64, W64, osh, seqs, kept_idx, restore_map, positions, y_prev):
+    """Oracle layer outputs at the given positions only: a retained position
+    (or, on a cold step, a cached one mapped to a retained row) is computed by
+    attention restricted to that query over its whole sequence; a position
+    restored from the cache takes y_prev (the previous step's values at the
+    same positions)."""
+    xf = x64.reshape(-1, osh.C)
+    where = {}
+    for qi, sq in enumerate(seqs):
+        for j, p in enumerate(sq):
+            where[p] = (qi, j)
+    out = np.empty((len(positions), osh.C))
+    need = {}
+    for i, p in enumerate(positions):
+        r = int(restore_map[p])
+        if r >= 0:
+            qi, j = where[int(kept_idx[r])]
+            need.setdefault(qi, []).append((i, j))
+        else:
+            assert y_prev is not None, "position restored from an empty cache"
+            out[i] = y_prev[i]
+    for qi, lst in need.items():
+        X = xf[np.asarray(seqs[qi], dtype=np.int64)]
+        rows = [j for _, j in lst]
+        Y = O.attention_rows(X, W64["wq"], W64["wk"], W64["wv"], W64["wo"], osh.heads, osh.head_dim, rows)
+        for (i, _), yrow in zip(lst, Y):
+            out[i] = yrow
+    return out
+
+
+def layer_step_sampled_parity(wl, x_np, sh, cf, osh, ocf, cache, ws, valid, W, W64, positions, y_prev):
+    """One oc_layer_cached step of a layer too large for the full oracle:
+    decisions and maps checked in full, outputs at the sampled positions.
+    Returns the oracle values there and statistics."""
+    x = dev_tensor(wl, x_np)
+    y, _, tr = oc.layer_cached(x, W, cache, sh, cf, ws=ws, trace=True)
+    torch.cuda.synchronize()
+    x64 = wl.f64(x_np).reshape(osh.F, osh.N, osh.C)
+    dec, _, st = decision_parity(x64, osh, ocf, tr, valid)
+    seqs = O.build_sequences(osh, ocf, dec)
+    kept_idx, cached_idx, rmap = O.kept_and_map(osh, ocf, dec, seqs, valid)
+    check_maps(tr, kept_idx, cached_idx, rmap)
+    ref = sampled_outputs(x64, W64, osh, seqs, kept_idx, rmap, positions, y_prev)
+    got = to_f64(y).reshape(-1, osh.C)[positions]
+    err = rel_err(got, ref)
+    tol = TOL[wl.dtype]
+    assert err <= tol, f"sampled layer output error {err:.3g} > {tol}"
+    st.update(err=err, n_kept=len(kept_idx), n_seq=len(seqs))
+    return ref, st

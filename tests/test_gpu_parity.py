@@ -15,8 +15,8 @@ from oc_synth import make_workload, small_workload
 from oracle import oc_oracle as O
 import paper_2607_23844_amd as oc
 
-from parity import (TOL, dev_tensor, layer_step_parity, rel_err, shapes, to_f64, weights_dev, weights_f64,
-                    check_match, group_margins)
+from parity import (TOL, dev_tensor, layer_step_parity, layer_step_sampled_parity, rel_err, shapes, to_f64,
+                    weights_dev, weights_f64, check_match, group_margins)
 
 pytestmark = pytest.mark.gpu
 
@@ -233,3 +233,54 @@ def test_latte_spatial_planted_chain():
 def test_latte_temporal_chain():
     wl = make_workload("latte_temporal", 2)
     chain(wl, 2)
+
+
+# ---------------------------------------------------------------------------
+# SVD-XT-like U-Net level at full size (25 frames of 72x128 tokens, C=320):
+# decisions and maps in full, outputs on a seeded sample of positions
+# ---------------------------------------------------------------------------
+def sampled_chain(wl, n_steps, n_sample=256, seed=11):
+    sh, cf, osh, ocf = shapes(wl)
+    dev = torch.device("cuda:0")
+    ws = oc.workspace(sh, cf, dev)
+    cache = oc.LayerCache(sh, dev)
+    W, W64 = weights_dev(wl), weights_f64(wl)
+    rng = np.random.default_rng(seed)
+    positions = np.sort(rng.choice(osh.F * osh.N, n_sample, replace=False))
+    y_prev, valid, stats = None, False, []
+    for s in range(n_steps):
+        _say(f"  step {s} of {wl.name} gran={cf.gran} r={cf.r} rf={cf.r_frame} k={cf.patch_k} (sampled outputs)")
+        y_prev, st = layer_step_sampled_parity(wl, wl.steps[s], sh, cf, osh, ocf, cache, ws, valid, W, W64,
+                                               positions, y_prev)
+        _say(f"    {st}")
+        stats.append(st)
+        valid = True
+    return stats
+
+
+@pytest.mark.parametrize("name", ["svdxt_level_planted", "svdxt_level", "svdxt_level_k4"])
+def test_svdxt_level_spatial_sampled(name):
+    wl = make_workload(name, 2)
+    sampled_chain(wl, 2)
+
+
+def test_svdxt_level_temporal_full_sampled():
+    """The level's uncached temporal layer (its own weights): 9216 sequences
+    of 25 frames, checked at a seeded sample of positions."""
+    wl = make_workload("svdxt_level", 2)
+    tw = wl.t_weights
+    sh = oc.Shape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, 0, wl.dtype)
+    cf = oc.Cfg("block", 0.0, 0.0, 1, "matched")
+    x = dev_tensor(wl, wl.steps[1])
+    y, _ = oc.attn_full(x, weights_dev(wl, tw), sh, cf)
+    torch.cuda.synchronize()
+    x64 = wl.f64(wl.steps[1]).reshape(wl.F, wl.H * wl.W, wl.C)
+    W64 = weights_f64(wl, tw)
+    rng = np.random.default_rng(12)
+    ns = np.sort(rng.choice(wl.H * wl.W, 96, replace=False))
+    got = to_f64(y).reshape(wl.F, wl.H * wl.W, wl.C)[:, ns, :]
+    ref = np.stack([O.multi_head_attention(x64[:, n, :], W64["wq"], W64["wk"], W64["wv"], W64["wo"], wl.heads,
+                                           wl.head_dim) for n in ns], axis=1)
+    err = rel_err(got, ref)
+    _say(f"  temporal layer sampled error {err:.3g}")
+    assert err <= TOL[wl.dtype]

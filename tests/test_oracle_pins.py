@@ -264,6 +264,25 @@ def test_mha_vs_torch_sdpa_fp64():
     np.testing.assert_allclose(Y, T, rtol=1e-11, atol=1e-11)
 
 
+def test_attention_rows_vs_torch_sdpa_fp64():
+    """Row-restricted attention (used to sample outputs of long sequences)
+    against torch's scaled_dot_product_attention on the same rows."""
+    rng = np.random.default_rng(4)
+    L, C, heads, dh = 41, 16, 2, 8
+    X = rng.standard_normal((L, C))
+    wq, wk, wv = rng.standard_normal((3, heads * dh, C)) * 0.4
+    wo = rng.standard_normal((C, heads * dh)) * 0.4
+    rows = [0, 7, 19, 40, 7]
+    Y = O.attention_rows(X, wq, wk, wv, wo, heads, dh, rows)
+    Xt = torch.tensor(X)
+    q = torch.nn.functional.linear(Xt, torch.tensor(wq)).view(L, heads, dh).transpose(0, 1)
+    k = torch.nn.functional.linear(Xt, torch.tensor(wk)).view(L, heads, dh).transpose(0, 1)
+    v = torch.nn.functional.linear(Xt, torch.tensor(wv)).view(L, heads, dh).transpose(0, 1)
+    o = torch.nn.functional.scaled_dot_product_attention(q[None], k[None], v[None])[0]
+    T = torch.nn.functional.linear(o.transpose(0, 1).reshape(L, heads * dh), torch.tensor(wo)).numpy()
+    np.testing.assert_allclose(Y, T[rows], rtol=1e-11, atol=1e-11)
+
+
 def test_attention_permutation_equivariance():
     rng = np.random.default_rng(4)
     L, C, heads, dh = 11, 8, 2, 4
