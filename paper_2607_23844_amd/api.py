@@ -272,8 +272,9 @@ def attn_full(x: torch.Tensor, weights: Dict[str, torch.Tensor], shape: Shape, c
 
 
 class StageTimer:
-    """Per-stage kernel time from HIP events the library records around each
-    launch while this timer is attached to the calling thread."""
+    """Per-stage kernel time while this timer is attached to the calling
+    thread: every library kernel is launched with a pair of the timer's HIP
+    events, stamped by the runtime at the kernel's start and end."""
 
     def __init__(self):
         self._t = C.c_void_p()

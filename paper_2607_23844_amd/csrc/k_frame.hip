@@ -1,8 +1,9 @@
 // Frame stage (OmniCache §3.2.2 Frame Cache; §3.2.3 frame-pair metadata):
 // the F x F Gram matrix of whole-frame descriptors (N*C values each) on
-// MFMA with a deterministic split-K reduction, then frame similarities,
-// best matches, the selection of the most redundant odd frames and their
-// one-to-one pairing with even frames.
+// MFMA with a deterministic split-K reduction (per-block partials, then one
+// wave per Gram entry summing them in fp64 in a fixed order), then frame
+// similarities, best matches, the selection of the most redundant odd frames
+// and their one-to-one pairing with even frames.
 #include "oc_internal.h"
 #include "oc_launch.h"
 #include "oc_device.h"
@@ -28,7 +29,8 @@ int gram_blocks(const Plan &p) {
 // Partial Gram of frames over k in this block's range; lane l of a wave feeds
 // frame (l % 16) (+16 for the second tile) and k chunks [g*16, g*16+8) and
 // [g*16+8, g*16+16) of each 64-wide step (g = l / 16); the same fragment is
-// both MFMA operands, so the result is X X^T.
+// both MFMA operands, so the result is X X^T.  Entry (m, n) of block b goes
+// to part[(m*F + n) * n_blocks + b]: one entry's partials are contiguous.
 template <bool TWO>
 __global__ __launch_bounds__(256) void k_frame_gram(const uint16_t *__restrict__ x, int F, long D, int kw,
                                                      float *__restrict__ part) {
@@ -79,11 +81,12 @@ __global__ __launch_bounds__(256) void k_frame_gram(const uint16_t *__restrict__
         }
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < FMAX * FMAX; e += blockDim.x) {
-        float s = red[0][e];
+    for (int e = threadIdx.x; e < F * F; e += blockDim.x) {
+        const int src = (e / F) * FMAX + e % F;
+        float s = red[0][src];
 #pragma unroll
-        for (int w = 1; w < GRAM_WAVES; ++w) s += red[w][e];
-        part[(long)blockIdx.x * FMAX * FMAX + e] = s;
+        for (int w = 1; w < GRAM_WAVES; ++w) s += red[w][src];
+        part[(long)e * gridDim.x + blockIdx.x] = s;
     }
 }
 
@@ -100,24 +103,46 @@ __global__ void k_frame_gram_f32(const float *__restrict__ x, int F, long D, flo
         if ((int)threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
         __syncthreads();
     }
-    if (threadIdx.x == 0) part[i * FMAX + j] = (float)red[0];
+    if (threadIdx.x == 0) part[i * F + j] = (float)red[0];
 }
 
-// Deterministic fp64 sum of the partial Grams, frame cosines, best matches
-// of odd frames, and (pairing mode) selection, greedy pairing and the
-// attention-unit table.  One block.
-__global__ __launch_bounds__(1024) void k_frame_final(const float *__restrict__ part, int n_part, int F, int R_f,
+// Gram entry e = sum of its n_part partials, in fp64, one wave per entry:
+// lane l adds partials l, l+64, ... in order, then a fixed butterfly.
+__global__ __launch_bounds__(256) void k_frame_reduce(const float *__restrict__ part, int n_part, int n_entries,
+                                                      double *__restrict__ gram) {
+    const int lane = threadIdx.x & 63;
+    const int e = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (e >= n_entries) return;
+    const float *pe = part + (long)e * n_part;
+    double s = 0.0;
+    for (int b = lane; b < n_part; b += 64) s += (double)pe[b];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+    if (lane == 0) gram[e] = s;
+}
+
+// Frame cosines from the Gram matrix, best matches of odd frames (one
+// thread each), the R_f most redundant odd frames by rank (largest
+// similarity first, smallest frame on ties), and then either the Frame Cache
+// flags (flag / mtok per frame, when given) or, in pairing mode, the greedy
+// one-to-one pairing in selection order (a wave arg-max over the free even
+// frames per step) and the attention-unit table.  One block, F <= 32.
+__global__ __launch_bounds__(1024) void k_frame_final(const double *__restrict__ gram, int F, int R_f,
                                                       int pairing, double *__restrict__ fsim,
                                                       float *__restrict__ node_max, int32_t *__restrict__ node_idx,
                                                       int32_t *__restrict__ forder, int32_t *__restrict__ pairs,
-                                                      int32_t *__restrict__ units) {
+                                                      int32_t *__restrict__ units, int32_t *__restrict__ flag,
+                                                      int32_t *__restrict__ mtok) {
     __shared__ double G[FMAX * FMAX];
     __shared__ double cs[FMAX * FMAX];
+    __shared__ double bm[FMAX / 2];
+    __shared__ int bidx[FMAX / 2];
+    __shared__ int order[FMAX / 2];
     const int t = threadIdx.x;
+    const int n_src = F / 2, n_dst = (F + 1) / 2;
     if (t < FMAX * FMAX) {
-        double s = 0.0;
-        for (int b = 0; b < n_part; ++b) s += (double)part[(long)b * FMAX * FMAX + t];
-        G[t] = s;
+        const int i = t / FMAX, j = t % FMAX;
+        G[t] = (i < F && j < F) ? gram[i * F + j] : 0.0;
     }
     __syncthreads();
     if (t < FMAX * FMAX) {
@@ -131,73 +156,88 @@ __global__ __launch_bounds__(1024) void k_frame_final(const float *__restrict__ 
         fsim[t] = c;
     }
     __syncthreads();
-    if (t != 0) return;
-    const int n_src = F / 2, n_dst = (F + 1) / 2;
-    double bm[FMAX / 2];
-    for (int i = 0; i < n_src; ++i) {
-        const int s = 2 * i + 1;
+    if (t < n_src) {
+        const int s = 2 * t + 1;
         double best = -INFINITY;
         int bi = -1;
         for (int j = 0; j < n_dst; ++j) {
             const double c = cs[s * FMAX + 2 * j];
             if (c > best) { best = c; bi = 2 * j; }
         }
-        bm[i] = best;
-        node_max[i] = (float)best;
-        node_idx[i] = bi;
+        bm[t] = best;
+        bidx[t] = bi;
+        node_max[t] = (float)best;
+        node_idx[t] = bi;
+    }
+    __syncthreads();
+    bool sel = false;
+    if (t < n_src) {
+        int rank = 0;
+        for (int j = 0; j < n_src; ++j) rank += (bm[j] > bm[t] || (bm[j] == bm[t] && j < t)) ? 1 : 0;
+        sel = rank < R_f;
+        if (sel) {
+            order[rank] = 2 * t + 1;
+            forder[rank] = 2 * t + 1;
+        }
+    }
+    if (flag != nullptr && t < F) {
+        // Frame Cache: odd frame 2i+1 cached when selected, matched to its best even frame
+        const bool odd = t & 1;
+        bool c = false;
+        int m = -1;
+        if (odd) {
+            const int i = t >> 1;
+            int rank = 0;
+            for (int j = 0; j < n_src; ++j) rank += (bm[j] > bm[i] || (bm[j] == bm[i] && j < i)) ? 1 : 0;
+            c = rank < R_f;
+            m = c ? bidx[i] : -1;
+        }
+        flag[t] = c ? 1 : 0;
+        mtok[t] = m;
     }
     if (!pairing) return;
-    // the R_f most redundant odd frames, largest similarity first, smallest
-    // frame on ties
-    bool taken_src[FMAX / 2];
-    for (int i = 0; i < n_src; ++i) taken_src[i] = false;
+    __syncthreads();
+    if (t >= 64) return;
+    // wave 0: lane j stands for even frame 2j
+    const int lane = t;
+    bool taken = false;
+    int my_s = -1, my_d = -1;   // lane f < F: the pair whose smaller frame is f
+    unsigned long long in_pair = 0ull;
     for (int r = 0; r < R_f; ++r) {
-        int best = -1;
-        for (int i = 0; i < n_src; ++i)
-            if (!taken_src[i] && (best < 0 || bm[i] > bm[best])) best = i;
-        taken_src[best] = true;
-        forder[r] = 2 * best + 1;
+        const int s = order[r];
+        double v = (lane < n_dst && !taken) ? cs[s * FMAX + 2 * lane] : -INFINITY;
+        int ix = (lane < n_dst && !taken) ? lane : 64;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            const double v2 = __shfl_xor(v, o, 64);
+            const int i2 = __shfl_xor(ix, o, 64);
+            if (v2 > v || (v2 == v && i2 < ix)) { v = v2; ix = i2; }
+        }
+        const int d = 2 * ix;
+        if (lane == ix) taken = true;
+        if (lane == 0) {
+            pairs[2 * r] = s;
+            pairs[2 * r + 1] = d;
+        }
+        in_pair |= (1ull << s) | (1ull << d);
+        if (lane == min(s, d)) {
+            my_s = s;
+            my_d = d;
+        }
     }
-    // greedy one-to-one pairing in selection order
-    bool taken_dst[FMAX];
-    for (int f = 0; f < FMAX; ++f) taken_dst[f] = false;
-    bool in_pair[FMAX];
-    for (int f = 0; f < FMAX; ++f) in_pair[f] = false;
-    for (int r = 0; r < R_f; ++r) {
-        const int s = forder[r];
-        int bd = -1;
-        for (int j = 0; j < n_dst; ++j) {
-            const int d = 2 * j;
-            if (taken_dst[d]) continue;
-            if (bd < 0 || cs[s * FMAX + d] > cs[s * FMAX + bd]) bd = d;
-        }
-        taken_dst[bd] = true;
-        pairs[2 * r] = s;
-        pairs[2 * r + 1] = bd;
-        in_pair[s] = in_pair[bd] = true;
-    }
-    // attention units ordered by their smallest frame
-    int u = 0;
-    for (int f = 0; f < F; ++f) {
-        if (!in_pair[f]) {
-            units[2 * u] = f;
-            units[2 * u + 1] = -1;
-            ++u;
-            continue;
-        }
-        for (int r = 0; r < R_f; ++r) {
-            const int s = pairs[2 * r], d = pairs[2 * r + 1];
-            if (min(s, d) == f) {
-                units[2 * u] = s;
-                units[2 * u + 1] = d;
-                ++u;
-            }
-        }
+    // attention units ordered by their smallest frame: frame f starts a unit
+    // when it is in no pair or is the smaller frame of its pair
+    const bool starts = lane < F && (!((in_pair >> lane) & 1ull) || my_s >= 0);
+    const unsigned long long ballot = __builtin_amdgcn_ballot_w64(starts);
+    const int u = __builtin_popcountll(ballot & ((1ull << lane) - 1ull));
+    if (starts) {
+        units[2 * u] = my_s >= 0 ? my_s : lane;
+        units[2 * u + 1] = my_s >= 0 ? my_d : -1;
     }
 }
 
 hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, char *ws, float *node_max,
-                              int32_t *node_idx, hipStream_t st) {
+                              int32_t *node_idx, int32_t *flag, int32_t *mtok, hipStream_t st) {
     const long D = (long)p.N * p.C;
     int nb = gram_blocks(p);
     float *part = (float *)(ws + L.gram_part);
@@ -219,11 +259,18 @@ hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, cha
         }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    double *gram = (double *)(ws + L.fgram);
+    {
+        StageScope _stage(st, "frame_reduce");
+        launch_k(k_frame_reduce, (unsigned)cdiv(p.F * p.F, 4), 256, 0, st, (const float *)part, nb, p.F * p.F, gram);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
     {
         StageScope _stage(st, "frame_final");
-        launch_k(k_frame_final, 1, 1024, 0, st, part, nb, p.F, p.R_f, p.gran == 3 ? 1 : 0, (double *)(ws + L.fsim), node_max,
-                                          node_idx, (int32_t *)(ws + L.forder), (int32_t *)(ws + L.pairs),
-                                          (int32_t *)(ws + L.units));
+        launch_k(k_frame_final, 1, 1024, 0, st, (const double *)gram, p.F, p.R_f, p.gran == 3 ? 1 : 0,
+                 (double *)(ws + L.fsim), node_max, node_idx, (int32_t *)(ws + L.forder), (int32_t *)(ws + L.pairs),
+                 (int32_t *)(ws + L.units), flag, mtok);
     }
     return hipGetLastError();
 }

@@ -13,9 +13,11 @@
 namespace oc {
 
 // ----------------------------------------------------------------------------
-// inverse L2 norms of item descriptors (one wave per item); blocks past the
-// norm blocks convert the output-projection weights bf16 -> fp16 (exact in
-// the fp16 normal range, saturating outside), 8 elements per thread
+// inverse L2 norms of item descriptors: one wave per item, or one block per
+// item for descriptors made of several segments (blocks: a position over all
+// frames); blocks past the norm blocks convert the output-projection weights
+// bf16 -> fp16 (exact in the fp16 normal range, saturating outside), 8
+// elements per thread
 // ----------------------------------------------------------------------------
 template <typename T>
 __global__ void k_inv_norm(const T *__restrict__ x, float *__restrict__ inv, int n_items, int n_sub,
@@ -30,8 +32,34 @@ __global__ void k_inv_norm(const T *__restrict__ x, float *__restrict__ inv, int
     for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n_pack; i += (long)norm_blocks * blockDim.x)
         pack[i] = 0ull;
     constexpr int VEC = 16 / sizeof(T);
-    const int item = blockIdx.x * (blockDim.x / WAVE) + (threadIdx.x / WAVE);
     const int lane = threadIdx.x & (WAVE - 1);
+    if (n_sub > 1) {
+        // block per item: the segments' 16-byte chunks spread over the block,
+        // partial sums reduced in a fixed order
+        __shared__ float wsum[4];
+        const int item = blockIdx.x;
+        const int cpr = C / VEC;
+        float ss = 0.f;
+        for (int q = threadIdx.x; q < n_sub * cpr; q += blockDim.x) {
+            const int sg = q / cpr, c = (q - sg * cpr) * VEC;
+            const uint4 v = *reinterpret_cast<const uint4 *>(x + sg * sub_stride + (long)item * C + c);
+            const T *e = reinterpret_cast<const T *>(&v);
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) {
+                const float f = Elem<T>::ld(e + j);
+                ss = fmaf(f, f, ss);
+            }
+        }
+        ss = wave_sum(ss);
+        if (lane == 0) wsum[threadIdx.x / WAVE] = ss;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            const float t = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
+            inv[item] = t > 0.f ? (float)(1.0 / sqrt((double)t)) : 0.f;
+        }
+        return;
+    }
+    const int item = blockIdx.x * (blockDim.x / WAVE) + (threadIdx.x / WAVE);
     if (item >= n_items) return;
     float ss = 0.f;
     for (int s = 0; s < n_sub; ++s) {
@@ -56,7 +84,7 @@ hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, unsigned lo
     const int n_items = p.kind == KIND_BLOCK ? p.N : p.F * p.N;
     const int n_sub = p.kind == KIND_BLOCK ? p.F : 1;
     const long sub = (long)p.N * p.C;
-    const int blocks = cdiv(n_items, 4);
+    const int blocks = n_sub > 1 ? n_items : cdiv(n_items, 4);
     const long n8 = (wo && wo16 && p.bf16) ? n_wo / 8 : 0;
     const int cvt_blocks = n8 > 0 ? (int)std::min<long>((n8 + 255) / 256, 1024) : 0;
     if (p.bf16)
@@ -95,6 +123,7 @@ __global__ __launch_bounds__(256) void k_match_mfma(const uint16_t *__restrict__
     // consecutive logical blocks: the representative tiles of one candidate tile
     const int at = lid % n_at, bt = (lid / n_at) % n_bt, g = lid / (n_at * n_bt);
     const GroupMap::Grp gr = gm.group(g);
+    if (bt * BB >= gr.nsrc) return;   // past this group's candidates (groups of one call differ in size)
     const uint16_t *rowsA[T::CA], *rowsB[T::CB];
 #pragma unroll
     for (int i = 0; i < T::CA; ++i) {
@@ -160,6 +189,178 @@ __global__ __launch_bounds__(256) void k_match_mfma(const uint16_t *__restrict__
     }
 }
 
+// Sweep variant for short descriptors, many candidate tiles and several
+// representative tiles: block (candidate tile bt, group g) keeps its
+// candidates' descriptors in LDS, streams every representative tile through
+// one continuous LDS-DMA pipeline, keeps each candidate's best (value,
+// position) in registers and publishes it once (one 64-bit atomic maximum per
+// candidate; no other block touches it).  The group's representative norms
+// are staged in LDS first (D <= SWEEP_MAX_D).
+template <int BA, int BB, int WA, int WB>
+__global__ __launch_bounds__(256) void k_match_sweep(const uint16_t *__restrict__ x, const float *__restrict__ inv,
+                                                      GroupMap gm, int G, int S, int D, int K, int seg_len,
+                                                      long sub_stride, long item_stride, int n_bt, int n_at,
+                                                      unsigned long long *__restrict__ node_pack) {
+    using T = DmaTile<BA, BB, WA, WB>;
+    extern __shared__ __align__(16) uint16_t lds[];
+    __shared__ float snorm[SWEEP_MAX_D];
+    __shared__ float sv[WA * BB];
+    __shared__ int si[WA * BB];
+    const int lid = xcd_remap(blockIdx.x, n_bt * G);
+    const int bt = lid % n_bt, g = lid / n_bt;
+    const GroupMap::Grp gr = gm.group(g);
+    if (bt * BB >= gr.nsrc) return;
+    for (int a = threadIdx.x; a < n_at * BA; a += 256) {
+        const int id = a < D ? gm.dst_id(gr, a) : -1;
+        snorm[a] = id >= 0 ? inv[id] : -1.f;
+    }
+    __syncthreads();
+    const uint16_t *rowsB[T::CB];
+#pragma unroll
+    for (int i = 0; i < T::CB; ++i) {
+        const int b = bt * BB + T::chunk_row(i);
+        const int id = b < S ? gm.src_id(gr, b) : -1;
+        rowsB[i] = id >= 0 ? x + (long)id * item_stride : nullptr;
+    }
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wa = wave / WB;
+    float bv[T::TB];
+    int bi[T::TB];
+#pragma unroll
+    for (int j = 0; j < T::TB; ++j) {
+        bv[j] = -INFINITY;
+        bi[j] = -1;
+    }
+    T tile;
+    auto rows_a = [&](int u, int i) -> const uint16_t * {
+        const int a = u * BA + T::chunk_row(i);
+        const int id = a < D ? gm.dst_id(gr, a) : -1;
+        return id >= 0 ? x + (long)id * item_stride : nullptr;
+    };
+    auto epi = [&](int u) {
+#pragma unroll
+        for (int j = 0; j < T::TB; ++j) {
+            float v = -INFINITY;
+            int ix = -1;
+#pragma unroll
+            for (int i = 0; i < T::TA; ++i)
+#pragma unroll
+                for (int g4 = 0; g4 < 4; ++g4)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int ga = u * BA + T::a_of(i, g4) + e;
+                        const float w = snorm[ga];
+                        if (w >= 0.f) argmax_merge(v, ix, tile.acc[i][j][4 * g4 + e] * w, ga);
+                    }
+            argmax_merge(v, ix, __shfl_xor(v, 32, WAVE), __shfl_xor(ix, 32, WAVE));
+            argmax_merge(bv[j], bi[j], v, ix);
+        }
+    };
+    tile.run_tiles_bres(lds, rows_a, rowsB, x, x, K, n_at, epi);
+    if (lane < 32) {
+#pragma unroll
+        for (int j = 0; j < T::TB; ++j) {
+            const int bl = T::b_of(j);
+            sv[wa * BB + bl] = bv[j];
+            si[wa * BB + bl] = bi[j];
+        }
+    }
+    __syncthreads();
+    for (int bl = threadIdx.x; bl < BB; bl += 256) {
+        float v = sv[bl];
+        int ix = si[bl];
+        for (int w = 1; w < WA; ++w) argmax_merge(v, ix, sv[w * BB + bl], si[w * BB + bl]);
+        const int b = bt * BB + bl;
+        if (b < S && ix >= 0) atomicMax(&node_pack[(long)g * S + b], pack_argmax(v, ix));
+    }
+}
+
+// Split-K variant for long descriptors and few tiles (Block Cache: a
+// position's descriptor spans all frames): block (tile, split) computes the
+// raw dot products over its K range (whole 64-steps inside one segment) and
+// stores them to part[split][g][b][a]; k_match_part_reduce sums the splits in
+// order, applies the representative norms and takes the arg-max.
+template <int BA, int BB, int WA, int WB, bool DMA>
+__global__ __launch_bounds__(256) void k_match_part(const uint16_t *__restrict__ x, GroupMap gm, int G, int S, int D,
+                                                     int kc, int seg_len, long sub_stride, long item_stride,
+                                                     int n_bt, int n_at, int n_split, float *__restrict__ part) {
+    using T = MatchTile<BA, BB, WA, WB, DMA>;
+    extern __shared__ __align__(16) uint16_t lds[];
+    const int total = n_bt * n_at * G * n_split;
+    const int lid = xcd_remap(blockIdx.x, total);
+    const int sp = lid % n_split, tl = lid / n_split;
+    const int at = tl % n_at, bt = (tl / n_at) % n_bt, g = tl / (n_at * n_bt);
+    const GroupMap::Grp gr = gm.group(g);
+    if (bt * BB >= gr.nsrc) return;
+    // K range of this split: inside one segment
+    const long k0 = (long)sp * kc;
+    const long off = seg_len > 0 ? (k0 / seg_len) * sub_stride + (k0 % seg_len) : k0;
+    const uint16_t *rowsA[T::CA], *rowsB[T::CB];
+#pragma unroll
+    for (int i = 0; i < T::CA; ++i) {
+        const int a = at * BA + T::chunk_row(i);
+        const int id = a < D ? gm.dst_id(gr, a) : -1;
+        rowsA[i] = id >= 0 ? x + (long)id * item_stride + off : nullptr;
+    }
+#pragma unroll
+    for (int i = 0; i < T::CB; ++i) {
+        const int b = bt * BB + T::chunk_row(i);
+        const int id = b < S ? gm.src_id(gr, b) : -1;
+        rowsB[i] = id >= 0 ? x + (long)id * item_stride + off : nullptr;
+    }
+    T tile;
+    if constexpr (DMA) tile.run(lds, rowsA, rowsB, x, x, kc, 0, 0);
+    else tile.run(lds, rowsA, rowsB, kc, 0, 0);
+    float *pp = part + ((long)sp * G + g) * S * D;
+#pragma unroll
+    for (int j = 0; j < T::TB; ++j) {
+        const int b = bt * BB + T::b_of(j);
+        if (b >= S) continue;
+#pragma unroll
+        for (int i = 0; i < T::TA; ++i)
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int a = at * BA + T::a_of(i, g4) + e;
+                    if (a < D) pp[(long)b * D + a] = tile.acc[i][j][4 * g4 + e];
+                }
+    }
+}
+
+// One block per (group, candidate): wave q sums the splits q, q+4, ... of
+// representatives a = lane + 64c, wave 0 adds the four partial sums in order,
+// applies the representative norm and keeps the arg-max.
+__global__ __launch_bounds__(256) void k_match_part_reduce(const float *__restrict__ part, int n_split, int G, int S,
+                                                            int D, const float *__restrict__ inv, GroupMap gm,
+                                                            unsigned long long *__restrict__ node_pack) {
+    __shared__ float red[4][64];
+    const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
+    const int g = blockIdx.x / S, b = blockIdx.x - g * S;
+    const GroupMap::Grp gr = gm.group(g);
+    if (gm.src_id(gr, b) < 0) return;
+    float bv = -INFINITY;
+    int bi = -1;
+    for (int a0 = 0; a0 < D; a0 += 64) {
+        const int a = a0 + lane;
+        float sum = 0.f;
+        if (a < D)
+            for (int sp = q; sp < n_split; sp += 4) sum += part[(((long)sp * G + g) * S + b) * D + a];
+        red[q][lane] = sum;
+        __syncthreads();
+        if (q == 0 && a < D) {
+            const int id = gm.dst_id(gr, a);
+            const float dot = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+            if (id >= 0) argmax_merge(bv, bi, dot * inv[id], a);
+        }
+        __syncthreads();
+    }
+    if (q != 0) return;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) argmax_merge(bv, bi, __shfl_xor(bv, o, WAVE), __shfl_xor(bi, o, WAVE));
+    if (lane == 0 && bi >= 0) node_pack[(long)g * S + b] = pack_argmax(bv, bi);
+}
+
 // fp32 similarity + arg-max (small fp32 layers): one thread per candidate.
 __global__ void k_match_f32(const float *__restrict__ x, const float *__restrict__ inv, GroupMap gm, int G, int S,
                             int D, int K, int seg_len, long sub_stride, long item_stride,
@@ -211,6 +412,14 @@ __global__ void k_match_unpack(const unsigned long long *__restrict__ node_pack,
     node_idx[i] = ix >= 0 ? gm.dst_id(gr, ix) : -1;
 }
 
+template <typename KernelPtr>
+static hipError_t allow_lds(KernelPtr k, size_t lds, bool &done) {
+    if (done || lds <= 65536) return hipSuccess;
+    const hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e == hipSuccess) done = true;
+    return e;
+}
+
 template <int BA, int BB, int WA, int WB, bool DMA>
 static hipError_t go_match(const Plan &p, const uint16_t *x, const float *inv, const GroupMap &gm, int K,
                            int seg_len, long sub_stride, long item_stride, unsigned long long *node_pack,
@@ -219,23 +428,54 @@ static hipError_t go_match(const Plan &p, const uint16_t *x, const float *inv, c
     const int G = p.n_groups, S = p.n_src_max, D = p.n_dst_max;
     const int n_bt = cdiv(S, BB), n_at = cdiv(D, BA);
     const size_t lds = T::LDS_BYTES;
-    if (lds > 65536) {
-        static bool attr = false;
-        if (!attr) {
-            const hipError_t e = hipFuncSetAttribute((const void *)k_match_mfma<BA, BB, WA, WB, DMA>,
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (e != hipSuccess) return e;
-            attr = true;
-        }
-    }
+    static bool attr = false;
+    hipError_t e = allow_lds(k_match_mfma<BA, BB, WA, WB, DMA>, lds, attr);
+    if (e != hipSuccess) return e;
     launch_k(k_match_mfma<BA, BB, WA, WB, DMA>, n_bt * n_at * G, 256, lds, st, x, inv, gm, G, S, D, K, seg_len,
-                                                                          sub_stride, item_stride, n_bt, n_at,
-                                                                          node_pack);
+             sub_stride, item_stride, n_bt, n_at, node_pack);
+    return hipGetLastError();
+}
+
+template <int BA, int BB, int WA, int WB>
+static hipError_t go_sweep(const Plan &p, const uint16_t *x, const float *inv, const GroupMap &gm, int K,
+                           int seg_len, long sub_stride, long item_stride, unsigned long long *node_pack,
+                           hipStream_t st) {
+    using T = DmaTile<BA, BB, WA, WB>;
+    const int G = p.n_groups, S = p.n_src_max, D = p.n_dst_max;
+    const int n_bt = cdiv(S, BB), n_at = cdiv(D, BA);
+    if (n_at * BA > SWEEP_MAX_D || K > SWEEP_MAX_K || seg_len != 0) return hipErrorInvalidValue;
+    const size_t lds = T::bres_lds_bytes(K);
+    static bool attr = false;
+    hipError_t e = allow_lds(k_match_sweep<BA, BB, WA, WB>, lds, attr);
+    if (e != hipSuccess) return e;
+    launch_k(k_match_sweep<BA, BB, WA, WB>, n_bt * G, 256, lds, st, x, inv, gm, G, S, D, K, seg_len,
+             sub_stride, item_stride, n_bt, n_at, node_pack);
+    return hipGetLastError();
+}
+
+template <int BA, int BB, int WA, int WB, bool DMA>
+static hipError_t go_split(const Plan &p, const MatchSplit &ms, const uint16_t *x, const float *inv,
+                           const GroupMap &gm, int seg_len, long sub_stride, long item_stride, float *part,
+                           unsigned long long *node_pack, hipStream_t st) {
+    using T = MatchTile<BA, BB, WA, WB, DMA>;
+    const int G = p.n_groups, S = p.n_src_max, D = p.n_dst_max;
+    const int n_bt = cdiv(S, BB), n_at = cdiv(D, BA);
+    const size_t lds = T::LDS_BYTES;
+    static bool attr = false;
+    hipError_t e = allow_lds(k_match_part<BA, BB, WA, WB, DMA>, lds, attr);
+    if (e != hipSuccess) return e;
+    launch_k(k_match_part<BA, BB, WA, WB, DMA>, n_bt * n_at * G * ms.n_split, 256, lds, st, x, gm, G, S, D, ms.kc,
+             seg_len, sub_stride, item_stride, n_bt, n_at, ms.n_split, part);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    launch_k(k_match_part_reduce, (unsigned)((long)G * S), 256, 0, st, (const float *)part, ms.n_split, G, S, D, inv,
+             gm, node_pack);
     return hipGetLastError();
 }
 
 hipError_t launch_match(const Plan &p, const void *x, const float *inv, const int32_t *units,
-                        unsigned long long *node_pack, float *node_max, int32_t *node_idx, hipStream_t st) {
+                        unsigned long long *node_pack, float *part, float *node_max, int32_t *node_idx,
+                        hipStream_t st) {
     const GroupMap gm = group_map(p, units);
     const int G = p.n_groups, S = p.n_src_max, D = p.n_dst_max;
     const bool block = p.kind == KIND_BLOCK;
@@ -247,26 +487,36 @@ hipError_t launch_match(const Plan &p, const void *x, const float *inv, const in
         StageScope _stage(st, "match");
         if (p.bf16) {
             const uint16_t *xb = (const uint16_t *)x;
-            // representative tile height by group size: 128, 64 or 32; large
-            // groups stream by LDS DMA when the K steps allow it
+            const MatchSplit ms = match_split(p);
             const bool dma = K % 64 == 0 && (seg_len == 0 || seg_len % 64 == 0);
             hipError_t e;
-            if (D > 64)
+            if (ms.n_split > 1) {
+                // long descriptors, few tiles: split K (64-row tiles)
+                e = go_split<64, 64, 2, 2, true>(p, ms, xb, inv, gm, seg_len, sub_stride, item_stride, part,
+                                                 node_pack, st);
+            } else if (D > 64 && dma && match_sweeps(p)) {
+                // many candidate tiles: each block sweeps all representative tiles
+                e = go_sweep<128, 128, 2, 2>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride, node_pack,
+                                                   st);
+            } else if (D > 64) {
+                // representative tile height by group size: 128, 64 or 32; large
+                // groups stream by LDS DMA when the K steps allow it
                 e = dma ? go_match<128, 128, 2, 2, true>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride,
                                                          node_pack, st)
                         : go_match<128, 64, 2, 2, false>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride,
                                                          node_pack, st);
-            else if (D > 32)
+            } else if (D > 32) {
                 e = go_match<64, 64, 2, 2, false>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride, node_pack,
                                                   st);
-            else
+            } else {
                 e = go_match<32, 128, 1, 4, false>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride, node_pack,
                                                    st);
+            }
             if (e != hipSuccess) return e;
         } else {
             dim3 grid(cdiv(S, 64), G);
             launch_k(k_match_f32, grid, 64, 0, st, (const float *)x, inv, gm, G, S, D, K, seg_len, sub_stride,
-                                             item_stride, node_pack);
+                     item_stride, node_pack);
         }
     }
     hipError_t e = hipGetLastError();

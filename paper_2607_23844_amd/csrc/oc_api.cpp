@@ -167,8 +167,13 @@ Layout make_layout(const Plan &p) {
     L.node_pack = take(GS * 8);
     L.node_max = take(GS * 4);
     L.node_idx = take(GS * 4);
+    {
+        const MatchSplit ms = match_split(p);
+        L.mpart = take(ms.n_split > 1 ? (size_t)ms.n_split * GS * p.n_dst_max * 4 : 0);
+    }
     const bool frames = p.gran == OC_GRAN_FRAME || p.gran == OC_GRAN_FRAME_TOKEN;
     L.gram_part = take(frames ? (size_t)gram_blocks(p) * 1024 * 4 : 0);
+    L.fgram = take(frames ? 1024 * 8 : 0);
     L.fsim = take(frames ? 1024 * 8 : 0);
     L.fmax = take(64 * 4);
     L.fidx = take(64 * 4);
@@ -238,13 +243,18 @@ oc_status run_match(const Plan &p, const Layout &L, const void *x, float *node_m
     if (frames) {
         float *fm = p.gran == OC_GRAN_FRAME ? node_max : at<float>(ws, L.fmax);
         int32_t *fi = p.gran == OC_GRAN_FRAME ? node_idx : at<int32_t>(ws, L.fidx);
-        HIP_TRY(launch_frame_stage(p, L, x, w, fm, fi, st), "frame stage");
+        // Frame Cache: the frame stage also writes the per-frame selection
+        const bool fsel = p.gran == OC_GRAN_FRAME;
+        HIP_TRY(launch_frame_stage(p, L, x, w, fm, fi, fsel ? at<int32_t>(ws, L.flag) : nullptr,
+                                   fsel ? at<int32_t>(ws, L.mtok) : nullptr, st),
+                "frame stage");
     }
     if (p.kind == KIND_FRAME) return OC_OK;
     unsigned long long *pack = at<unsigned long long>(ws, L.node_pack);
     HIP_TRY(launch_inv_norm(p, x, at<float>(ws, L.inv), pack, (long)p.n_groups * p.n_src_max, wo, wo16,
                             (long)p.C * p.hd, st), "inv_norm");
-    HIP_TRY(launch_match(p, x, at<float>(ws, L.inv), units_of(p, L, ws), pack, reduce ? node_max : nullptr,
+    HIP_TRY(launch_match(p, x, at<float>(ws, L.inv), units_of(p, L, ws), pack, at<float>(ws, L.mpart),
+                         reduce ? node_max : nullptr,
                          reduce ? node_idx : nullptr, st),
             "match");
     return OC_OK;
@@ -268,7 +278,8 @@ oc_status run_select(const Plan &p, const Layout &L, float *node_max, int32_t *n
                         "map matched");
             return OC_OK;
         }
-    } else {
+    } else if (!(from_pack && p.kind == KIND_FRAME)) {
+        // (Frame Cache in a layer call: the frame stage wrote the selection)
         HIP_TRY(launch_select(p, units, node_max, node_idx, at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok), st),
                 "select");
     }

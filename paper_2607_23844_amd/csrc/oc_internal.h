@@ -34,8 +34,8 @@ struct Plan {
 
 // Workspace carve-up (byte offsets from the caller's ws base).
 struct Layout {
-    size_t inv, node_pack, node_max, node_idx;
-    size_t gram_part, fsim, fmax, fidx, forder, pairs, units;
+    size_t inv, node_pack, node_max, node_idx, mpart;
+    size_t gram_part, fgram, fsim, fmax, fidx, forder, pairs, units;
     size_t flag, mtok, fcnt, kept, cached, rmap;
     size_t attn;             // start of the attention workspace (Q, K, O, V)
     size_t total;
@@ -66,11 +66,47 @@ struct StageScope {
 // fp16 into wo16, all in one launch.
 hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, unsigned long long *node_pack, long n_pack,
                            const void *wo, void *wo16, long n_wo, hipStream_t st);
-// node_max == nullptr: node_pack only (the selection unpacks it)
+// Similarity kernel choice (bf16): long descriptors over few 64x64 tiles
+// (Block Cache) split K into n_split ranges of kc elements, each inside one
+// segment of the descriptor, with fp32 partials [n_split][G][S][D] in the
+// workspace; many candidate tiles with several representative tiles sweep
+// the representatives per candidate tile; otherwise one block per tile pair.
+struct MatchSplit { int n_split, kc; };
+inline MatchSplit match_split(const Plan &p) {
+    MatchSplit m{1, 0};
+    if (!p.bf16 || p.kind == KIND_FRAME) return m;
+    const bool block = p.kind == KIND_BLOCK;
+    const int K = block ? p.F * p.C : p.C;
+    const int seg = block ? p.C : 0;
+    if (K % 64 != 0 || (seg > 0 && seg % 64 != 0)) return m;
+    const int nk = K / 64;
+    const long tiles = (long)((p.n_src_max + 63) / 64) * ((p.n_dst_max + 63) / 64) * p.n_groups;
+    if (tiles >= 128 || nk < 16) return m;
+    const long target = 256 / tiles;
+    int sps = (int)((nk + target - 1) / target);   // 64-steps per split
+    const int per_seg = seg > 0 ? seg / 64 : nk;
+    while (per_seg % sps != 0 || nk % sps != 0) ++sps;
+    if (nk / sps < 2) return m;
+    m.n_split = nk / sps;
+    m.kc = sps * 64;
+    return m;
+}
+constexpr int SWEEP_MAX_D = 4096;   // representatives per group for the sweep variant
+constexpr int SWEEP_MAX_K = 320;    // descriptor length it keeps in LDS (with the ring and norms: <= 160 KiB)
+inline bool match_sweeps(const Plan &p) {
+    const int n_bt = (p.n_src_max + 127) / 128, n_at = (p.n_dst_max + 127) / 128;
+    return p.bf16 && p.kind == KIND_TOKEN && p.C % 64 == 0 && p.C <= SWEEP_MAX_K && n_at >= 2 &&
+           n_at * 128 <= SWEEP_MAX_D && (long)n_bt * p.n_groups >= 512;
+}
+// node_max == nullptr: node_pack only (the selection unpacks it); part: the
+// split-K partials (match_split), unused otherwise
 hipError_t launch_match(const Plan &p, const void *x, const float *inv, const int32_t *units,
-                        unsigned long long *node_pack, float *node_max, int32_t *node_idx, hipStream_t st);
+                        unsigned long long *node_pack, float *part, float *node_max, int32_t *node_idx,
+                        hipStream_t st);
+// flag / mtok given (Frame Cache): the frame stage also writes the per-frame
+// selection, so no selection launch is needed
 hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, char *ws,
-                              float *node_max, int32_t *node_idx, hipStream_t st);
+                              float *node_max, int32_t *node_idx, int32_t *flag, int32_t *mtok, hipStream_t st);
 hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_max, const int32_t *node_idx,
                          int32_t *flag, int32_t *mtok, hipStream_t st);
 // selection straight from node_pack; node_max / node_idx are written as

@@ -39,6 +39,11 @@ class LayerRunner:
         self._c.valid = 0
         self._c.step = 0
 
+    def use_current_stream(self):
+        """Launch on torch's current stream from now on (e.g. under graph capture)."""
+        self._stream = _stream(self.cache.y)
+        self._args_tail = self._args_tail[:-1] + (self._stream,)
+
     def __call__(self, x: torch.Tensor) -> torch.Tensor:
         st = self._fn(C.byref(self._sh), C.byref(self._cf), x.data_ptr(), self._ctx_ptr, *self._args_tail)
         if st != 0:
@@ -64,6 +69,10 @@ class FullRunner:
         self._ctx_ptr = ctx.data_ptr() if ctx is not None else None
         self._tail = (C.byref(self._w), self.y.data_ptr(), self.y_ctx.data_ptr() if self.y_ctx is not None else None,
                       self.ws.data_ptr(), self.ws.numel(), _stream(self.y))
+
+    def use_current_stream(self):
+        """Launch on torch's current stream from now on (e.g. under graph capture)."""
+        self._tail = self._tail[:-1] + (_stream(self.y),)
 
     def __call__(self, x: torch.Tensor) -> torch.Tensor:
         st = self._fn(C.byref(self._sh), C.byref(self._cf), x.data_ptr(), self._ctx_ptr, *self._tail)
