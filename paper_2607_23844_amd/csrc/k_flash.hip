@@ -398,6 +398,130 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
         }
 }
 
+// Short sequences (at most 64 keys, e.g. temporal attention over frames):
+// one wave per (sequence, head), no LDS and no barriers.  The wave holds K
+// and Vt of the whole sequence in registers (KB blocks of 32 keys) and, per
+// block of 32 queries, computes S^T = K Q^T, the exact row maximum, P =
+// exp2(s - max) in fp16, the running sum of that fp16 P, and O^T = Vt P^T on
+// the same MFMA layouts as the long-sequence kernel.
+template <int DH, int KB>
+__global__ __launch_bounds__(256) void k_attn_short(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
+                                                     const uint16_t *__restrict__ Vt, uint16_t *__restrict__ O, int hd,
+                                                     int heads, int n_seq, int L, int Lk, int lpad) {
+    constexpr int DK = (DH + 15) / 16 * 16, NKS = DK / 16;
+    constexpr int DV = (DH + 31) / 32 * 32, NDB = DV / 32;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, ln = lane & 31, lg = lane >> 5;
+    const long unit = (long)blockIdx.x * 4 + wave;
+    if (unit >= (long)n_seq * heads) return;   // whole waves only; the kernel has no block barrier
+    const int h = (int)(unit % heads), s = (int)(unit / heads);
+    const long row0 = (long)s * L;
+    const uint16_t *vbase = Vt + ((long)h * n_seq + s) * DH * lpad;
+    auto ld = [](const uint16_t *p, bool ok) {
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (ok) v = *reinterpret_cast<const uint4 *>(p);
+        return __builtin_bit_cast(f16x8, v);
+    };
+    f16x8 kf[KB][NKS], vf[NDB][2 * KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+        const int key = kb * 32 + ln;
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+            const int d0 = ks * 16 + lg * 8;
+            kf[kb][ks] = ld(K + (row0 + key) * hd + h * DH + d0, key < Lk && d0 < DH);
+        }
+    }
+    // Vt positions whose key is past the end are zeroed here (the padding of
+    // Vt is not guaranteed for short sequences)
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int k4 = 0; k4 < 2 * KB; ++k4) {
+            const int d = db * 32 + ln;
+            f16x8 v = ld(vbase + (long)d * lpad + k4 * 16 + lg * 8, d < DH);
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (k4 * 16 + vt_key_of_pos(lg * 8 + e) >= Lk) v[e] = (_Float16)0.f;
+            vf[db][k4] = v;
+        }
+    const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
+    const int n_qb = (Lk + 31) / 32;
+    for (int qb = 0; qb < n_qb; ++qb) {
+        const int q = qb * 32 + ln;
+        f16x8 qf[NKS];
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+            const int d0 = ks * 16 + lg * 8;
+            qf[ks] = ld(Q + (row0 + q) * hd + h * DH + d0, q < Lk && d0 < DH);
+        }
+        f32x16 sc[KB];
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+            sc[kb] = f32x16{};
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks)
+                sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf[kb][ks], qf[ks], sc[kb], 0, 0, 0);
+        }
+        float m = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                if (kb * 32 + 8 * (i >> 2) + 4 * lg + (i & 3) >= Lk) sc[kb][i] = -INFINITY;
+                m = fmaxf(m, sc[kb][i]);
+            }
+        m = fmaxf(m, __shfl_xor(m, 32, 64));
+        f16x8 pf[2 * KB];
+        float l0 = 0.f, l1 = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+                f16x8 f;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) f[e] = (_Float16)__builtin_amdgcn_exp2f(sc[kb][8 * hf + e] - m);
+                pf[kb * 2 + hf] = f;
+                l0 = __builtin_amdgcn_fdot2(f.s01, ones, l0, false);
+                l1 = __builtin_amdgcn_fdot2(f.s23, ones, l1, false);
+                l0 = __builtin_amdgcn_fdot2(f.s45, ones, l0, false);
+                l1 = __builtin_amdgcn_fdot2(f.s67, ones, l1, false);
+            }
+        float lt = l0 + l1;
+        lt += __shfl_xor(lt, 32, 64);
+        f32x16 o[NDB];
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+            o[db] = f32x16{};
+#pragma unroll
+            for (int k4 = 0; k4 < 2 * KB; ++k4)
+                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[db][k4], pf[k4], o[db], 0, 0, 0);
+        }
+        if (q >= Lk) continue;
+        const float inv = 1.f / lt;
+        uint16_t *orow = O + (row0 + q) * hd + h * DH;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+                const int d = db * 32 + 8 * g4 + 4 * lg;
+                if (d >= DH) continue;
+                u16x4 v;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = f2h_bits(o[db][4 * g4 + e] * inv);
+                *reinterpret_cast<u16x4 *>(orow + d) = v;
+            }
+    }
+}
+
+template <int DH, int KB>
+static hipError_t go_short(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
+    const long waves = (long)a.n_seq * p.heads;
+    launch_k(k_attn_short<DH, KB>, (unsigned)((waves + 3) / 4), 256, 0, st, (const uint16_t *)a.q,
+             (const uint16_t *)a.k, (const uint16_t *)a.vt, (uint16_t *)a.o, p.hd, p.heads, a.n_seq, a.L, Lk,
+             a.lpad);
+    return hipGetLastError();
+}
+
 template <int DH, int NW, bool DMA>
 static hipError_t go(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
     const int n_qt = cdiv(Lk, 32 * NW);
@@ -416,13 +540,13 @@ static hipError_t go(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
     return hipGetLastError();
 }
 
-// Waves per block by sequence length: a short sequence gets one or two
-// waves (32 queries each) per block, a long one four (DMA-staged when the
-// head dim allows it).
+// By sequence length: up to 64 keys the register-only short kernel, else
+// four waves (32 queries each) per block, DMA-staged when the head dim
+// allows it.
 template <int DH>
 static hipError_t go_dh(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
-    if (Lk <= 32) return go<DH, 1, false>(p, a, Lk, st);
-    if (Lk <= 64) return go<DH, 2, false>(p, a, Lk, st);
+    if (Lk <= 32) return go_short<DH, 1>(p, a, Lk, st);
+    if (Lk <= 64) return go_short<DH, 2>(p, a, Lk, st);
     if constexpr (DH % 64 == 0) {
         if (flash_uses_dma(DH, Lk)) return go<DH, 4, true>(p, a, Lk, st);
     }

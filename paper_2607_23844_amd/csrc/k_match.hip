@@ -108,7 +108,7 @@ hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, unsigned lo
 // representative norm is applied before the arg-max, the candidate's own
 // norm (a positive constant per row) when unpacking.
 template <int BA, int BB, int WA, int WB, bool DMA>
-using MatchTile = typename std::conditional<DMA, DmaTile<BA, BB, WA, WB>, MfmaTile<BA, BB, WA, WB>>::type;
+using MatchTile = typename std::conditional<DMA, DmaTile<BA, BB, WA, WB, false, 2>, MfmaTile<BA, BB, WA, WB>>::type;
 
 template <int BA, int BB, int WA, int WB, bool DMA>
 __global__ __launch_bounds__(256) void k_match_mfma(const uint16_t *__restrict__ x, const float *__restrict__ inv,
@@ -501,8 +501,8 @@ hipError_t launch_match(const Plan &p, const void *x, const float *inv, const in
             } else if (D > 64) {
                 // representative tile height by group size: 128, 64 or 32; large
                 // groups stream by LDS DMA when the K steps allow it
-                e = dma ? go_match<128, 128, 2, 2, true>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride,
-                                                         node_pack, st)
+                e = dma ? go_match<128, 64, 2, 2, true>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride,
+                                                        node_pack, st)
                         : go_match<128, 64, 2, 2, false>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride,
                                                          node_pack, st);
             } else if (D > 32) {

@@ -14,10 +14,9 @@
 // Rows r < n_main come from x (through row_idx when given); rows after them
 // are the uncached context tokens of a single sequence.
 //
-// Engines: the V and output projections use the LDS-DMA tile (128 x 64)
-// when their K is a multiple of 64, the register-staged tile (128 x 128)
-// otherwise; the Q/K projection uses the register-staged tile (measured
-// faster at its shape).  Epilogues go through LDS: the tile is staged as
+// Engines: with K a multiple of 64 the LDS-DMA tile (Q/K: 128 x 128 double
+// buffered; V and output: 128 x 64, three stages), the register-staged tile
+// (128 x 128) otherwise.  Epilogues go through LDS: the tile is staged as
 // whole output rows and written in 16-byte chunks, so every store is a
 // contiguous run of a row (Vt rows included).
 //
@@ -99,14 +98,17 @@ static hipError_t allow_lds(KernelPtr k, size_t bytes, bool &done) {
 }
 
 // ---------------------------------------------------------------------------
-// Q, K: a in [0, 2*hd) are rows of wq then wk; b = batch rows.
+// Q, K: a in [0, 2*hd) are rows of wq then wk; b = batch rows.  The DMA
+// engine runs double-buffered here (two blocks per CU).
 // ---------------------------------------------------------------------------
-using QKTile = MfmaTile<128, 128, 2, 2>;
+template <bool DMA>
+using QKTile = typename std::conditional<DMA, DmaTile<128, 128, 2, 2, false, 2>, MfmaTile<128, 128, 2, 2>>::type;
 
+template <bool DMA>
 __global__ __launch_bounds__(256) void k_proj_qk(RowMap rm, const uint16_t *__restrict__ wq,
                                                  const uint16_t *__restrict__ wk, int hd, float qscale, int n_at,
                                                  int n_bt, uint16_t *__restrict__ Q, uint16_t *__restrict__ K) {
-    using T = QKTile;
+    using T = QKTile<DMA>;
     constexpr int BA = 128, BB = 128;
     extern __shared__ __align__(16) uint16_t lds[];
     int at, bt;
@@ -120,7 +122,7 @@ __global__ __launch_bounds__(256) void k_proj_qk(RowMap rm, const uint16_t *__re
 #pragma unroll
     for (int i = 0; i < T::CB; ++i) rowsB[i] = rm.row(bt * BB + T::chunk_row(i));
     T t;
-    t.run(lds, rowsA, rowsB, rm.C, 0, 0);
+    run_tile(t, lds, rowsA, rowsB, wq, rm.row(0), rm.C, typename std::conditional<DMA, DmaRows, RegRows>::type{});
     const int a0 = at * BA, b0 = bt * BB;
     stage_rows<BA>(t, lds, [&](float v, int a) { return f2h_bits(a0 + a < hd ? v * qscale : v); },
                    [](int a) { return a; });
@@ -214,9 +216,13 @@ hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, h
     {
         StageScope _stage(st, "proj_qk");
         const int n_at = cdiv(2 * p.hd, 128), n_bt = cdiv(rm.n_rows, 128);
-        launch_k(k_proj_qk, n_at * n_bt, 256, QKTile::LDS_BYTES, st, rm, (const uint16_t *)a.wq, (const uint16_t *)a.wk,
-                                                               p.hd, qscale, n_at, n_bt, (uint16_t *)a.q,
-                                                               (uint16_t *)a.k);
+        if (p.C % 64 == 0) {
+            launch_k(k_proj_qk<true>, n_at * n_bt, 256, QKTile<true>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
+                     (const uint16_t *)a.wk, p.hd, qscale, n_at, n_bt, (uint16_t *)a.q, (uint16_t *)a.k);
+        } else {
+            launch_k(k_proj_qk<false>, n_at * n_bt, 256, QKTile<false>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
+                     (const uint16_t *)a.wk, p.hd, qscale, n_at, n_bt, (uint16_t *)a.q, (uint16_t *)a.k);
+        }
     }
     {
         StageScope _stage(st, "proj_v");

@@ -4,7 +4,9 @@
 // operands travel global -> LDS with global_load_lds (16 bytes per lane, no
 // staging registers).
 //
-// K is walked in steps of 64 through a ring of NST LDS stages.  Iteration kt
+// K is walked in steps of 64 through a ring of NST LDS stages.  With NST = 2
+// (double buffer, small enough for two blocks per CU) step kt+1 is loaded
+// while step kt's MFMAs run.  With NST >= 3, iteration kt
 // issues the loads of step kt+NST-1 into the stage that step kt-1 left, waits
 // for this wave's loads of step kt+1, passes one barrier (which publishes
 // step kt+1 from every wave), reads step kt+1's MFMA fragments into the
@@ -38,7 +40,7 @@ struct DmaTile {
     static_assert(WA * WB == 4, "4 waves");
     static_assert(TA >= 1 && TB >= 1 && WTA % 32 == 0 && WTB % 32 == 0, "wave tile must be a multiple of 32");
     static_assert(BA % 32 == 0 && BB % 32 == 0, "tile rows per DMA instruction");
-    static_assert(NST >= 3 && NST <= 4, "ring of 3 or 4 stages");
+    static_assert(NST >= 2 && NST <= 4, "ring of 2 to 4 stages");
     typedef typename std::conditional<F16, f16x8, bf16x8>::type frag;
 
     f32x16 acc[TA][TB];
@@ -131,6 +133,28 @@ struct DmaTile {
                 OC_WAIT_VMCNT(0);
             }
         };
+        if constexpr (NST == 2) {
+            // double buffer: the MFMAs of step kt overlap the DMA of step
+            // kt+1; the fragments of kt+1 are read after the barrier that
+            // publishes it (two blocks per CU hide that latency)
+            issue(0);
+            OC_WAIT_VMCNT(0);
+            barrier_lds();
+            Frags f;
+            read_frags(lds, f);
+            for (int kt = 0; kt < nk; ++kt) {
+                if (kt + 1 < nk) issue(kt + 1);   // its stage was last read before the previous barrier
+                mfmas(f);
+                if (kt + 1 < nk) {
+                    OC_WAIT_VMCNT(0);
+                    barrier_lds();
+                    read_frags(lds + ((kt + 1) & 1) * STAGE, f);
+                }
+            }
+            OC_WAIT_VMCNT(0);
+            __syncthreads();
+            return;
+        }
 #pragma unroll
         for (int s = 0; s < D; ++s)
             if (s < nk) issue(s);
