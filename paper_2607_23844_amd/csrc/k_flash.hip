@@ -109,25 +109,29 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
 
     // DMA: instruction j of this wave fills LDS chunks q = (wave*I + j)*64 + lane
     // of a buffer (row q / chunks-per-row, slot q % chunks-per-row); the lane
-    // fetches the chunk that the swizzle puts in that slot
+    // fetches the chunk that the swizzle puts in that slot.  Buffer loads
+    // with a fixed per-lane offset and the tile's offset in a scalar: K rows
+    // past the end read as zeros (their scores are masked), and no address
+    // arithmetic is left per tile.
     constexpr int IK = DMA ? KCH / NT : 1, IV = DMA ? VCH / NT : 1;
     static_assert(!DMA || (KCH % NT == 0 && VCH % NT == 0), "DMA tile split");
-    const uint16_t *kd[IK];
-    int kdrow[IK];
-    const uint16_t *vd[IV];
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    i32x4 krs = {0, 0, 0, 0}, vrs = {0, 0, 0, 0};
+    int kvo[IK], vvo[IV];
     if constexpr (DMA) {
+        krs = buffer_rsrc(kbase, (int)((long)(Lk - 1) * hd * 2 + DH * 2));
+        vrs = buffer_rsrc(vbase, DH * lpad * 2);
 #pragma unroll
         for (int j = 0; j < IK; ++j) {
             const int q = (wave * IK + j) * 64 + lane;
             const int r = q / (DK / 8), c = dma_slot<LDK>(r, q % (DK / 8));
-            kdrow[j] = r;
-            kd[j] = kbase + c * 8;
+            kvo[j] = (r * hd + c * 8) * 2;
         }
 #pragma unroll
         for (int j = 0; j < IV; ++j) {
             const int q = (wave * IV + j) * 64 + lane;
             const int d = q / (KT / 8), c = dma_slot<LDV>(d, q % (KT / 8));
-            vd[j] = vbase + (long)d * lpad + c * 8;
+            vvo[j] = (d * lpad + c * 8) * 2;
         }
     }
     auto issue = [&](int kt) {
@@ -135,14 +139,11 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
         uint16_t *kb = Ks + buf * C::KBUF;
         uint16_t *vb = Vs + buf * C::VBUF;
 #pragma unroll
-        for (int j = 0; j < IK; ++j) {
-            const int row = min(k0 + kdrow[j], Lk - 1);
-            __builtin_amdgcn_global_load_lds((glb_vp)(kd[j] + (long)row * hd), (lds_vp)(kb + (wave * IK + j) * 512),
-                                             16, 0, 0);
-        }
+        for (int j = 0; j < IK; ++j)
+            buffer_load_lds(krs, (lds_vp)(kb + (wv * IK + j) * 512), 16, kvo[j], k0 * hd * 2, 0, 0);
 #pragma unroll
         for (int j = 0; j < IV; ++j)
-            __builtin_amdgcn_global_load_lds((glb_vp)(vd[j] + k0), (lds_vp)(vb + (wave * IV + j) * 512), 16, 0, 0);
+            buffer_load_lds(vrs, (lds_vp)(vb + (wv * IV + j) * 512), 16, vvo[j], k0 * 2, 0, 0);
     };
 
     // this thread's staging chunks (fixed across tiles)
@@ -225,6 +226,8 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
 #pragma unroll
     for (int db = 0; db < NDB; ++db) o[db] = osv[db] = f32x16{};
     float m = 0.f, l0 = 0.f, l1 = 0.f;
+    // -m in every slot: the first S MFMA of a tile adds it (changes only on the slow path)
+    f32x16 negm = f32x16{};
 
     const int n_kt = cdiv(Lk, KT);
     constexpr int IPT = IK + IV;   // DMA instructions per wave and tile
@@ -262,14 +265,10 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
         if (DMA && kt + 3 < n_kt) issue(kt + 3);
         // S^T - m
         f32x16 sc[2];
-        {
-            f32x16 init;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) init[i] = -m;
-            sc[0] = sc[1] = init;
-        }
+        for (int kb2 = 0; kb2 < 2; ++kb2) sc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf[kb2][0], qf[0], negm, 0, 0, 0);
 #pragma unroll
-        for (int ks = 0; ks < NKS; ++ks)
+        for (int ks = 1; ks < NKS; ++ks)
 #pragma unroll
             for (int kb2 = 0; kb2 < 2; ++kb2)
                 sc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf[kb2][ks], qf[ks], sc[kb2], 0, 0, 0);
@@ -345,6 +344,8 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
 #pragma unroll
                 for (int i = 0; i < 16; ++i) sc[kb2][i] -= tt;
             m += tt;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) negm[i] = -m;
             exps();
         }
         // running sum of the fp16 P, fp32 accumulation
@@ -548,7 +549,7 @@ static hipError_t go_dh(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st
     if (Lk <= 32) return go_short<DH, 1>(p, a, Lk, st);
     if (Lk <= 64) return go_short<DH, 2>(p, a, Lk, st);
     if constexpr (DH % 64 == 0) {
-        if (flash_uses_dma(DH, Lk)) return go<DH, 4, true>(p, a, Lk, st);
+        if (flash_uses_dma(DH, Lk, p.hd)) return go<DH, 4, true>(p, a, Lk, st);
     }
     return go<DH, 4, false>(p, a, Lk, st);
 }

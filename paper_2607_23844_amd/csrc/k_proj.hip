@@ -227,7 +227,7 @@ hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, h
     {
         StageScope _stage(st, "proj_v");
         const int Lk = a.n_seq == 1 ? rm.n_rows : a.L;
-        const int zero_pad = flash_uses_dma(p.dh, Lk) ? 1 : 0;
+        const int zero_pad = flash_uses_dma(p.dh, Lk, p.hd) ? 1 : 0;
         const int n_at = cdiv(rm.n_rows, 128);
         if (p.C % 64 == 0) {
             static bool attr = false;

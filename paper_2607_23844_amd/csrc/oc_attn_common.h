@@ -45,7 +45,10 @@ __device__ __forceinline__ int vt_key_of_pos(int p) { return (p & ~12) | ((p & 4
 // Whether the attention kernel stages K/V by DMA for this head dim and key
 // count.  The DMA path relies on the V projection having zeroed the padded
 // key positions [Lk, lpad) of every Vt row.
-inline bool flash_uses_dma(int dh, int Lk) { return dh % 64 == 0 && dh <= 128 && Lk >= 256; }
+// (buffer offsets of K are 32-bit: Lk * hd * 2 bytes must stay below 2^31)
+inline bool flash_uses_dma(int dh, int Lk, int hd) {
+    return dh % 64 == 0 && dh <= 128 && Lk >= 256 && (long)Lk * hd * 2 < (1L << 31);
+}
 
 hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, hipStream_t st);
 hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStream_t st);

@@ -65,6 +65,23 @@ __device__ __forceinline__ void argmax_merge(float &v, int &i, float v2, int i2)
     if (v2 > v || (v2 == v && (unsigned)i2 < (unsigned)i)) { v = v2; i = i2; }
 }
 
+// Raw buffer resources (stride 0): offsets at or past num_records bytes read
+// as zero.  The LDS-destination buffer load is the LLVM intrinsic, bound by
+// name; the fourth word selects 32-bit data on gfx950.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+constexpr int BUF_RSRC_WORD3 = 0x00020000;
+__device__ __forceinline__ i32x4 buffer_rsrc(const void *base, int num_bytes) {
+    const unsigned long a = (unsigned long)base;
+    i32x4 r;
+    r.x = (int)(unsigned)(a & 0xFFFFFFFFul);
+    r.y = (int)(unsigned)((a >> 32) & 0xFFFFul);
+    r.z = num_bytes;
+    r.w = BUF_RSRC_WORD3;
+    return r;
+}
+__device__ void buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) void *lds, int size, int voffset,
+                                int soffset, int offset, int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
+
 // Order-preserving map of a float to uint32 (larger float -> larger key).
 __device__ __forceinline__ uint32_t float_key(float f) {
     uint32_t u = __float_as_uint(f);

@@ -44,6 +44,20 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, name), name
 
 
+def test_library_leaves_no_library_symbol_undefined():
+    """Every kernel and function of the library is defined in it: a kernel
+    whose host stub the compiler dropped would only fail at its first launch
+    (the library is loaded with lazy binding)."""
+    import shutil
+    import subprocess
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    out = subprocess.run([nm, "-C", "--undefined-only", L.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    missing = [l.strip() for l in out.splitlines() if "oc::" in l or " oc_" in l]
+    assert not missing, "undefined in the library: " + "; ".join(missing[:5])
+
+
 def test_python_binding_covers_every_declared_symbol():
     assert set(declared_functions()) <= set(L._SIGS)
 
