@@ -19,6 +19,14 @@ namespace oc {
 // bf16 -> fp16 (exact in the fp16 normal range, saturating outside), 8
 // elements per thread
 // ----------------------------------------------------------------------------
+// lanes per item for rows of `chunks` 16-byte chunks: the largest power of
+// two not above chunks, between 8 and 64
+__host__ __device__ inline int lanes_per_item(int chunks) {
+    int l = 8;
+    while (l < 64 && 2 * l <= chunks) l *= 2;
+    return l;
+}
+
 template <typename T>
 __global__ void k_inv_norm(const T *__restrict__ x, float *__restrict__ inv, int n_items, int n_sub,
                            long sub_stride, int C, int norm_blocks, unsigned long long *__restrict__ pack,
@@ -59,23 +67,25 @@ __global__ void k_inv_norm(const T *__restrict__ x, float *__restrict__ inv, int
         }
         return;
     }
-    const int item = blockIdx.x * (blockDim.x / WAVE) + (threadIdx.x / WAVE);
-    if (item >= n_items) return;
+    // LPI lanes per item (a power of two up to 64, about one 16-byte chunk
+    // per lane for short rows): 256 / LPI items per block
+    const int lpi = lanes_per_item(C / VEC);
+    const int sub = threadIdx.x & (lpi - 1);
+    const int item = blockIdx.x * (blockDim.x / lpi) + threadIdx.x / lpi;
+    if (item >= n_items) return;   // (whole lane groups: the reduction below stays inside one)
+    const T *row = x + (long)item * C;
     float ss = 0.f;
-    for (int s = 0; s < n_sub; ++s) {
-        const T *row = x + s * sub_stride + (long)item * C;
-        for (int c = lane * VEC; c < C; c += WAVE * VEC) {
-            const uint4 v = *reinterpret_cast<const uint4 *>(row + c);
-            const T *e = reinterpret_cast<const T *>(&v);
+    for (int c = sub * VEC; c < C; c += lpi * VEC) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(row + c);
+        const T *e = reinterpret_cast<const T *>(&v);
 #pragma unroll
-            for (int j = 0; j < VEC; ++j) {
-                const float f = Elem<T>::ld(e + j);
-                ss = fmaf(f, f, ss);
-            }
+        for (int j = 0; j < VEC; ++j) {
+            const float f = Elem<T>::ld(e + j);
+            ss = fmaf(f, f, ss);
         }
     }
-    ss = wave_sum(ss);
-    if (lane == 0) inv[item] = ss > 0.f ? (float)(1.0 / sqrt((double)ss)) : 0.f;
+    for (int o = lpi >> 1; o > 0; o >>= 1) ss += __shfl_xor(ss, o, WAVE);
+    if (sub == 0) inv[item] = ss > 0.f ? (float)(1.0 / sqrt((double)ss)) : 0.f;
 }
 
 hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, unsigned long long *node_pack, long n_pack,
@@ -84,7 +94,8 @@ hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, unsigned lo
     const int n_items = p.kind == KIND_BLOCK ? p.N : p.F * p.N;
     const int n_sub = p.kind == KIND_BLOCK ? p.F : 1;
     const long sub = (long)p.N * p.C;
-    const int blocks = n_sub > 1 ? n_items : cdiv(n_items, 4);
+    const int chunks = p.C / (p.bf16 ? 8 : 4);
+    const int blocks = n_sub > 1 ? n_items : cdiv(n_items, 256 / lanes_per_item(chunks));
     const long n8 = (wo && wo16 && p.bf16) ? n_wo / 8 : 0;
     const int cvt_blocks = n8 > 0 ? (int)std::min<long>((n8 + 255) / 256, 1024) : 0;
     if (p.bf16)
@@ -203,7 +214,7 @@ __global__ __launch_bounds__(256) void k_match_sweep(const uint16_t *__restrict_
                                                       unsigned long long *__restrict__ node_pack) {
     using T = DmaTile<BA, BB, WA, WB>;
     extern __shared__ __align__(16) uint16_t lds[];
-    __shared__ float snorm[SWEEP_MAX_D];
+    __shared__ __align__(16) float snorm[SWEEP_MAX_D];
     __shared__ float sv[WA * BB];
     __shared__ int si[WA * BB];
     const int lid = xcd_remap(blockIdx.x, n_bt * G);
@@ -237,26 +248,47 @@ __global__ __launch_bounds__(256) void k_match_sweep(const uint16_t *__restrict_
         const int id = a < D ? gm.dst_id(gr, a) : -1;
         return id >= 0 ? x + (long)id * item_stride : nullptr;
     };
+    // per tile: scale by the representative norms, take the tile maximum per
+    // candidate and lane half, and only when it beats the running best find
+    // its smallest position (tiles come in ascending position, so a later
+    // equal value never replaces an earlier one); the lane halves are merged
+    // once at the end
+    const int d_full = D - BA;   // tiles starting at or below this have only valid representatives
     auto epi = [&](int u) {
+        const bool full = u * BA <= d_full && gm.dst_id(gr, u * BA + BA - 1) >= 0;
 #pragma unroll
-        for (int j = 0; j < T::TB; ++j) {
-            float v = -INFINITY;
-            int ix = -1;
+        for (int j = 0; j < T::TB; ++j)
 #pragma unroll
-            for (int i = 0; i < T::TA; ++i)
+            for (int i = 0; i < T::TA; ++i) {
+                float t[16];
 #pragma unroll
-                for (int g4 = 0; g4 < 4; ++g4)
+                for (int g4 = 0; g4 < 4; ++g4) {
+                    const int al = u * BA + T::a_of(i, g4);
+                    const float4 w = *reinterpret_cast<const float4 *>(&snorm[al]);
+                    const float wv[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const int ga = u * BA + T::a_of(i, g4) + e;
-                        const float w = snorm[ga];
-                        if (w >= 0.f) argmax_merge(v, ix, tile.acc[i][j][4 * g4 + e] * w, ga);
+                        float v = tile.acc[i][j][4 * g4 + e] * wv[e];
+                        if (!full && wv[e] < 0.f) v = -INFINITY;
+                        t[4 * g4 + e] = v;
                     }
-            argmax_merge(v, ix, __shfl_xor(v, 32, WAVE), __shfl_xor(ix, 32, WAVE));
-            argmax_merge(bv[j], bi[j], v, ix);
-        }
+                }
+                float m = t[0];
+#pragma unroll
+                for (int k = 1; k < 16; ++k) m = fmaxf(m, t[k]);
+                if (m > bv[j]) {
+                    int ix = -1;
+#pragma unroll
+                    for (int k = 15; k >= 0; --k)
+                        if (t[k] == m) ix = u * BA + T::a_of(i, k >> 2) + (k & 3);
+                    bv[j] = m;
+                    bi[j] = ix;
+                }
+            }
     };
     tile.run_tiles_bres(lds, rows_a, rowsB, x, x, K, n_at, epi);
+#pragma unroll
+    for (int j = 0; j < T::TB; ++j) argmax_merge(bv[j], bi[j], __shfl_xor(bv[j], 32, WAVE), __shfl_xor(bi[j], 32, WAVE));
     if (lane < 32) {
 #pragma unroll
         for (int j = 0; j < T::TB; ++j) {

@@ -43,22 +43,24 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
     __shared__ uint32_t red[3][SEL_WAVES];
     __shared__ int sh[17];
     __shared__ int sel_info[3];
+    // candidate keys, staged through LDS (klds, S words): read from global
+    // memory in slabs (thread t: i = j*SEL_THREADS + t, coalesced), then held
+    // by thread t as the contiguous run i = t*ipt + j for the radix passes, so
+    // that one wave's histogram updates mix distant (less correlated)
+    // candidates; candidates i >= the group's count are not valid
+    extern __shared__ uint32_t klds[];
     const int g = blockIdx.x;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int ipt = cdiv(S, SEL_THREADS);
     const GroupMap::Grp gr = gm.group(g);
     const int R = gr.R;
+    const int n_src = min(gr.nsrc, S);
 
-    uint32_t key[SEL_IPT];
-    int32_t nid[SEL_IPT];
-    uint32_t vmask = 0;
-    int nvalid_local = 0;
-    uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+    int32_t nid[SEL_IPT];   // slab layout
 #pragma unroll
     for (int j = 0; j < SEL_IPT; ++j) {
-        key[j] = 0;
         nid[j] = -1;
-        const int i = t * ipt + j;
+        const int i = j * SEL_THREADS + t;
         if (j >= ipt || i >= S) continue;
         const long gi = (long)g * S + i;
         const int sid = gm.src_id(gr, i);
@@ -83,7 +85,19 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
             v = node_max_in[gi];
             nid[j] = node_idx_in[gi];
         }
-        key[j] = float_key(v);
+        klds[i] = float_key(v);
+    }
+    __syncthreads();
+    uint32_t key[SEL_IPT];   // run layout
+    uint32_t vmask = 0;
+    int nvalid_local = 0;
+    uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+#pragma unroll
+    for (int j = 0; j < SEL_IPT; ++j) {
+        key[j] = 0;
+        const int i = t * ipt + j;
+        if (j >= ipt || i >= n_src) continue;
+        key[j] = klds[i];
         vmask |= 1u << j;
         ++nvalid_local;
         lo = min(lo, key[j]);
@@ -196,20 +210,30 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
         int eq_total;
         eq_rank = block_exclusive_scan(eq_local, sh, eq_total);
     }
+    // decisions in the run layout, published as bytes in klds (every thread
+    // read its keys from klds before the barriers above)
+    uint8_t *cbyte = reinterpret_cast<uint8_t *>(klds);
+    if (!none && !all) {
+#pragma unroll
+        for (int j = 0; j < SEL_IPT; ++j) {
+            if (!((vmask >> j) & 1u)) continue;
+            bool c;
+            if (key[j] > tau) c = true;
+            else if (key[j] == tau) { c = !tie || eq_rank < need; ++eq_rank; }
+            else c = false;
+            cbyte[t * ipt + j] = c ? 1 : 0;
+        }
+    }
+    __syncthreads();
     // frame compaction (kept_idx given): flags of the frame's N tokens in LDS
     __shared__ uint8_t fl[SEL_COMPACT_MAX_N];
     const bool compact = kept_idx != nullptr;
     const long fbase = (long)g * N;
 #pragma unroll
     for (int j = 0; j < SEL_IPT; ++j) {
-        if (!((vmask >> j) & 1u)) continue;
-        const int i = t * ipt + j;
-        bool c;
-        if (none) c = false;
-        else if (all) c = true;
-        else if (key[j] > tau) c = true;
-        else if (key[j] == tau) { c = !tie || eq_rank < need; ++eq_rank; }
-        else c = false;
+        const int i = j * SEL_THREADS + t;
+        if (j >= ipt || i >= n_src) continue;
+        const bool c = all || (!none && cbyte[i] != 0);
         const int id = gm.src_id(gr, i);
         flag[id] = c ? 1 : 0;
         mtok[id] = c ? nid[j] : -1;
@@ -225,31 +249,41 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
     }
     if (!compact) return;
     __syncthreads();
-    // one scan over the frame's tokens in id order gives both ranks: kept
-    // count in the low 16 bits, cached count in the high 16 (N < 32768)
-    const int cpt = cdiv(N, SEL_THREADS), p0 = t * cpt;
-    int packed = 0;
-    for (int j = 0; j < cpt; ++j) {
-        const int n = p0 + j;
-        if (n < N) packed += fl[n] ? (1 << 16) : 1;
+    // ranks over the frame's tokens in id order: position n = j*SEL_THREADS
+    // + t (slab j, wave, lane); a slab's cached tokens counted per wave by a
+    // ballot, one scan over the (slab, wave) counts, then a lane's cached
+    // rank is its wave's prefix plus the cached lanes below it; the kept rank
+    // is the position minus the cached rank
+    __shared__ int wcnt[SEL_COMPACT_MAX_N / 64];
+    const int nslab = cdiv(N, SEL_THREADS);
+    for (int j = 0; j < nslab; ++j) {
+        const int n = j * SEL_THREADS + t;
+        const unsigned long long b = __builtin_amdgcn_ballot_w64(n < N && fl[n] != 0);
+        if (lane == 0) wcnt[j * SEL_WAVES + wave] = __builtin_popcountll(b);
     }
+    __syncthreads();
+    const int n_cnt = nslab * SEL_WAVES;   // <= SEL_COMPACT_MAX_N / 64 = 384 <= SEL_THREADS
     int tot;
-    const int pre = block_exclusive_scan(packed, sh, tot);
-    int krank = pre & 0xFFFF, crank = pre >> 16;
+    const int pre = block_exclusive_scan(t < n_cnt ? wcnt[t] : 0, sh, tot);
+    if (t < n_cnt) wcnt[t] = pre;
+    __syncthreads();
     const int n_c = gr.R;   // every frame caches exactly its budget
-    for (int j = 0; j < cpt; ++j) {
-        const int n = p0 + j;
-        if (n >= N) break;
+    const unsigned long long below = (1ull << lane) - 1ull;
+    for (int j = 0; j < nslab; ++j) {
+        const int n = j * SEL_THREADS + t;
+        const bool c = n < N && fl[n] != 0;
+        const unsigned long long b = __builtin_amdgcn_ballot_w64(c);
+        if (n >= N) continue;
+        const int crank = wcnt[j * SEL_WAVES + wave] + __builtin_popcountll(b & below);
+        const int krank = n - crank;
         const int pid = (int)(fbase + n);
-        if (fl[n]) {
+        if (c) {
             if (crank < n_c) cached_idx[(long)g * n_c + crank] = pid;
             rmap[pid] = -1;
-            ++crank;
         } else {
             const int row = g * L + krank;
             if (krank < L) kept_idx[row] = pid;
             rmap[pid] = krank < L ? row : -2;
-            ++krank;
         }
     }
 }
@@ -258,7 +292,7 @@ hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_
                          int32_t *flag, int32_t *mtok, hipStream_t st) {
     {
         StageScope _stage(st, "select");
-        launch_k(k_select<false>, p.n_groups, SEL_THREADS, 0, st, node_max, node_idx, nullptr, nullptr, nullptr, nullptr,
+        launch_k(k_select<false>, p.n_groups, SEL_THREADS, (size_t)p.n_src_max * 4, st, node_max, node_idx, nullptr, nullptr, nullptr, nullptr,
                                                             group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max,
                                                             flag, mtok, nullptr, nullptr, nullptr, p.N, p.seq_len);
     }
@@ -272,7 +306,7 @@ hipError_t launch_select_packed(const Plan &p, const int32_t *units, const unsig
     if (compact && !select_compacts(p)) return hipErrorInvalidValue;
     {
         StageScope _stage(st, "select");
-        launch_k(k_select<true>, p.n_groups, SEL_THREADS, 0, st, nullptr, nullptr, node_pack, inv, node_max, node_idx,
+        launch_k(k_select<true>, p.n_groups, SEL_THREADS, (size_t)p.n_src_max * 4, st, nullptr, nullptr, node_pack, inv, node_max, node_idx,
                                                            group_map(p, units), p.n_groups, p.n_src_max,
                                                            p.n_dst_max, flag, mtok, kept_idx, cached_idx, rmap, p.N,
                                                            p.seq_len);

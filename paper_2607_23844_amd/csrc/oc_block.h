@@ -15,10 +15,17 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int *sh /* >= 17 ints
     }
     if (lane == 63) sh[wave] = x;
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int run = 0;
-        for (int w = 0; w < nw; ++w) { const int c = sh[w]; sh[w] = run; run += c; }
-        sh[16] = run;
+    if (wave == 0) {
+        // exclusive scan of the (at most 16) wave totals across lanes
+        const int c = lane < nw ? sh[lane] : 0;
+        int s = c;
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) {
+            const int y = __shfl_up(s, o, 64);
+            if (lane >= o) s += y;
+        }
+        if (lane < nw) sh[lane] = s - c;
+        if (lane == nw - 1) sh[16] = s;
     }
     __syncthreads();
     const int excl = sh[wave] + x - v;
