@@ -200,21 +200,21 @@ __global__ __launch_bounds__(256) void k_match_mfma(const uint16_t *__restrict__
     }
 }
 
-// Sweep variant for short descriptors, many candidate tiles and several
-// representative tiles: block (candidate tile bt, group g) keeps its
-// candidates' descriptors in LDS, streams every representative tile through
-// one continuous LDS-DMA pipeline, keeps each candidate's best (value,
-// position) in registers and publishes it once (one 64-bit atomic maximum per
-// candidate; no other block touches it).  The group's representative norms
-// are staged in LDS first (D <= SWEEP_MAX_D).
+// Sweep variant for many candidate tiles and several representative tiles:
+// block (candidate tile bt, group g) streams every representative tile (and
+// its candidates again, from L2) through one continuous double-buffered
+// LDS-DMA pipeline (small enough for two blocks per CU), keeps each
+// candidate's best (value, position) in registers and publishes it once (one
+// 64-bit atomic maximum per candidate; no other block touches it).  The
+// group's representative norms are staged in LDS first (D <= SWEEP_MAX_D).
 template <int BA, int BB, int WA, int WB>
 __global__ __launch_bounds__(256) void k_match_sweep(const uint16_t *__restrict__ x, const float *__restrict__ inv,
                                                       GroupMap gm, int G, int S, int D, int K, int seg_len,
                                                       long sub_stride, long item_stride, int n_bt, int n_at,
                                                       unsigned long long *__restrict__ node_pack) {
-    using T = DmaTile<BA, BB, WA, WB>;
+    using T = DmaTile<BA, BB, WA, WB, false, 2>;
     extern __shared__ __align__(16) uint16_t lds[];
-    __shared__ __align__(16) float snorm[SWEEP_MAX_D];
+    float *const snorm = reinterpret_cast<float *>(lds + T::LDS_BYTES / 2);   // n_at * BA norms after the ring
     __shared__ float sv[WA * BB];
     __shared__ int si[WA * BB];
     const int lid = xcd_remap(blockIdx.x, n_bt * G);
@@ -286,7 +286,7 @@ __global__ __launch_bounds__(256) void k_match_sweep(const uint16_t *__restrict_
                 }
             }
     };
-    tile.run_tiles_bres(lds, rows_a, rowsB, x, x, K, n_at, epi);
+    tile.run_tiles(lds, rows_a, rowsB, x, x, K, seg_len, sub_stride, n_at, epi);
 #pragma unroll
     for (int j = 0; j < T::TB; ++j) argmax_merge(bv[j], bi[j], __shfl_xor(bv[j], 32, WAVE), __shfl_xor(bi[j], 32, WAVE));
     if (lane < 32) {
@@ -472,11 +472,11 @@ template <int BA, int BB, int WA, int WB>
 static hipError_t go_sweep(const Plan &p, const uint16_t *x, const float *inv, const GroupMap &gm, int K,
                            int seg_len, long sub_stride, long item_stride, unsigned long long *node_pack,
                            hipStream_t st) {
-    using T = DmaTile<BA, BB, WA, WB>;
+    using T = DmaTile<BA, BB, WA, WB, false, 2>;
     const int G = p.n_groups, S = p.n_src_max, D = p.n_dst_max;
     const int n_bt = cdiv(S, BB), n_at = cdiv(D, BA);
-    if (n_at * BA > SWEEP_MAX_D || K > SWEEP_MAX_K || seg_len != 0) return hipErrorInvalidValue;
-    const size_t lds = T::bres_lds_bytes(K);
+    if (n_at * BA > SWEEP_MAX_D) return hipErrorInvalidValue;
+    const size_t lds = T::LDS_BYTES + (size_t)n_at * BA * 4;
     static bool attr = false;
     hipError_t e = allow_lds(k_match_sweep<BA, BB, WA, WB>, lds, attr);
     if (e != hipSuccess) return e;

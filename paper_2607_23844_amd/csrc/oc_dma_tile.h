@@ -260,6 +260,27 @@ struct DmaTile {
                 clear();
             }
         };
+        if constexpr (NST == 2) {
+            // double buffer: the MFMAs of step s overlap the DMA of step s+1
+            issue(0);
+            OC_WAIT_VMCNT(0);
+            barrier_lds();
+            Frags f;
+            read_frags(lds, f);
+            for (int s = 0; s < ns; ++s) {
+                if (s + 1 < ns) issue(s + 1);   // its stage was last read before the previous barrier
+                mfmas(f);
+                finish(s);
+                if (s + 1 < ns) {
+                    OC_WAIT_VMCNT(0);
+                    barrier_lds();
+                    read_frags(lds + ((s + 1) & 1) * STAGE, f);
+                }
+            }
+            OC_WAIT_VMCNT(0);
+            __syncthreads();
+            return;
+        }
 #pragma unroll
         for (int s = 0; s < D; ++s)
             if (s < ns) issue(s);
@@ -282,122 +303,6 @@ struct DmaTile {
                 wait_for(s + 2, s + 1 + D < ns ? s + 1 + D : ns - 1);
                 barrier_lds();
                 read_frags(lds + ((s + 2) % NST) * STAGE, f0);
-            }
-            mfmas(f1);
-            finish(s + 1);
-        }
-        OC_WAIT_VMCNT(0);
-        __syncthreads();
-    }
-
-    // As run_tiles, for short K (nk <= 6 steps): the B operand is loaded into
-    // LDS once, all its K steps side by side after the A ring, and only A
-    // streams through the ring (no re-reads of B from L2 per tile).
-    static constexpr size_t bres_lds_bytes(int K) {
-        return (size_t)NST * BA * BK * 2 + (size_t)(K / BK) * BB * BK * 2;
-    }
-    template <typename RowsA, typename Epi>
-    __device__ __forceinline__ void run_tiles_bres(uint16_t *lds, RowsA rows_a, const uint16_t *const *rowsB,
-                                                   const uint16_t *fallbackA, const uint16_t *fallbackB, int K,
-                                                   int n_tiles, Epi epi) {
-        const int t = threadIdx.x, wave = t >> 6, lane = t & 63, lr = lane & 31, lh = lane >> 5;
-        constexpr int ASTAGE = BA * BK;
-        uint16_t *const Bres = lds + NST * ASTAGE;
-        auto clear = [&]() {
-#pragma unroll
-            for (int i = 0; i < TA; ++i)
-#pragma unroll
-                for (int j = 0; j < TB; ++j) acc[i][j] = f32x16{};
-        };
-        clear();
-        const int nk = K / BK, ns = nk * n_tiles;
-        int ca[CA];
-#pragma unroll
-        for (int i = 0; i < CA; ++i) {
-            const int r = chunk_row(i);
-            ca[i] = ((t & 7) ^ ((r >> 1) & 7)) << 3;
-        }
-        // B: every K step once, into its own slot after the ring
-        for (int kt = 0; kt < nk; ++kt) {
-#pragma unroll
-            for (int i = 0; i < CB; ++i) {
-                const int r = chunk_row(i);
-                const uint16_t *pb = (rowsB[i] ? rowsB[i] : fallbackB) + (((t & 7) ^ ((r >> 1) & 7)) << 3);
-                __builtin_amdgcn_global_load_lds((glb_vp)(pb + kt * BK), (lds_vp)(Bres + kt * BB * BK + (wave + 4 * i) * 512),
-                                                 16, 0, 0);
-            }
-        }
-        int cur_u = -1;
-        const uint16_t *pa[CA];
-        auto issue = [&](int s) {
-            const int u = s / nk, kt = s - u * nk;
-            if (u != cur_u) {
-                cur_u = u;
-#pragma unroll
-                for (int i = 0; i < CA; ++i) {
-                    const uint16_t *r = rows_a(u, i);
-                    pa[i] = (r ? r : fallbackA) + ca[i];
-                }
-            }
-            uint16_t *st = lds + (s % NST) * ASTAGE;
-#pragma unroll
-            for (int i = 0; i < CA; ++i)
-                __builtin_amdgcn_global_load_lds((glb_vp)(pa[i] + kt * BK), (lds_vp)(st + (wave + 4 * i) * 512), 16, 0,
-                                                 0);
-        };
-        auto read = [&](int s, Frags &f) {
-            const int kt = s % nk;
-            const uint16_t *As = lds + (s % NST) * ASTAGE, *Bs = Bres + kt * BB * BK;
-            const int wa = wave / WB, wb = wave % WB;
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                const int c = ks * 2 + lh;
-#pragma unroll
-                for (int i = 0; i < TA; ++i) f.a[ks][i] = *reinterpret_cast<const frag *>(As + slot(wa * WTA + i * 32 + lr, c));
-#pragma unroll
-                for (int j = 0; j < TB; ++j) f.b[ks][j] = *reinterpret_cast<const frag *>(Bs + slot(wb * WTB + j * 32 + lr, c));
-            }
-        };
-        auto wait_for = [&](int s, int last_issued) {
-            const int later = last_issued - s;
-            if (NST == 4 && later >= 2) {
-                OC_WAIT_VMCNT(2 * CA);
-            } else if (later >= 1) {
-                OC_WAIT_VMCNT(CA);
-            } else {
-                OC_WAIT_VMCNT(0);
-            }
-        };
-        constexpr int D = NST - 1;
-        auto finish = [&](int s) {
-            if (s % nk == nk - 1) {
-                epi(s / nk);
-                clear();
-            }
-        };
-#pragma unroll
-        for (int s = 0; s < D; ++s)
-            if (s < ns) issue(s);
-        // B and A step 0 landed (B was issued first)
-        wait_for(0, (ns < D ? ns : D) - 1);
-        barrier_lds();
-        Frags f0, f1;
-        read(0, f0);
-        for (int s = 0; s < ns; s += 2) {
-            if (s + D < ns) issue(s + D);
-            if (s + 1 < ns) {
-                wait_for(s + 1, s + D < ns ? s + D : ns - 1);
-                barrier_lds();
-                read(s + 1, f1);
-            }
-            mfmas(f0);
-            finish(s);
-            if (s + 1 >= ns) break;
-            if (s + 1 + D < ns) issue(s + 1 + D);
-            if (s + 2 < ns) {
-                wait_for(s + 2, s + 1 + D < ns ? s + 1 + D : ns - 1);
-                barrier_lds();
-                read(s + 2, f0);
             }
             mfmas(f1);
             finish(s + 1);

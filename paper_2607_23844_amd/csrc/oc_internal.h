@@ -91,12 +91,11 @@ inline MatchSplit match_split(const Plan &p) {
     m.kc = sps * 64;
     return m;
 }
-constexpr int SWEEP_MAX_D = 4096;   // representatives per group for the sweep variant
-constexpr int SWEEP_MAX_K = 320;    // descriptor length it keeps in LDS (with the ring and norms: <= 160 KiB)
+constexpr int SWEEP_MAX_D = 4096;   // representatives per group for the sweep variant (norms in LDS)
 inline bool match_sweeps(const Plan &p) {
     const int n_bt = (p.n_src_max + 127) / 128, n_at = (p.n_dst_max + 127) / 128;
-    return p.bf16 && p.kind == KIND_TOKEN && p.C % 64 == 0 && p.C <= SWEEP_MAX_K && n_at >= 2 &&
-           n_at * 128 <= SWEEP_MAX_D && (long)n_bt * p.n_groups >= 512;
+    return p.bf16 && p.kind == KIND_TOKEN && p.C % 64 == 0 && n_at >= 2 && n_at * 128 <= SWEEP_MAX_D &&
+           (long)n_bt * p.n_groups >= 512;
 }
 // node_max == nullptr: node_pack only (the selection unpacks it); part: the
 // split-K partials (match_split), unused otherwise
