@@ -15,31 +15,37 @@ namespace oc {
 
 constexpr int CMP_THREADS = 1024;
 
-// cached tokens per frame (token-kind flags)
-__global__ void k_frame_counts(const int32_t *__restrict__ flag, int N, int32_t *__restrict__ fcnt) {
-    __shared__ int sh[17];
-    const int f = blockIdx.x;
-    int c = 0;
-    for (int n = threadIdx.x; n < N; n += blockDim.x) c += flag[(long)f * N + n] ? 1 : 0;
-    int total;
-    (void)block_exclusive_scan(c, sh, total);
-    if (threadIdx.x == 0) fcnt[f] = total;
+// Token kinds, chunked: a frame's tokens in chunks of CMP_THREADS (one per
+// thread).  k_chunk_counts counts each chunk's cached tokens; block (unit u,
+// chunk q) of k_compact_chunks then takes its bases from those counts (kept
+// rows before it in its unit, cached tokens before it in id order) and its
+// in-chunk ranks from per-wave ballots.  A unit's chunks are those of frame
+// fa, then those of frame fb (pairs).
+__global__ __launch_bounds__(CMP_THREADS) void k_chunk_counts(const int32_t *__restrict__ flag, int N, int nch,
+                                                              int32_t *__restrict__ ccnt) {
+    __shared__ int wsum[CMP_THREADS / 64];
+    const int f = blockIdx.x / nch, c = blockIdx.x - f * nch;
+    const int i = c * CMP_THREADS + threadIdx.x;
+    const bool cached = i < N && flag[(long)f * N + i] != 0;
+    const unsigned long long b = __builtin_amdgcn_ballot_w64(cached);
+    if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = __builtin_popcountll(b);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int tot = 0;
+        for (int w = 0; w < CMP_THREADS / 64; ++w) tot += wsum[w];
+        ccnt[blockIdx.x] = tot;
+    }
 }
 
-// One block per attention unit (a frame, or a frame pair s, d): retained
-// tokens of the unit's frames in ascending id become rows [u*L, u*L+L).
-// fcnt == nullptr: every frame caches static_cnt tokens (token groups of
-// plain frames, a fixed budget per group).
-__global__ __launch_bounds__(CMP_THREADS) void k_compact_units(const int32_t *__restrict__ units, int F,
-                                                               const int32_t *__restrict__ flag,
-                                                               const int32_t *__restrict__ fcnt, int static_cnt,
-                                                               int N, int L, int n_cached,
-                                                               int32_t *__restrict__ kept_idx,
-                                                               int32_t *__restrict__ cached_idx,
-                                                               int32_t *__restrict__ rmap) {
+__global__ __launch_bounds__(CMP_THREADS) void k_compact_chunks(const int32_t *__restrict__ units, int F, int N,
+                                                                int nch, const int32_t *__restrict__ flag,
+                                                                const int32_t *__restrict__ ccnt, int L,
+                                                                int n_cached, int32_t *__restrict__ kept_idx,
+                                                                int32_t *__restrict__ cached_idx,
+                                                                int32_t *__restrict__ rmap) {
     __shared__ int sh[17];
-    __shared__ int base[3];
-    const int u = blockIdx.x;
+    __shared__ int wpre[CMP_THREADS / 64];
+    const int u = blockIdx.x / (2 * nch), q = blockIdx.x - u * 2 * nch;
     int fa = u, fb = -1;
     if (units != nullptr) {
         const int s = units[2 * u], d = units[2 * u + 1];
@@ -47,50 +53,48 @@ __global__ __launch_bounds__(CMP_THREADS) void k_compact_units(const int32_t *__
         fb = d >= 0 ? max(s, d) : -1;
     }
     if (fa < 0 || fa >= F || fb >= F) return;   // malformed unit table
-    if (threadIdx.x == 0) {
-        if (fcnt == nullptr) {
-            base[0] = fa * static_cnt;
-            base[1] = fb >= 0 ? fb * static_cnt : 0;
-            base[2] = static_cnt;
-        } else {
-            int ca = 0, cb = 0;
-            for (int f = 0; f < fa; ++f) ca += fcnt[f];
-            if (fb >= 0) for (int f = 0; f < fb; ++f) cb += fcnt[f];
-            base[0] = ca;          // cached tokens before frame fa
-            base[1] = cb;          // cached tokens before frame fb
-            base[2] = fcnt[fa];    // cached tokens in frame fa
-        }
-    }
-    __syncthreads();
-    const int n_u = fb >= 0 ? 2 * N : N;
-    const int ipt = cdiv(n_u, CMP_THREADS);
-    const int i0 = threadIdx.x * ipt;
-    int kept_local = 0, cached_local = 0;
-    for (int j = 0; j < ipt; ++j) {
-        const int i = i0 + j;
-        if (i >= n_u) break;
-        const int p = i < N ? fa * N + i : fb * N + (i - N);
-        if (flag[p]) ++cached_local; else ++kept_local;
+    if (q >= (fb >= 0 ? 2 : 1) * nch) return;
+    const int f = q < nch ? fa : fb, c = q < nch ? q : q - nch;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    // bases: kept rows of the unit's earlier chunks, cached tokens of earlier
+    // chunks in id order (earlier frames, then earlier chunks of this frame)
+    int kb = 0, cb = 0;
+    for (int e = t; e < F * nch; e += CMP_THREADS) {
+        const int fe = e / nch, ce = e - fe * nch;
+        const int n = ccnt[e];
+        const int len = min(CMP_THREADS, N - ce * CMP_THREADS);
+        if (fe < f || (fe == f && ce < c)) cb += n;
+        const bool in_unit_before = (fe == fa && (f == fb || ce < c)) || (fe == fb && f == fb && ce < c);
+        if (in_unit_before) kb += len - n;
     }
     int tot;
-    int krank = block_exclusive_scan(kept_local, sh, tot);
-    int crank = block_exclusive_scan(cached_local, sh, tot);
-    for (int j = 0; j < ipt; ++j) {
-        const int i = i0 + j;
-        if (i >= n_u) break;
-        const bool second = i >= N;
-        const int p = second ? fb * N + (i - N) : fa * N + i;
-        if (flag[p]) {
-            const int pos = second ? base[1] + (crank - base[2]) : base[0] + crank;
-            if (pos >= 0 && pos < n_cached) cached_idx[pos] = p;
-            rmap[p] = -1;
-            ++crank;
-        } else {
-            const int row = u * L + krank;
-            if (krank < L) kept_idx[row] = p;
-            rmap[p] = krank < L ? row : -2;
-            ++krank;
-        }
+    (void)block_exclusive_scan(kb, sh, tot);
+    kb = tot;
+    (void)block_exclusive_scan(cb, sh, tot);
+    cb = tot;
+    const int i = c * CMP_THREADS + t;
+    const long p = (long)f * N + i;
+    const bool cached = i < N && flag[p] != 0;
+    const unsigned long long b = __builtin_amdgcn_ballot_w64(cached);
+    if (lane == 0) wpre[wave] = __builtin_popcountll(b);
+    __syncthreads();
+    if (t == 0) {
+        int run = 0;
+        for (int w = 0; w < CMP_THREADS / 64; ++w) { const int x = wpre[w]; wpre[w] = run; run += x; }
+    }
+    __syncthreads();
+    if (i >= N) return;
+    const int crank = wpre[wave] + __builtin_popcountll(b & ((1ull << lane) - 1ull));
+    const int krank = t - crank;
+    if (cached) {
+        const int pos = cb + crank;
+        if (pos < n_cached) cached_idx[pos] = (int)p;
+        rmap[p] = -1;
+    } else {
+        const int k = kb + krank;
+        const int row = u * L + k;
+        if (k < L) kept_idx[row] = (int)p;
+        rmap[p] = k < L ? row : -2;
     }
 }
 
@@ -187,18 +191,14 @@ hipError_t launch_compact(const Plan &p, const int32_t *units, const int32_t *fl
     const long total = (long)p.F * p.N;
     const unsigned grid = (unsigned)std::min<long>((total + 255) / 256, 4096);
     if (p.kind == KIND_TOKEN) {
-        // frame pairs split their budget between two frames in a data-dependent
-        // way: count per frame; plain frames cache k*k*R_tok tokens each
+        // chunk counts, then every (unit, chunk) block from them
+        const int nch = cdiv(p.N, CMP_THREADS);
         const bool pairs = p.gran == 3;
-        if (pairs) {
-            StageScope _stage(st, "frame_counts");
-            launch_k(k_frame_counts, p.F, 1024, 0, st, flag, p.N, fcnt);
-        }
         {
             StageScope _stage(st, "compact");
-            launch_k(k_compact_units, p.n_units, CMP_THREADS, 0, st, pairs ? units : nullptr, p.F, flag,
-                                                                pairs ? fcnt : nullptr, p.k * p.k * p.R_tok, p.N,
-                                                                p.seq_len, p.n_cached, kept_idx, cached_idx, rmap);
+            launch_k(k_chunk_counts, (unsigned)(p.F * nch), CMP_THREADS, 0, st, flag, p.N, nch, fcnt);
+            launch_k(k_compact_chunks, (unsigned)(p.n_units * 2 * nch), CMP_THREADS, 0, st, pairs ? units : nullptr,
+                     p.F, p.N, nch, flag, (const int32_t *)fcnt, p.seq_len, p.n_cached, kept_idx, cached_idx, rmap);
         }
     } else if (p.kind == KIND_BLOCK) {
         {

@@ -182,7 +182,7 @@ Layout make_layout(const Plan &p) {
     L.units = take(64 * 4);
     L.flag = take(FN * 4);
     L.mtok = take(FN * 4);
-    L.fcnt = take((size_t)p.F * 4);
+    L.fcnt = take((size_t)p.F * ((p.N + 1023) / 1024) * 4);   // cached tokens per 1024-token chunk
     L.kept = take(FN * 4);
     L.cached = take(FN * 4);
     L.rmap = take(FN * 4);
