@@ -13,8 +13,9 @@ namespace oc {
 struct RowMapF {
     const float *x; const int32_t *row_idx; int n_main;
     const float *ctx; int n_rows; int C;
+    int tF, tN;
     __device__ __forceinline__ const float *row(int r) const {
-        if (r < n_main) return x + (long)(row_idx ? row_idx[r] : r) * C;
+        if (r < n_main) return x + batch_token(r, row_idx, tF, tN) * C;
         return ctx + (long)(r - n_main) * C;
     }
 };
@@ -66,7 +67,7 @@ __global__ void k_attn_f32(const float *__restrict__ Q, const float *__restrict_
 }
 
 __global__ void k_out_f32(const float *__restrict__ O, int n_rows, int hd, const float *__restrict__ wo, int C,
-                          int n_main, const int32_t *__restrict__ out_idx, float *__restrict__ y,
+                          int n_main, const int32_t *__restrict__ out_idx, int tF, int tN, float *__restrict__ y,
                           float *__restrict__ y_ctx) {
     const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (long)n_rows * C) return;
@@ -75,7 +76,7 @@ __global__ void k_out_f32(const float *__restrict__ O, int n_rows, int hd, const
     const float *w = wo + (long)c * hd;
     float acc = 0.f;
     for (int k = 0; k < hd; ++k) acc = fmaf(o[k], w[k], acc);
-    if (r < n_main) y[(long)(out_idx ? out_idx[r] : r) * C + c] = acc;
+    if (r < n_main) y[batch_token(r, out_idx, tF, tN) * C + c] = acc;
     else y_ctx[(long)(r - n_main) * C + c] = acc;
 }
 
@@ -110,13 +111,13 @@ hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st) {
     const int Lk = a.L + (a.n_seq == 1 ? a.n_ctx : 0);
     if (n_rows == 0) return hipSuccess;
     if (p.bf16) {
-        const RowMap rm{(const uint16_t *)a.x, a.row_idx, a.n_main, (const uint16_t *)a.ctx, n_rows, p.C};
+        const RowMap rm{(const uint16_t *)a.x, a.row_idx, a.n_main, (const uint16_t *)a.ctx, n_rows, p.C, a.tF, a.tN};
         hipError_t e = launch_proj_qkv(p, rm, a, st);
         if (e != hipSuccess) return e;
         if ((e = launch_flash(p, a, Lk, st)) != hipSuccess) return e;
         return launch_proj_out(p, n_rows, a, st);
     }
-    const RowMapF rm{(const float *)a.x, a.row_idx, a.n_main, (const float *)a.ctx, n_rows, p.C};
+    const RowMapF rm{(const float *)a.x, a.row_idx, a.n_main, (const float *)a.ctx, n_rows, p.C, a.tF, a.tN};
     const long nq = (long)n_rows * 3 * p.hd;
     {
         StageScope _stage(st, "proj_f32");
@@ -136,8 +137,8 @@ hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st) {
     {
         StageScope _stage(st, "out_f32");
         launch_k(k_out_f32, (unsigned)((no + 255) / 256), 256, 0, st, (const float *)a.o, n_rows, p.hd,
-                                                                 (const float *)a.wo, p.C, a.n_main, a.out_idx,
-                                                                 (float *)a.y, (float *)a.y_ctx);
+                                                                 (const float *)a.wo, p.C, a.n_main, a.out_idx, a.tF,
+                                                                 a.tN, (float *)a.y, (float *)a.y_ctx);
     }
     return hipGetLastError();
 }

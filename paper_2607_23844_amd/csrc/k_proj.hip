@@ -256,7 +256,8 @@ using OTile =
 template <bool DMA>
 __global__ __launch_bounds__(256) void k_proj_out(const uint16_t *__restrict__ O, int n_rows, int hd,
                                                   const uint16_t *__restrict__ wo, int C, int n_main,
-                                                  const int32_t *__restrict__ out_idx, int n_at, int n_bt,
+                                                  const int32_t *__restrict__ out_idx, int tF, int tN, int n_at,
+                                                  int n_bt,
                                                   uint16_t *__restrict__ y, uint16_t *__restrict__ y_ctx) {
     using T = OTile<DMA>;
     constexpr int BA = 128, BB = DMA ? 64 : 128;
@@ -282,7 +283,7 @@ __global__ __launch_bounds__(256) void k_proj_out(const uint16_t *__restrict__ O
     write_rows<BA, BB>(lds, min(BA, C - a0), [&](int b, int c0) -> uint16_t * {
         const int r = b0 + b;
         if (r >= n_rows) return nullptr;
-        uint16_t *yrow = r < n_main ? y + (long)(out_idx ? out_idx[r] : r) * C : y_ctx + (long)(r - n_main) * C;
+        uint16_t *yrow = r < n_main ? y + batch_token(r, out_idx, tF, tN) * C : y_ctx + (long)(r - n_main) * C;
         return yrow + a0 + c0;
     });
 }
@@ -309,12 +310,12 @@ hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStre
         if (e != hipSuccess) return e;
         const int n_bt = cdiv(n_rows, 64);
         launch_k(k_proj_out<true>, n_at * n_bt, 256, OTile<true>::LDS_BYTES, st, 
-            (const uint16_t *)a.o, n_rows, p.hd, (const uint16_t *)a.wo16, p.C, a.n_main, a.out_idx, n_at, n_bt,
+            (const uint16_t *)a.o, n_rows, p.hd, (const uint16_t *)a.wo16, p.C, a.n_main, a.out_idx, a.tF, a.tN, n_at, n_bt,
             (uint16_t *)a.y, (uint16_t *)a.y_ctx);
     } else {
         const int n_bt = cdiv(n_rows, 128);
         launch_k(k_proj_out<false>, n_at * n_bt, 256, OTile<false>::LDS_BYTES, st, 
-            (const uint16_t *)a.o, n_rows, p.hd, (const uint16_t *)a.wo16, p.C, a.n_main, a.out_idx, n_at, n_bt,
+            (const uint16_t *)a.o, n_rows, p.hd, (const uint16_t *)a.wo16, p.C, a.n_main, a.out_idx, a.tF, a.tN, n_at, n_bt,
             (uint16_t *)a.y, (uint16_t *)a.y_ctx);
     }
     return hipGetLastError();

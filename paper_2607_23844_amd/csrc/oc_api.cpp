@@ -528,24 +528,19 @@ oc_status oc_attn_full(const oc_shape *shape, const oc_cfg *cfg, const void *x, 
     const Plan p = full_plan(p0);
     const Layout L = make_layout(p0);
     if ((s = check_ws(ws, ws_bytes, workspace_for(shape, cfg))) != OC_OK) return s;
-    int32_t *flag = at<int32_t>(ws, L.flag);
-    int32_t *kept = at<int32_t>(ws, L.kept), *cached = at<int32_t>(ws, L.cached), *rmap = at<int32_t>(ws, L.rmap);
-    // spatial layers keep every token in place (the identity row map needs
-    // no index list); temporal layers gather one sequence per position
-    const bool identity = p.kind == KIND_TOKEN;
-    if (!identity) {
-        HIP_TRY(launch_fill_i32(flag, (long)p.F * p.N, 0, stream), "fill");
-        HIP_TRY(launch_compact(p, nullptr, flag, at<int32_t>(ws, L.mtok), at<int32_t>(ws, L.fcnt), kept, cached,
-                               rmap, 0, stream), "compact");
-    }
+    // no index lists: spatial layers keep every token in place, temporal
+    // layers take one sequence per position (row n*F + f is token f*N + n)
+    const bool temporal = p.kind == KIND_BLOCK;
     const AttnWs aw = attn_ws(p, p.n_seq, p.seq_len, L.attn);
     AttnArgs a;
     std::memset(&a, 0, sizeof(a));
-    a.x = x; a.row_idx = identity ? nullptr : kept; a.n_main = p.n_kept;
+    a.tF = temporal ? p.F : 0;
+    a.tN = p.N;
+    a.x = x; a.row_idx = nullptr; a.n_main = p.n_kept;
     a.ctx = shape->n_ctx > 0 ? ctx : nullptr; a.n_ctx = shape->n_ctx;
     a.n_seq = p.n_seq; a.L = p.seq_len;
     a.wq = w->wq; a.wk = w->wk; a.wv = w->wv; a.wo = w->wo;
-    a.y = y; a.out_idx = identity ? nullptr : kept; a.y_ctx = y_ctx;
+    a.y = y; a.out_idx = nullptr; a.y_ctx = y_ctx;
     a.q = at<char>(ws, aw.q); a.k = at<char>(ws, aw.k); a.o = at<char>(ws, aw.o); a.vt = at<char>(ws, aw.v);
     a.lpad = aw.lpad;
     a.wo16 = at<char>(ws, aw.wo16);

@@ -7,12 +7,25 @@ namespace oc {
 
 // Batch row r of the reduced attention: x rows (through row_idx) then the
 // context rows.  nullptr past the end (a zero row for the tile loaders).
+// Batch row r (< n_main) -> token: through idx when given, else, for the
+// uncached temporal layer (tF > 0), the sequence-per-position order
+// r = n*tF + f -> token f*tN + n, else r itself.
+__device__ __forceinline__ long batch_token(int r, const int32_t *idx, int tF, int tN) {
+    if (idx != nullptr) return idx[r];
+    if (tF > 0) {
+        const int n = r / tF;
+        return (long)(r - n * tF) * tN + n;
+    }
+    return r;
+}
+
 struct RowMap {
     const uint16_t *x; const int32_t *row_idx; int n_main;
     const uint16_t *ctx; int n_rows; int C;
+    int tF, tN;
     __device__ __forceinline__ const uint16_t *row(int r) const {
         if (r >= n_rows) return nullptr;
-        if (r < n_main) return x + (long)(row_idx ? row_idx[r] : r) * C;
+        if (r < n_main) return x + batch_token(r, row_idx, tF, tN) * C;
         return ctx + (long)(r - n_main) * C;
     }
 };

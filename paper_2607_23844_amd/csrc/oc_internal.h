@@ -150,6 +150,7 @@ struct AttnArgs {
     void *wo16;                       // workspace: wo converted to fp16 (bf16 layers)
     int wo16_ready;                   // wo16 already converted by an earlier launch of this call
     int lpad;                         // padded keys per sequence in vt
+    int tF, tN;                       // no index lists: row r = n*tF + f is token f*tN + n (tF > 0)
 };
 hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st);
 bool attn_head_dim_supported(int dh);
