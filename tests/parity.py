@@ -19,7 +19,7 @@ from oracle import oc_oracle as O
 import paper_2607_23844_amd as oc
 
 BAND = 1e-4
-TOL = {"bf16": 2e-2, "f32": 1e-4}
+TOL = {"bf16": 1e-2, "f32": 1e-4}
 NODE_MAX_TOL = {"token": 2e-6, "block": 2e-6, "frame": 1e-5}
 
 
@@ -55,9 +55,18 @@ def shapes(wl, gran=None, r=None, r_frame=None, patch_k=None, cold="matched"):
     return sh, cf, osh, ocf
 
 
-def rel_err(y: np.ndarray, ref: np.ndarray) -> float:
+def rel_err(y: np.ndarray, ref: np.ndarray, out_dtype: str = "f32") -> float:
+    """Largest |y - ref| over RMS(ref).  For bf16 outputs the part that the
+    final rounding of ref to bf16 accounts for (half a bf16 ulp of ref, 8
+    significant bits) is taken off every element first: a correctly rounded
+    result scores 0, and what remains is the error of the computation
+    itself."""
     rms = float(np.sqrt(np.mean(ref * ref)))
-    return float(np.max(np.abs(y - ref))) / max(rms, 1e-30)
+    d = np.abs(y - ref)
+    if out_dtype == "bf16":
+        _, e = np.frexp(np.abs(ref))          # |ref| = f * 2^e, f in [0.5, 1)
+        d = np.maximum(d - np.ldexp(1.0, e - 9), 0.0)
+    return float(np.max(d)) / max(rms, 1e-30)
 
 
 def group_margins(x64: np.ndarray, g: O.Group) -> np.ndarray:
@@ -194,11 +203,11 @@ def layer_step_parity(wl, x_np, sh, cf, osh, ocf, cache, ws, ora_cache, valid, c
     _, forced, st = decision_parity(x64, osh, ocf, tr, valid)
     res = O.layer_step(x64, ctx64, W64, osh, ocf, ora_cache, valid, forced=forced)
     check_maps(tr, res.kept_idx, res.cached_idx, res.restore_map)
-    err = rel_err(to_f64(y).reshape(res.y.shape), res.y)
+    err = rel_err(to_f64(y).reshape(res.y.shape), res.y, wl.dtype)
     tol = TOL[wl.dtype]
     assert err <= tol, f"layer output error {err:.3g} > {tol}"
     if ctx64 is not None:
-        e2 = rel_err(to_f64(y_ctx), res.y_ctx)
+        e2 = rel_err(to_f64(y_ctx), res.y_ctx, wl.dtype)
         assert e2 <= tol, f"context output error {e2:.3g} > {tol}"
         err = max(err, e2)
     st.update(err=err)
@@ -249,7 +258,7 @@ def layer_step_sampled_parity(wl, x_np, sh, cf, osh, ocf, cache, ws, valid, W, W
     check_maps(tr, kept_idx, cached_idx, rmap)
     ref = sampled_outputs(x64, W64, osh, seqs, kept_idx, rmap, positions, y_prev)
     got = to_f64(y).reshape(-1, osh.C)[positions]
-    err = rel_err(got, ref)
+    err = rel_err(got, ref, wl.dtype)
     tol = TOL[wl.dtype]
     assert err <= tol, f"sampled layer output error {err:.3g} > {tol}"
     st.update(err=err, n_kept=len(kept_idx), n_seq=len(seqs))

@@ -90,7 +90,7 @@ def test_small_layer_chain(case, cold):
 # individual entry points
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("dtype,dh,n_seq,L,n_ctx", [
-    ("bf16", 64, 1, 2381 - 333, 333), ("bf16", 64, 3, 130, 0), ("bf16", 72, 5, 77, 0), ("bf16", 72, 7, 16, 0),
+    ("bf16", 64, 1, 2381 - 333, 333), ("bf16", 64, 3, 130, 0), ("bf16", 64, 2, 700, 0), ("bf16", 64, 2, 256, 0), ("bf16", 72, 5, 77, 0), ("bf16", 72, 7, 16, 0),
     ("bf16", 16, 2, 9, 0), ("bf16", 128, 1, 200, 5), ("f32", 64, 1, 128, 0), ("f32", 16, 3, 33, 0),
 ])
 def test_attn_reduced_vs_oracle(dtype, dh, n_seq, L, n_ctx):
@@ -110,11 +110,11 @@ def test_attn_reduced_vs_oracle(dtype, dh, n_seq, L, n_ctx):
                             ctx=dev_tensor(wl, ctx_s) if n_ctx else None)
     torch.cuda.synchronize()
     yk64, yc64 = O.attn_reduced(wl.f64(xk_s), wl.f64(ctx_s) if n_ctx else None, weights_f64(wl), heads, dh)
-    e = rel_err(to_f64(y), yk64)
-    _say(f"  err {e:.3g}")
+    e = rel_err(to_f64(y), yk64, dtype)
+    _say(f"  err {e:.3g} (raw {rel_err(to_f64(y), yk64):.3g})")
     assert e <= TOL[dtype]
     if n_ctx:
-        assert rel_err(to_f64(yc), yc64) <= TOL[dtype]
+        assert rel_err(to_f64(yc), yc64, dtype) <= TOL[dtype]
 
 
 def test_gather_restore_bit_exact():
@@ -281,6 +281,6 @@ def test_svdxt_level_temporal_full_sampled():
     got = to_f64(y).reshape(wl.F, wl.H * wl.W, wl.C)[:, ns, :]
     ref = np.stack([O.multi_head_attention(x64[:, n, :], W64["wq"], W64["wk"], W64["wv"], W64["wo"], wl.heads,
                                            wl.head_dim) for n in ns], axis=1)
-    err = rel_err(got, ref)
+    err = rel_err(got, ref, wl.dtype)
     _say(f"  temporal layer sampled error {err:.3g}")
     assert err <= TOL[wl.dtype]
