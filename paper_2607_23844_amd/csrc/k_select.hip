@@ -19,6 +19,7 @@ namespace oc {
 constexpr int SEL_THREADS = 1024;
 constexpr int SEL_WAVES = SEL_THREADS / 64;
 constexpr int SEL_IPT = 16;            // candidates per thread: groups up to 16384
+constexpr int SEL_HISTS = 4;           // radix histograms (one per SIMD)
 
 
 // One block per group.  PACKED: node_max / node_idx are unpacked from the
@@ -38,8 +39,9 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
                                                         int32_t *__restrict__ mtok, int32_t *__restrict__ kept_idx,
                                                         int32_t *__restrict__ cached_idx,
                                                         int32_t *__restrict__ rmap, int N, int L) {
-    // per-wave digit histograms, double-buffered across radix passes
-    __shared__ int hist[2][SEL_WAVES][256];
+    // digit histograms, one per SIMD (waves w, w+4, ... share one),
+    // double-buffered across radix passes
+    __shared__ int hist[2][SEL_HISTS][256];
     __shared__ uint32_t red[3][SEL_WAVES];
     __shared__ int sh[17];
     __shared__ int sel_info[3];
@@ -56,34 +58,54 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
     const int R = gr.R;
     const int n_src = min(gr.nsrc, S);
 
-    int32_t nid[SEL_IPT];   // slab layout
+    // slab layout: every load of the thread's candidates is issued first
+    // (one round trip), then they are unpacked
+    int32_t nid[SEL_IPT], sids[SEL_IPT];
+    unsigned long long pk[SEL_IPT];
+    float iv[SEL_IPT];
 #pragma unroll
     for (int j = 0; j < SEL_IPT; ++j) {
         nid[j] = -1;
+        sids[j] = -1;
+        if (j >= ipt) continue;
+        const int i = j * SEL_THREADS + t;
+        const long gi = (long)g * S + i;
+        const int sid = i < S ? gm.src_id(gr, i) : -1;
+        sids[j] = sid;
+        pk[j] = 0;
+        iv[j] = 0.f;
+        if (sid >= 0) {
+            if constexpr (PACKED) {
+                pk[j] = node_pack[gi];
+                iv[j] = inv[sid];
+            } else {
+                iv[j] = node_max_in[gi];
+                nid[j] = node_idx_in[gi];
+            }
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < SEL_IPT; ++j) {
         const int i = j * SEL_THREADS + t;
         if (j >= ipt || i >= S) continue;
         const long gi = (long)g * S + i;
-        const int sid = gm.src_id(gr, i);
-        if (sid < 0) {
+        if (sids[j] < 0) {
             if (PACKED && node_max_out != nullptr) {
                 node_max_out[gi] = -INFINITY;
                 node_idx_out[gi] = -1;
             }
             continue;
         }
-        float v;
+        float v = iv[j];
         if constexpr (PACKED) {
             int ix;
-            unpack_argmax(node_pack[gi], v, ix);
-            v *= inv[sid];
+            unpack_argmax(pk[j], v, ix);
+            v *= iv[j];
             nid[j] = ix >= 0 ? gm.dst_id(gr, ix) : -1;
             if (node_max_out != nullptr) {
                 node_max_out[gi] = v;
                 node_idx_out[gi] = nid[j];
             }
-        } else {
-            v = node_max_in[gi];
-            nid[j] = node_idx_in[gi];
         }
         klds[i] = float_key(v);
     }
@@ -117,7 +139,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
         red[2][wave] = hi;
     }
     // clear both histogram buffers meanwhile
-    for (int e = t; e < 2 * SEL_WAVES * 256; e += SEL_THREADS) (&hist[0][0][0])[e] = 0;
+    for (int e = t; e < 2 * SEL_HISTS * 256; e += SEL_THREADS) (&hist[0][0][0])[e] = 0;
     __syncthreads();
     int n_valid = 0;
     uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
@@ -149,7 +171,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
             const int bit_lo = max(bit_hi - 7, 0);
             const int nbits = bit_hi - bit_lo + 1;
             const uint32_t dmask = (1u << nbits) - 1u;
-            int *hw = hist[buf][wave];
+            int *hw = hist[buf][wave % SEL_HISTS];
 #pragma unroll
             for (int j = 0; j < SEL_IPT; ++j)
                 if (((vmask >> j) & 1u) && (key[j] & mask) == prefix) atomicAdd(&hw[(key[j] >> bit_lo) & dmask], 1);
@@ -161,7 +183,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
                 for (int q = 0; q < 4; ++q) {
                     int cq = 0;
 #pragma unroll
-                    for (int w = 0; w < SEL_WAVES; ++w) cq += hist[buf][w][4 * t + q];
+                    for (int w = 0; w < SEL_HISTS; ++w) cq += hist[buf][w][4 * t + q];
                     c[q] = cq;
                     sum += cq;
                 }
@@ -183,7 +205,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
                 }
             }
             // the other buffer, used by the next pass, was last read a pass ago
-            for (int e = t; e < SEL_WAVES * 256; e += SEL_THREADS) (&hist[buf ^ 1][0][0])[e] = 0;
+            for (int e = t; e < SEL_HISTS * 256; e += SEL_THREADS) (&hist[buf ^ 1][0][0])[e] = 0;
             __syncthreads();
             const int sel = sel_info[0];
             remaining -= sel_info[1];
@@ -192,14 +214,18 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
             mask |= dmask << bit_lo;
             bit_hi = bit_lo - 1;
             buf ^= 1;
+            // the whole selected bin is taken: every key of it is >= prefix
+            // (lower bits zero) and every key below it is < prefix, so prefix
+            // is an exact threshold with no tie to break
+            if (remaining == n_eq) break;
         }
         tau = prefix;
         need = remaining;
     }
 
     // exact selection: key > tau, or key == tau among the first `need` in
-    // index order; without a tie to break (every key equal to tau taken) no
-    // rank is needed
+    // index order; without a tie to break (every key equal to tau taken, or
+    // the passes stopped at a bin taken whole) no rank is needed
     const bool tie = !none && !all && need < n_eq;
     int eq_rank = 0;
     if (tie) {
@@ -234,7 +260,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
         const int i = j * SEL_THREADS + t;
         if (j >= ipt || i >= n_src) continue;
         const bool c = all || (!none && cbyte[i] != 0);
-        const int id = gm.src_id(gr, i);
+        const int id = sids[j];
         flag[id] = c ? 1 : 0;
         mtok[id] = c ? nid[j] : -1;
         if (compact) fl[id - fbase] = c ? 1 : 0;
