@@ -65,8 +65,7 @@ def stage_work(shape, pl, n_ctx):
     attn_flop = 4.0 * pl.n_seq * lk * lk * hd
     S, D, G = pl.n_src_max, pl.n_dst_max, pl.n_groups
     return {
-        "proj_qk": ("mfma", 2.0 * rows * C * 2 * hd),
-        "proj_v": ("mfma", 2.0 * rows * C * hd),
+        "proj_qkv": ("mfma", 2.0 * rows * C * 3 * hd),
         "flash": ("mfma", attn_flop),
         "proj_out": ("mfma", 2.0 * rows * hd * C),
         "match": ("mfma", 2.0 * G * S * D * C),

@@ -92,7 +92,9 @@ AttnWs attn_ws(const Plan &p, int n_seq, int L, size_t base) {
     w.k = w.q + m;
     w.o = w.k + m;
     w.v = w.o + m;
-    const size_t vb = p.bf16 ? al((size_t)p.heads * n_seq * p.dh * w.lpad * e) : m;
+    // Vt (or, for short sequences, V rows: never more than m)
+    const size_t vt = al((size_t)p.heads * n_seq * p.dh * w.lpad * e);
+    const size_t vb = p.bf16 ? (vt > m ? vt : m) : m;
     w.wo16 = w.v + vb;
     const size_t wb = p.bf16 ? al((size_t)p.C * p.hd * 2) : 0;
     w.bytes = w.wo16 + wb - base;

@@ -400,15 +400,16 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
 }
 
 // Short sequences (at most 64 keys, e.g. temporal attention over frames):
-// one wave per (sequence, head), no LDS and no barriers.  The wave holds K
-// and Vt of the whole sequence in registers (KB blocks of 32 keys) and, per
+// one wave per (sequence, head), no LDS and no barriers.  V comes by rows
+// here (the projection writes it like Q and K).  The wave holds K and the
+// Vt fragments of the whole sequence in registers (KB blocks of 32 keys) and, per
 // block of 32 queries, computes S^T = K Q^T, the exact row maximum, P =
 // exp2(s - max) in fp16, the running sum of that fp16 P, and O^T = Vt P^T on
 // the same MFMA layouts as the long-sequence kernel.
 template <int DH, int KB>
 __global__ __launch_bounds__(256) void k_attn_short(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
-                                                     const uint16_t *__restrict__ Vt, uint16_t *__restrict__ O, int hd,
-                                                     int heads, int n_seq, int L, int Lk, int lpad) {
+                                                     const uint16_t *__restrict__ V, uint16_t *__restrict__ O, int hd,
+                                                     int heads, int n_seq, int L, int Lk) {
     constexpr int DK = (DH + 15) / 16 * 16, NKS = DK / 16;
     constexpr int DV = (DH + 31) / 32 * 32, NDB = DV / 32;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, ln = lane & 31, lg = lane >> 5;
@@ -416,7 +417,6 @@ __global__ __launch_bounds__(256) void k_attn_short(const uint16_t *__restrict__
     if (unit >= (long)n_seq * heads) return;   // whole waves only; the kernel has no block barrier
     const int h = (int)(unit % heads), s = (int)(unit / heads);
     const long row0 = (long)s * L;
-    const uint16_t *vbase = Vt + ((long)h * n_seq + s) * DH * lpad;
     auto ld = [](const uint16_t *p, bool ok) {
         uint4 v = make_uint4(0, 0, 0, 0);
         if (ok) v = *reinterpret_cast<const uint4 *>(p);
@@ -432,17 +432,22 @@ __global__ __launch_bounds__(256) void k_attn_short(const uint16_t *__restrict__
             kf[kb][ks] = ld(K + (row0 + key) * hd + h * DH + d0, key < Lk && d0 < DH);
         }
     }
-    // Vt positions whose key is past the end are zeroed here (the padding of
-    // Vt is not guaranteed for short sequences)
+    // V is stored by rows here: the A operand of O^T = Vt P^T (lane: d, 8
+    // keys) is gathered from 8 rows, in the key order of the score slots
+    // (vt_key_of_pos); keys past the end are zero
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int k4 = 0; k4 < 2 * KB; ++k4) {
             const int d = db * 32 + ln;
-            f16x8 v = ld(vbase + (long)d * lpad + k4 * 16 + lg * 8, d < DH);
+            f16x8 v;
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                if (k4 * 16 + vt_key_of_pos(lg * 8 + e) >= Lk) v[e] = (_Float16)0.f;
+            for (int e = 0; e < 8; ++e) {
+                const int key = k4 * 16 + vt_key_of_pos(lg * 8 + e);
+                uint16_t b = 0;
+                if (key < Lk && d < DH) b = V[(row0 + key) * hd + h * DH + d];
+                v[e] = __builtin_bit_cast(_Float16, b);
+            }
             vf[db][k4] = v;
         }
     const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
@@ -518,8 +523,7 @@ template <int DH, int KB>
 static hipError_t go_short(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
     const long waves = (long)a.n_seq * p.heads;
     launch_k(k_attn_short<DH, KB>, (unsigned)((waves + 3) / 4), 256, 0, st, (const uint16_t *)a.q,
-             (const uint16_t *)a.k, (const uint16_t *)a.vt, (uint16_t *)a.o, p.hd, p.heads, a.n_seq, a.L, Lk,
-             a.lpad);
+             (const uint16_t *)a.k, (const uint16_t *)a.vt, (uint16_t *)a.o, p.hd, p.heads, a.n_seq, a.L, Lk);
     return hipGetLastError();
 }
 
@@ -546,8 +550,7 @@ static hipError_t go(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
 // allows it.
 template <int DH>
 static hipError_t go_dh(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
-    if (Lk <= 32) return go_short<DH, 1>(p, a, Lk, st);
-    if (Lk <= 64) return go_short<DH, 2>(p, a, Lk, st);
+    if (attn_short(Lk)) return Lk <= 32 ? go_short<DH, 1>(p, a, Lk, st) : go_short<DH, 2>(p, a, Lk, st);
     if constexpr (DH % 64 == 0) {
         if (flash_uses_dma(DH, Lk, p.hd)) return go<DH, 4, true>(p, a, Lk, st);
     }

@@ -5,8 +5,8 @@
 // in fp16 (three more mantissa bits than bf16, same MFMA rate): Q is stored
 // pre-multiplied by log2(e)/sqrt(head_dim) so that the attention kernel's
 // scores are already in the log2 domain.
-//   k_proj_qk : [rows, C] x [2*H*dh, C]^T -> Q, K [rows, H*dh]
-//   k_proj_v  : -> Vt [H][seq][dh][Lpad], keys contiguous per (head, d),
+//   k_proj_qkv: [rows, C] x [3*H*dh, C]^T -> Q, K [rows, H*dh] and
+//               Vt [H][seq][dh][Lpad], keys contiguous per (head, d),
 //               quads 1 and 2 of every 16-key block swapped (vt_key_of_pos)
 //   k_proj_out: O [rows, H*dh] (fp16) x wo [C, H*dh] -> y rows, written
 //               straight to their positions (row -> out_idx[row]) or to the
@@ -14,9 +14,9 @@
 // Rows r < n_main come from x (through row_idx when given); rows after them
 // are the uncached context tokens of a single sequence.
 //
-// Engines: with K a multiple of 64 the LDS-DMA tile (Q/K: 128 x 128 double
-// buffered; V and output: 128 x 64, three stages), the register-staged tile
-// (128 x 128) otherwise.  Epilogues go through LDS: the tile is staged as
+// Engines: with K a multiple of 64 the LDS-DMA tile (Q/K/V: 128 x 128
+// double buffered; output: 128 x 64, three stages), the register-staged
+// tile (128 x 128) otherwise.  Epilogues go through LDS: the tile is staged as
 // whole output rows and written in 16-byte chunks, so every store is a
 // contiguous run of a row (Vt rows included).
 //
@@ -98,63 +98,69 @@ static hipError_t allow_lds(KernelPtr k, size_t bytes, bool &done) {
 }
 
 // ---------------------------------------------------------------------------
-// Q, K: a in [0, 2*hd) are rows of wq then wk; b = batch rows.  The DMA
-// engine runs double-buffered here (two blocks per CU).
+// Q, K and V in one launch of 128 x 128 tiles.  The first n_qk tiles are
+// row tiles: a in [0, nw*hd) are rows of wq, wk (and wv when nw = 3), b =
+// batch rows, staged as rows of Q, K (and of V, row-major [rows, H*dh], for
+// short sequences, whose attention reads V by rows).  With nw = 2 the rest
+// are V tiles with the roles swapped: a = batch
+// rows, b in [0, hd) = rows of wv, so that a staged row is a row of
+// Vt[h][s][d][pos].  V tiles whose rows are a 16-aligned run of one
+// sequence (a single sequence, or L % 128 == 0) are written as Vt rows:
+// the positions of the tile's tokens, zero for positions past the end (the
+// key padding up to lpad), in whole chunks.  Otherwise elements are stored
+// one by one and, when the attention kernel needs it, the key padding is
+// zeroed separately.  The DMA engine runs double-buffered (two blocks per
+// CU).
 // ---------------------------------------------------------------------------
 template <bool DMA>
-using QKTile = typename std::conditional<DMA, DmaTile<128, 128, 2, 2, false, 2>, MfmaTile<128, 128, 2, 2>>::type;
+using QKVTile = typename std::conditional<DMA, DmaTile<128, 128, 2, 2, false, 2>, MfmaTile<128, 128, 2, 2>>::type;
 
 template <bool DMA>
-__global__ __launch_bounds__(256) void k_proj_qk(RowMap rm, const uint16_t *__restrict__ wq,
-                                                 const uint16_t *__restrict__ wk, int hd, float qscale, int n_at,
-                                                 int n_bt, uint16_t *__restrict__ Q, uint16_t *__restrict__ K) {
-    using T = QKTile<DMA>;
+__global__ __launch_bounds__(256) void k_proj_qkv(RowMap rm, const uint16_t *__restrict__ wq,
+                                                  const uint16_t *__restrict__ wk, const uint16_t *__restrict__ wv,
+                                                  int hd, int dh, float qscale, int nw, int n_qk_at, int n_v_bt, int n_bt,
+                                                  int n_seq, int L, int lpad, int zero_pad,
+                                                  uint16_t *__restrict__ Q, uint16_t *__restrict__ K,
+                                                  uint16_t *__restrict__ Vt) {
+    using T = QKVTile<DMA>;
+    using Rows = typename std::conditional<DMA, DmaRows, RegRows>::type;
     constexpr int BA = 128, BB = 128;
     extern __shared__ __align__(16) uint16_t lds[];
-    int at, bt;
-    tile_order(xcd_remap(blockIdx.x, n_at * n_bt), n_at, n_bt, at, bt);
+    const int n_qk = n_qk_at * n_bt;
+    const int total = n_qk + n_bt * n_v_bt;
+    const int lid = xcd_remap(blockIdx.x, total);
     const uint16_t *rowsA[T::CA], *rowsB[T::CB];
-#pragma unroll
-    for (int i = 0; i < T::CA; ++i) {
-        const int a = at * BA + T::chunk_row(i);
-        rowsA[i] = a < hd ? wq + (long)a * rm.C : (a < 2 * hd ? wk + (long)(a - hd) * rm.C : nullptr);
-    }
-#pragma unroll
-    for (int i = 0; i < T::CB; ++i) rowsB[i] = rm.row(bt * BB + T::chunk_row(i));
     T t;
-    run_tile(t, lds, rowsA, rowsB, wq, rm.row(0), rm.C, typename std::conditional<DMA, DmaRows, RegRows>::type{});
-    const int a0 = at * BA, b0 = bt * BB;
-    stage_rows<BA>(t, lds, [&](float v, int a) { return f2h_bits(a0 + a < hd ? v * qscale : v); },
-                   [](int a) { return a; });
-    __syncthreads();
-    write_rows<BA, BB>(lds, min(BA, 2 * hd - a0), [&](int b, int c0) -> uint16_t * {
-        const int r = b0 + b, a = a0 + c0;
-        if (r >= rm.n_rows) return nullptr;
-        return a < hd ? Q + (long)r * hd + a : K + (long)r * hd + (a - hd);
-    });
-}
-
-// ---------------------------------------------------------------------------
-// V: a = batch rows, b in [0, hd) = rows of wv.  Vt[h][s][d][pos].  Tiles
-// whose rows are a 16-aligned run of one sequence (a single sequence, or
-// L % 128 == 0) are staged as Vt rows: the positions of the tile's tokens,
-// zero for positions past the end (the key padding up to lpad), written
-// as whole chunks.  Otherwise elements are stored one by one and, when the
-// attention kernel needs it, the key padding is zeroed separately.
-// ---------------------------------------------------------------------------
-template <bool DMA>
-using VTile = typename std::conditional<DMA, DmaTile<128, 64, 2, 2>, MfmaTile<128, 128, 2, 2>>::type;
-
-template <bool DMA>
-__global__ __launch_bounds__(256) void k_proj_v(RowMap rm, const uint16_t *__restrict__ wv, int hd, int dh,
-                                                int n_seq, int L, int lpad, int n_at, int n_bt, int zero_pad,
-                                                uint16_t *__restrict__ Vt) {
-    using T = VTile<DMA>;
-    constexpr int BA = 128, BB = DMA ? 64 : 128;
-    extern __shared__ __align__(16) uint16_t lds[];
+    if (lid < n_qk) {
+        int at, bt;
+        tile_order(lid, n_qk_at, n_bt, at, bt);
+#pragma unroll
+        for (int i = 0; i < T::CA; ++i) {
+            const int a = at * BA + T::chunk_row(i);
+            const uint16_t *w = a < hd ? wq + (long)a * rm.C
+                              : a < 2 * hd ? wk + (long)(a - hd) * rm.C
+                                           : wv + (long)(a - 2 * hd) * rm.C;
+            rowsA[i] = a < nw * hd ? w : nullptr;
+        }
+#pragma unroll
+        for (int i = 0; i < T::CB; ++i) rowsB[i] = rm.row(bt * BB + T::chunk_row(i));
+        run_tile(t, lds, rowsA, rowsB, wq, rm.row(0), rm.C, Rows{});
+        const int a0 = at * BA, b0 = bt * BB;
+        stage_rows<BA>(t, lds, [&](float v, int a) { return f2h_bits(a0 + a < hd ? v * qscale : v); },
+                       [](int a) { return a; });
+        __syncthreads();
+        write_rows<BA, BB>(lds, min(BA, nw * hd - a0), [&](int b, int c0) -> uint16_t * {
+            const int r = b0 + b, a = a0 + c0;
+            if (r >= rm.n_rows) return nullptr;
+            return a < hd ? Q + (long)r * hd + a
+                 : a < 2 * hd ? K + (long)r * hd + (a - hd)
+                              : Vt + (long)r * hd + (a - 2 * hd);
+        });
+        return;
+    }
+    // V tile: at over batch rows, bt over features
     int at, bt;
-    tile_order(xcd_remap(blockIdx.x, n_at * n_bt), n_at, n_bt, at, bt);
-    const uint16_t *rowsA[T::CA], *rowsB[T::CB];
+    tile_order(lid - n_qk, n_bt, n_v_bt, at, bt);
 #pragma unroll
     for (int i = 0; i < T::CA; ++i) rowsA[i] = rm.row(at * BA + T::chunk_row(i));
 #pragma unroll
@@ -162,8 +168,7 @@ __global__ __launch_bounds__(256) void k_proj_v(RowMap rm, const uint16_t *__res
         const int b = bt * BB + T::chunk_row(i);
         rowsB[i] = b < hd ? wv + (long)b * rm.C : nullptr;
     }
-    T t;
-    run_tile(t, lds, rowsA, rowsB, rm.row(0), wv, rm.C, typename std::conditional<DMA, DmaRows, RegRows>::type{});
+    run_tile(t, lds, rowsA, rowsB, rm.row(0), wv, rm.C, Rows{});
     const int Lk = n_seq == 1 ? rm.n_rows : L;
     const int r0 = at * BA, f0 = bt * BB;
     if (n_seq == 1 || L % BA == 0) {
@@ -198,10 +203,10 @@ __global__ __launch_bounds__(256) void k_proj_v(RowMap rm, const uint16_t *__res
                 }
     }
     // zero the padded key positions [Lk, lpad) of this block's features, for
-    // the sequences s = at, at + n_at, ... (the DMA-staged attention reads them)
+    // the sequences s = at, at + n_bt, ... (the DMA-staged attention reads them)
     const int npad = lpad - Lk;
     if (zero_pad && npad > 0) {
-        for (int sq = at; sq < n_seq; sq += n_at)
+        for (int sq = at; sq < n_seq; sq += n_bt)
             for (int idx = threadIdx.x; idx < BB * npad; idx += blockDim.x) {
                 const int f = f0 + idx / npad, jj = Lk + idx % npad;
                 if (f >= hd) continue;
@@ -213,34 +218,21 @@ __global__ __launch_bounds__(256) void k_proj_v(RowMap rm, const uint16_t *__res
 
 hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, hipStream_t st) {
     const float qscale = (float)(1.4426950408889634 / sqrt((double)p.dh));
-    {
-        StageScope _stage(st, "proj_qk");
-        const int n_at = cdiv(2 * p.hd, 128), n_bt = cdiv(rm.n_rows, 128);
-        if (p.C % 64 == 0) {
-            launch_k(k_proj_qk<true>, n_at * n_bt, 256, QKTile<true>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
-                     (const uint16_t *)a.wk, p.hd, qscale, n_at, n_bt, (uint16_t *)a.q, (uint16_t *)a.k);
-        } else {
-            launch_k(k_proj_qk<false>, n_at * n_bt, 256, QKTile<false>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
-                     (const uint16_t *)a.wk, p.hd, qscale, n_at, n_bt, (uint16_t *)a.q, (uint16_t *)a.k);
-        }
-    }
-    {
-        StageScope _stage(st, "proj_v");
-        const int Lk = a.n_seq == 1 ? rm.n_rows : a.L;
-        const int zero_pad = flash_uses_dma(p.dh, Lk, p.hd) ? 1 : 0;
-        const int n_at = cdiv(rm.n_rows, 128);
-        if (p.C % 64 == 0) {
-            static bool attr = false;
-            hipError_t e = allow_lds(k_proj_v<true>, VTile<true>::LDS_BYTES, attr);
-            if (e != hipSuccess) return e;
-            const int n_bt = cdiv(p.hd, 64);
-            launch_k(k_proj_v<true>, n_at * n_bt, 256, VTile<true>::LDS_BYTES, st, 
-                rm, (const uint16_t *)a.wv, p.hd, p.dh, a.n_seq, a.L, a.lpad, n_at, n_bt, zero_pad, (uint16_t *)a.vt);
-        } else {
-            const int n_bt = cdiv(p.hd, 128);
-            launch_k(k_proj_v<false>, n_at * n_bt, 256, VTile<false>::LDS_BYTES, st, 
-                rm, (const uint16_t *)a.wv, p.hd, p.dh, a.n_seq, a.L, a.lpad, n_at, n_bt, zero_pad, (uint16_t *)a.vt);
-        }
+    StageScope _stage(st, "proj_qkv");
+    const int Lk = a.n_seq == 1 ? rm.n_rows : a.L;
+    const int zero_pad = flash_uses_dma(p.dh, Lk, p.hd) ? 1 : 0;
+    // short sequences: V rows from the Q/K tiles (nw = 3), no V tiles
+    const int nw = attn_short(Lk) ? 3 : 2;
+    const int n_qk_at = cdiv(nw * p.hd, 128), n_v_bt = nw == 3 ? 0 : cdiv(p.hd, 128), n_bt = cdiv(rm.n_rows, 128);
+    const int total = n_qk_at * n_bt + n_bt * n_v_bt;
+    if (p.C % 64 == 0) {
+        launch_k(k_proj_qkv<true>, total, 256, QKVTile<true>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
+                 (const uint16_t *)a.wk, (const uint16_t *)a.wv, p.hd, p.dh, qscale, nw, n_qk_at, n_v_bt, n_bt, a.n_seq,
+                 a.L, a.lpad, zero_pad, (uint16_t *)a.q, (uint16_t *)a.k, (uint16_t *)a.vt);
+    } else {
+        launch_k(k_proj_qkv<false>, total, 256, QKVTile<false>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
+                 (const uint16_t *)a.wk, (const uint16_t *)a.wv, p.hd, p.dh, qscale, nw, n_qk_at, n_v_bt, n_bt, a.n_seq,
+                 a.L, a.lpad, zero_pad, (uint16_t *)a.q, (uint16_t *)a.k, (uint16_t *)a.vt);
     }
     return hipGetLastError();
 }

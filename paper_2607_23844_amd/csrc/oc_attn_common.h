@@ -63,6 +63,11 @@ inline bool flash_uses_dma(int dh, int Lk, int hd) {
     return dh % 64 == 0 && dh <= 128 && Lk >= 256 && (long)Lk * hd * 2 < (1L << 31);
 }
 
+// Whether the attention runs the register-only kernel for short sequences
+// (at most 64 keys).  V is then stored row-major like Q and K ([rows, H*dh],
+// fp16) instead of as Vt.
+inline bool attn_short(int Lk) { return Lk <= 64; }
+
 hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, hipStream_t st);
 hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStream_t st);
 hipError_t launch_flash(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st);
