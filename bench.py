@@ -27,30 +27,40 @@ sys.path.insert(0, ROOT)
 METRIC = "cached attn-layer tokens/sec & latency vs uncached at r; MFMA % / HBM GB/s"
 PEAK_MFMA_TFLOPS = 2516.6     # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
-# Counter summary of the dominant kernel (rocprofv3 FETCH_SIZE / WRITE_SIZE
-# runs, scaled by a copy kernel of known size) and the sources it was taken on.
+# Counter summary of the step's kernels (rocprofv3 FETCH_SIZE / WRITE_SIZE
+# runs, scaled by a copy kernel of known size) and the sources each was taken on.
 PROFILE = os.path.join(ROOT, "profiles", "sd3_1024_r050_kernels.md")
-FLASH_SOURCES = ("k_flash.hip", "oc_attn_common.h", "oc_device.h")
+_COMMON = ("oc_attn_common.h", "oc_device.h")
+KERNEL_SOURCES = {
+    "flash": ("k_flash.hip",) + _COMMON,
+    "proj_qkv": ("k_proj.hip", "oc_dma_tile.h", "oc_mfma_tile.h") + _COMMON,
+    "proj_out": ("k_proj.hip", "oc_dma_tile.h", "oc_mfma_tile.h") + _COMMON,
+    "match": ("k_match.hip", "oc_dma_tile.h", "oc_mfma_tile.h", "oc_groups.h", "oc_device.h"),
+    "select": ("k_select.hip", "oc_groups.h", "oc_block.h", "oc_device.h"),
+    "inv_norm": ("k_match.hip", "oc_device.h"),
+}
 
 
-def flash_source_hash():
+def kernel_source_hash(stage):
+    """First 16 hex digits of the SHA-1 of the stage's kernel sources."""
     import hashlib
     h = hashlib.sha1()
-    for f in FLASH_SOURCES:
+    for f in KERNEL_SOURCES[stage]:
         with open(os.path.join(ROOT, "paper_2607_23844_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def flash_traffic():
-    """HBM bytes per flash launch from the committed counter summary, or None
-    when there is none or the kernel's sources changed since it was taken."""
+def kernel_traffic(stage):
+    """HBM bytes per launch of a stage's kernel from the committed counter
+    summary, or None when there is none or its sources changed since."""
     try:
         with open(PROFILE) as fh:
-            kv = dict(l.split(":", 1) for l in fh.read().splitlines() if l.startswith("flash_"))
-        if kv["flash_source_sha1"].strip() != flash_source_hash():
+            kv = dict((k.strip(), v.strip()) for k, v in
+                      (l.split(":", 1) for l in fh.read().splitlines() if l.startswith(("traffic.", "sha1."))))
+        if stage not in KERNEL_SOURCES or kv[f"sha1.{stage}"] != kernel_source_hash(stage):
             return None
-        return int(float(kv["flash_traffic_bytes_per_launch"]))
+        return int(float(kv[f"traffic.{stage}"]))
     except (OSError, KeyError, ValueError):
         return None
 
@@ -283,6 +293,9 @@ def run_gpu(args):
     for name, (tot_ms, n) in stages.items():
         avg_us = tot_ms * 1e3 / max(n, 1)
         d = dict(avg_us=round(avg_us, 3), launches_per_step=n / K)
+        tr = kernel_traffic(name)
+        if tr is not None:
+            d["traffic"] = tr
         if name in work:
             kind, amount = work[name]
             if kind == "mfma":
@@ -295,7 +308,7 @@ def run_gpu(args):
     dom = max(stages, key=lambda s: stages[s][0])
     dom_avg_us = stages[dom][0] * 1e3 / stages[dom][1]
     roof = None
-    traffic = flash_traffic() if dom == "flash" else None
+    traffic = kernel_traffic(dom)
     if dom in work:
         kind, amount = work[dom]
         if kind == "mfma":
