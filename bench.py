@@ -143,8 +143,9 @@ def timed_ms(fn, inputs, K, W):
 
 def run_other_configs(args):
     """The Latte-like spatial (Frame Cache) and temporal (Block Cache) layers
-    and the SVD-XT-like level (Frame+Token spatial layer, uncached temporal
-    layer): warm cached latency against the uncached layer."""
+    and the SVD-XT-like level (Frame+Token spatial layer with whole-frame or
+    patch-local token matching, uncached temporal layer): warm cached latency
+    against the uncached layer."""
     import numpy as np
     import torch
     import paper_2607_23844_amd as oc
@@ -154,8 +155,11 @@ def run_other_configs(args):
     dev = torch.device("cuda:0")
     K, Wm = args.cfg_steps, 3
     out = {}
+    # SVD-XT twice: token matching over whole frames (k = 1) and patch-local
+    # (k = 4: 4x4 patches, the paper's hierarchy for lower matching cost)
     for key, name in (("latte_spatial_frame_cache", "latte_spatial"), ("latte_temporal_block_cache", "latte_temporal"),
-                      ("svdxt_level_frame_token_cache", "svdxt_level")):
+                      ("svdxt_level_frame_token_cache", "svdxt_level"),
+                      ("svdxt_level_frame_token_cache_k4", "svdxt_level_k4")):
         wl = make_workload(name, 3)
 
         def t(a):

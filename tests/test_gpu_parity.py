@@ -73,6 +73,11 @@ SMALL = [
     dict(gran="frame_token", F=9, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r_frame=0.45, patch_k=2,
          planted=True),
     dict(gran="frame_token", F=6, H=8, W=8, C=32, heads=2, head_dim=16, dtype="f32", r_frame=0.35, planted=True),
+    # every candidate cached (r < 1 is required; floor(0.99 * 64) = 63 is
+    # clamped to the 48 candidates): only the representatives (and the
+    # context) are computed
+    dict(gran="token", F=1, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r=0.99, n_ctx=3),
+    dict(gran="block", F=4, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r=0.99),
 ]
 
 
