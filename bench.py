@@ -195,10 +195,35 @@ def run_other_configs(args):
     return out
 
 
+def run_data_movement_svdxt(args):
+    """The gather and restore entry points at the SVD-XT-like level (25
+    frames of 9216 tokens, C = 320, 92160 retained rows): large enough for
+    HBM bandwidth rather than launch latency to set their time."""
+    import numpy as np
+    import torch
+    import paper_2607_23844_amd as oc
+    from oc_synth import make_workload
+
+    dev = torch.device("cuda:0")
+    wl = make_workload("svdxt_level", 2)
+
+    def t(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    xs = [t(s) for s in wl.steps]
+    W = {k: t(getattr(wl, k)) for k in ("wq", "wk", "wv", "wo")}
+    shape = oc.Shape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, 0, "bf16")
+    cfg = oc.Cfg(wl.gran, r=wl.r, r_frame=wl.r_frame, patch_k=wl.patch_k)
+    res = run_data_movement(args, shape, cfg, W, xs, None)
+    del xs, W
+    torch.cuda.empty_cache()
+    return res
+
+
 def run_data_movement(args, shape, cfg, W, xs, ctx):
-    """The standalone gather and (in-place) restore entry points at the SD3
-    shape: kernel time and HBM GB/s (2 n_kept C bytes-per-element moved) with
-    warm caches and after a 512 MiB write that flushes L2 and MALL."""
+    """The standalone gather and (in-place) restore entry points: kernel time
+    and HBM GB/s (2 n_kept C bytes-per-element moved) with warm caches and
+    after a 512 MiB write that flushes L2 and MALL."""
     import torch
     import paper_2607_23844_amd as oc
 
@@ -383,6 +408,8 @@ def main():
         del src, dst
     g = run_gpu(args)
     others = None if args.no_configs else run_other_configs(args)
+    if not args.no_configs:
+        g["moves"]["svdxt_level"] = run_data_movement_svdxt(args)
     cpu = None if args.no_cpu else run_cpu_baseline(args)
     ms = g["ms"]
     line = {

@@ -1,34 +1,81 @@
 // Coalesced row movement: gather of retained rows and restoration of cached
 // positions (OmniCache §3.2.1 / §3.2.3 restoration at the original
-// positions; App. A gather-scatter).  Each thread moves one 16-byte chunk of
-// a row; consecutive threads cover consecutive chunks of a row.
+// positions; App. A gather-scatter).  Rows move in 16-byte chunks,
+// consecutive threads on consecutive chunks of a row.
 #include "oc_internal.h"
 #include "oc_launch.h"
 #include "oc_device.h"
 
 namespace oc {
 
+// A thread moves CPT 16-byte chunks of one row: with upr = cpr / CPT
+// threads per row, thread l of a row takes chunks l, l + upr, ... so that
+// each load and store instruction of a wave covers consecutive chunks.  All
+// loads are issued before the stores.  Index math is 32-bit unless the
+// chunk count reaches 2^31 (WIDE).
+template <int CPT, bool WIDE>
+__device__ __forceinline__ void unit_of(long u, int upr, long &row, int &lane) {
+    if constexpr (WIDE) {
+        row = u / upr;
+        lane = (int)(u - row * upr);
+    } else {
+        const int r = (int)u / upr;
+        row = r;
+        lane = (int)u - r * upr;
+    }
+}
+
+// CPT chunks at stride upr: every load before any store, in named registers
+// (a private array here was placed in LDS by the compiler)
+template <int CPT>
+__device__ __forceinline__ void copy_chunks(const uint4 *src, uint4 *dst, int upr) {
+    if constexpr (CPT == 4) {
+        const uint4 a = src[0], b = src[upr], c = src[2 * upr], d = src[3 * upr];
+        dst[0] = a;
+        dst[upr] = b;
+        dst[2 * upr] = c;
+        dst[3 * upr] = d;
+    } else {
+        static_assert(CPT == 1, "one or four chunks per thread");
+        dst[0] = src[0];
+    }
+}
+
 // x_kept[i] = x[kept_idx[i]]
+template <int CPT, bool WIDE>
 __global__ void k_gather(const uint4 *__restrict__ x, const int32_t *__restrict__ kept_idx, int n_rows, int cpr,
                          long n_src_rows, uint4 *__restrict__ out) {
-    const long total = (long)n_rows * cpr;
-    for (long c = (long)blockIdx.x * blockDim.x + threadIdx.x; c < total; c += (long)gridDim.x * blockDim.x) {
-        const int r = (int)(c / cpr), j = (int)(c - (long)r * cpr);
+    const int upr = cpr / CPT;
+    const long total = (long)n_rows * upr;
+    for (long u = (long)blockIdx.x * blockDim.x + threadIdx.x; u < total; u += (long)gridDim.x * blockDim.x) {
+        long r;
+        int l;
+        unit_of<CPT, WIDE>(u, upr, r, l);
         const int s = kept_idx[r];
-        if (s >= 0 && s < n_src_rows) out[c] = x[(long)s * cpr + j];
+        if (s < 0 || s >= n_src_rows) continue;
+        const uint4 *src = x + (long)s * cpr + l;
+        uint4 *dst = out + r * cpr + l;
+        copy_chunks<CPT>(src, dst, upr);
     }
 }
 
 // y[p] = y_kept[map[p]] (0 <= map < n_rows) or cache_y[p] (map == -1)
+template <int CPT, bool WIDE>
 __global__ void k_restore(const uint4 *__restrict__ yk, int n_rows, const int32_t *__restrict__ rmap,
                           const uint4 *cache, long n_pos, int cpr, uint4 *y) {
-    const long total = n_pos * cpr;
-    for (long c = (long)blockIdx.x * blockDim.x + threadIdx.x; c < total; c += (long)gridDim.x * blockDim.x) {
-        const long p = c / cpr;
-        const int j = (int)(c - p * cpr);
+    const int upr = cpr / CPT;
+    const long total = n_pos * upr;
+    for (long u = (long)blockIdx.x * blockDim.x + threadIdx.x; u < total; u += (long)gridDim.x * blockDim.x) {
+        long p;
+        int l;
+        unit_of<CPT, WIDE>(u, upr, p, l);
         const int m = rmap[p];
-        if (m >= 0 && m < n_rows) y[c] = yk[(long)m * cpr + j];
-        else if (m == -1 && cache != nullptr && cache != y) y[c] = cache[c];
+        const uint4 *src;
+        if (m >= 0 && m < n_rows) src = yk + (long)m * cpr + l;
+        else if (m == -1 && cache != nullptr && cache != y) src = cache + p * cpr + l;
+        else continue;
+        uint4 *dst = y + p * cpr + l;
+        copy_chunks<CPT>(src, dst, upr);
     }
 }
 
@@ -59,14 +106,26 @@ static unsigned grid_for(long chunks) {
     return (unsigned)(b < 1 ? 1 : (b > 8192 ? 8192 : b));
 }
 
+template <typename G4, typename G1>
+static void launch_rows(long rows, int cpr, G4 four, G1 one) {
+    const bool by4 = cpr % 4 == 0;
+    const long units = rows * (by4 ? cpr / 4 : cpr);
+    const bool wide = units >= (1L << 31);
+    if (by4) four(units, wide);
+    else one(units, wide);
+}
+
 hipError_t launch_gather(const Plan &p, const void *x, const int32_t *kept_idx, int n_rows, void *x_kept,
                          hipStream_t st) {
     const int cpr = p.C * p.esz / 16;
-    {
-        StageScope _stage(st, "gather");
-        launch_k(k_gather, grid_for((long)n_rows * cpr), 256, 0, st, (const uint4 *)x, kept_idx, n_rows, cpr,
-                                                               (long)p.F * p.N, (uint4 *)x_kept);
-    }
+    const long n_src = (long)p.F * p.N;
+    StageScope _stage(st, "gather");
+    auto go = [&](auto kern, long units) {
+        launch_k(kern, grid_for(units), 256, 0, st, (const uint4 *)x, kept_idx, n_rows, cpr, n_src, (uint4 *)x_kept);
+    };
+    launch_rows(n_rows, cpr,
+                [&](long u, bool wide) { wide ? go(k_gather<4, true>, u) : go(k_gather<4, false>, u); },
+                [&](long u, bool wide) { wide ? go(k_gather<1, true>, u) : go(k_gather<1, false>, u); });
     return hipGetLastError();
 }
 
@@ -74,11 +133,14 @@ hipError_t launch_restore(const Plan &p, const void *y_kept, int n_rows, const i
                           void *y, hipStream_t st) {
     const int cpr = p.C * p.esz / 16;
     const long n_pos = (long)p.F * p.N;
-    {
-        StageScope _stage(st, "restore");
-        launch_k(k_restore, grid_for(n_pos * cpr), 256, 0, st, (const uint4 *)y_kept, n_rows, rmap, (const uint4 *)cache_y,
-                                                         n_pos, cpr, (uint4 *)y);
-    }
+    StageScope _stage(st, "restore");
+    auto go = [&](auto kern, long units) {
+        launch_k(kern, grid_for(units), 256, 0, st, (const uint4 *)y_kept, n_rows, rmap, (const uint4 *)cache_y, n_pos,
+                 cpr, (uint4 *)y);
+    };
+    launch_rows(n_pos, cpr,
+                [&](long u, bool wide) { wide ? go(k_restore<4, true>, u) : go(k_restore<4, false>, u); },
+                [&](long u, bool wide) { wide ? go(k_restore<1, true>, u) : go(k_restore<1, false>, u); });
     return hipGetLastError();
 }
 
