@@ -114,7 +114,12 @@ hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st) {
     if (n_rows == 0) return hipSuccess;
     if (p.bf16) {
         const RowMap rm{(const uint16_t *)a.x, a.row_idx, a.n_main, (const uint16_t *)a.ctx, n_rows, p.C, a.tF, a.tN};
-        hipError_t e = launch_proj_qkv(p, rm, a, st);
+        hipError_t e;
+        if (qkv_attn_short_applies(p, a)) {
+            if ((e = launch_qkv_attn_short(p, rm, a, st)) != hipSuccess) return e;
+            return launch_proj_out(p, n_rows, a, st);
+        }
+        e = launch_proj_qkv(p, rm, a, st);
         if (e != hipSuccess) return e;
         if ((e = launch_flash(p, a, Lk, st)) != hipSuccess) return e;
         return launch_proj_out(p, n_rows, a, st);

@@ -68,6 +68,11 @@ inline bool flash_uses_dma(int dh, int Lk, int hd) {
 // fp16) instead of as Vt.
 inline bool attn_short(int Lk) { return Lk <= 64; }
 
+// Q/K/V projection and attention fused for short sequences of head dim 64
+// (k_short.hip); O is then projected by launch_proj_out.
+bool qkv_attn_short_applies(const Plan &p, const AttnArgs &a);
+hipError_t launch_qkv_attn_short(const Plan &p, const RowMap &rm, const AttnArgs &a, hipStream_t st);
+
 hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, hipStream_t st);
 hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStream_t st);
 hipError_t launch_flash(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st);

@@ -67,6 +67,7 @@ SMALL = [
     dict(gran="token", F=1, H=24, W=24, C=128, heads=2, head_dim=64, dtype="bf16", r=0.75, patch_k=3),
     dict(gran="block", F=6, H=8, W=8, C=64, heads=2, head_dim=16, dtype="bf16"),
     dict(gran="block", F=5, H=8, W=12, C=48, heads=3, head_dim=16, dtype="f32", patch_k=2),
+    dict(gran="block", F=9, H=8, W=8, C=128, heads=2, head_dim=64, dtype="bf16"),
     dict(gran="frame", F=8, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", planted=True, r_frame=0.25),
     dict(gran="frame", F=7, H=4, W=8, C=32, heads=2, head_dim=16, dtype="f32", planted=True, r_frame=0.45),
     dict(gran="frame_token", F=7, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r_frame=0.3, planted=True),
@@ -95,7 +96,10 @@ def test_small_layer_chain(case, cold):
 # individual entry points
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("dtype,dh,n_seq,L,n_ctx", [
-    ("bf16", 64, 1, 2381 - 333, 333), ("bf16", 64, 3, 130, 0), ("bf16", 64, 2, 700, 0), ("bf16", 64, 2, 256, 0), ("bf16", 72, 5, 77, 0), ("bf16", 72, 7, 16, 0),
+    ("bf16", 64, 1, 2381 - 333, 333), ("bf16", 64, 3, 130, 0), ("bf16", 64, 2, 700, 0), ("bf16", 64, 2, 256, 0),
+    # head dim 64, at most 64 keys: projection and attention fused per tile of
+    # whole sequences (ragged last tile; 2, 3, 5 and 128 sequences per tile)
+    ("bf16", 64, 7, 25, 0), ("bf16", 64, 5, 64, 0), ("bf16", 64, 4, 33, 0), ("bf16", 64, 130, 1, 0), ("bf16", 72, 5, 77, 0), ("bf16", 72, 7, 16, 0),
     ("bf16", 16, 2, 9, 0), ("bf16", 128, 1, 200, 5), ("f32", 64, 1, 128, 0), ("f32", 16, 3, 33, 0),
 ])
 def test_attn_reduced_vs_oracle(dtype, dh, n_seq, L, n_ctx):
