@@ -394,7 +394,7 @@ __global__ __launch_bounds__(256) void k_match_part_reduce(const float *__restri
 }
 
 // fp32 similarity + arg-max (small fp32 layers): one thread per candidate.
-__global__ void k_match_f32(const float *__restrict__ x, const float *__restrict__ inv, GroupMap gm, int G, int S,
+__global__ void k_match_f32(const float *__restrict__ x, const float *__restrict__ inv, GroupMap gm, int /*G*/, int S,
                             int D, int K, int seg_len, long sub_stride, long item_stride,
                             unsigned long long *__restrict__ node_pack) {
     const int g = blockIdx.y;

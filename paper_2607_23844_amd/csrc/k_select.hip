@@ -34,7 +34,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
                                                         const unsigned long long *__restrict__ node_pack,
                                                         const float *__restrict__ inv,
                                                         float *__restrict__ node_max_out,
-                                                        int32_t *__restrict__ node_idx_out, GroupMap gm, int G,
+                                                        int32_t *__restrict__ node_idx_out, GroupMap gm, int /*G*/,
                                                         int S, int D, int32_t *__restrict__ flag,
                                                         int32_t *__restrict__ mtok, int32_t *__restrict__ kept_idx,
                                                         int32_t *__restrict__ cached_idx,
