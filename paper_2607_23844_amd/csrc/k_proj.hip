@@ -241,18 +241,22 @@ hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, h
 // Output projection: a in [0, C) = rows of wo (fp16); b = batch rows of O.
 // y[out row][a].
 // ---------------------------------------------------------------------------
-template <bool DMA>
-using OTile =
-    typename std::conditional<DMA, DmaTile<128, 64, 2, 2, true>, MfmaTile<128, 128, 2, 2, true, false>>::type;
+// Tiles: 128 output features x 64 rows (three-stage DMA); for C a multiple
+// of 160 but not of 128 (e.g. 320) 160 features x 128 rows (double-buffered,
+// one wave row of four), so that no feature column is computed in vain.
+template <bool DMA, int BA = 128>
+using OTile = typename std::conditional<
+    DMA, typename std::conditional<BA == 160, DmaTile<160, 128, 1, 4, true, 2>, DmaTile<128, 64, 2, 2, true>>::type,
+    MfmaTile<128, 128, 2, 2, true, false>>::type;
 
-template <bool DMA>
+template <bool DMA, int BA>
 __global__ __launch_bounds__(256) void k_proj_out(const uint16_t *__restrict__ O, int n_rows, int hd,
                                                   const uint16_t *__restrict__ wo, int C, int n_main,
                                                   const int32_t *__restrict__ out_idx, int tF, int tN, int n_at,
                                                   int n_bt,
                                                   uint16_t *__restrict__ y, uint16_t *__restrict__ y_ctx) {
-    using T = OTile<DMA>;
-    constexpr int BA = 128, BB = DMA ? 64 : 128;
+    using T = OTile<DMA, BA>;
+    constexpr int BB = DMA ? (BA == 160 ? 128 : 64) : 128;
     extern __shared__ __align__(16) uint16_t lds[];
     int at, bt;
     tile_order(xcd_remap(blockIdx.x, n_at * n_bt), n_at, n_bt, at, bt);
@@ -295,20 +299,26 @@ hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStre
                                                                             (uint4 *)a.wo16);
     }
     StageScope _stage(st, "proj_out");
-    const int n_at = cdiv(p.C, 128);
+    auto go = [&](auto kern, size_t lds, int BA, int BB) -> hipError_t {
+        const int n_at = cdiv(p.C, BA), n_bt = cdiv(n_rows, BB);
+        launch_k(kern, n_at * n_bt, 256, lds, st, (const uint16_t *)a.o, n_rows, p.hd, (const uint16_t *)a.wo16, p.C,
+                 a.n_main, a.out_idx, a.tF, a.tN, n_at, n_bt, (uint16_t *)a.y, (uint16_t *)a.y_ctx);
+        return hipSuccess;
+    };
     if (p.hd % 64 == 0) {
-        static bool attr = false;
-        hipError_t e = allow_lds(k_proj_out<true>, OTile<true>::LDS_BYTES, attr);
-        if (e != hipSuccess) return e;
-        const int n_bt = cdiv(n_rows, 64);
-        launch_k(k_proj_out<true>, n_at * n_bt, 256, OTile<true>::LDS_BYTES, st, 
-            (const uint16_t *)a.o, n_rows, p.hd, (const uint16_t *)a.wo16, p.C, a.n_main, a.out_idx, a.tF, a.tN, n_at, n_bt,
-            (uint16_t *)a.y, (uint16_t *)a.y_ctx);
+        if (p.C % 160 == 0 && p.C % 128 != 0) {
+            static bool attr = false;
+            hipError_t e = allow_lds(k_proj_out<true, 160>, OTile<true, 160>::LDS_BYTES, attr);
+            if (e != hipSuccess) return e;
+            go(k_proj_out<true, 160>, OTile<true, 160>::LDS_BYTES, 160, 128);
+        } else {
+            static bool attr = false;
+            hipError_t e = allow_lds(k_proj_out<true, 128>, OTile<true, 128>::LDS_BYTES, attr);
+            if (e != hipSuccess) return e;
+            go(k_proj_out<true, 128>, OTile<true, 128>::LDS_BYTES, 128, 64);
+        }
     } else {
-        const int n_bt = cdiv(n_rows, 128);
-        launch_k(k_proj_out<false>, n_at * n_bt, 256, OTile<false>::LDS_BYTES, st, 
-            (const uint16_t *)a.o, n_rows, p.hd, (const uint16_t *)a.wo16, p.C, a.n_main, a.out_idx, a.tF, a.tN, n_at, n_bt,
-            (uint16_t *)a.y, (uint16_t *)a.y_ctx);
+        go(k_proj_out<false, 128>, OTile<false, 128>::LDS_BYTES, 128, 128);
     }
     return hipGetLastError();
 }
