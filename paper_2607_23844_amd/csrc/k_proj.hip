@@ -14,9 +14,9 @@
 // Rows r < n_main come from x (through row_idx when given); rows after them
 // are the uncached context tokens of a single sequence.
 //
-// Engines: with K a multiple of 64 the LDS-DMA tile (Q/K/V: 128 x 128
-// double buffered; output: 128 x 64, three stages), the register-staged
-// tile (128 x 128) otherwise.  Epilogues go through LDS: the tile is staged as
+// Engines: with K a multiple of 64 the LDS-DMA tile, double buffered (Q/K/V:
+// 128 x 128; output: 128 x 64, or 160 x 128 when C = 160 k), the
+// register-staged tile (128 x 128) otherwise.  Epilogues go through LDS: the tile is staged as
 // whole output rows and written in 16-byte chunks, so every store is a
 // contiguous run of a row (Vt rows included).
 //
@@ -241,12 +241,12 @@ hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, h
 // Output projection: a in [0, C) = rows of wo (fp16); b = batch rows of O.
 // y[out row][a].
 // ---------------------------------------------------------------------------
-// Tiles: 128 output features x 64 rows (three-stage DMA); for C a multiple
-// of 160 but not of 128 (e.g. 320) 160 features x 128 rows (double-buffered,
-// one wave row of four), so that no feature column is computed in vain.
+// Tiles (double-buffered DMA): 128 output features x 64 rows; for C a
+// multiple of 160 but not of 128 (e.g. 320) 160 features x 128 rows (one
+// wave row of four), so that no feature column is computed in vain.
 template <bool DMA, int BA = 128>
 using OTile = typename std::conditional<
-    DMA, typename std::conditional<BA == 160, DmaTile<160, 128, 1, 4, true, 2>, DmaTile<128, 64, 2, 2, true>>::type,
+    DMA, typename std::conditional<BA == 160, DmaTile<160, 128, 1, 4, true, 2>, DmaTile<128, 64, 2, 2, true, 2>>::type,
     MfmaTile<128, 128, 2, 2, true, false>>::type;
 
 template <bool DMA, int BA>
