@@ -45,7 +45,8 @@ namespace oc {
 
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
-constexpr float REBASE = 8.f;   // P = exp2(s - m) stays below 2^REBASE on the fast path
+constexpr float REBASE = 8.f;
+constexpr int FLASH_CUS = 256;   // compute units of the MI355X   // P = exp2(s - m) stays below 2^REBASE on the fast path
 
 template <int DH, bool DMA>
 struct FlashCfg {
@@ -546,13 +547,19 @@ static hipError_t go(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
 }
 
 // By sequence length: up to 64 keys the register-only short kernel, else
-// four waves (32 queries each) per block, DMA-staged when the head dim
-// allows it.
+// four waves (32 queries each) per block (eight when the grid is small),
+// DMA-staged when the head dim allows it.
 template <int DH>
 static hipError_t go_dh(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
     if (attn_short(Lk)) return Lk <= 32 ? go_short<DH, 1>(p, a, Lk, st) : go_short<DH, 2>(p, a, Lk, st);
     if constexpr (DH % 64 == 0) {
-        if (flash_uses_dma(DH, Lk, p.hd)) return go<DH, 4, true>(p, a, Lk, st);
+        if (flash_uses_dma(DH, Lk, p.hd)) {
+            // a grid of four-wave blocks that would not fill two per CU:
+            // eight-wave blocks (256 queries share each K/V tile)
+            const long blocks4 = (long)cdiv(Lk, 128) * p.heads * a.n_seq;
+            if (blocks4 <= 2L * FLASH_CUS) return go<DH, 8, true>(p, a, Lk, st);
+            return go<DH, 4, true>(p, a, Lk, st);
+        }
     }
     return go<DH, 4, false>(p, a, Lk, st);
 }
