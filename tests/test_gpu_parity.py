@@ -206,6 +206,54 @@ def test_repeat_runs_are_bit_identical():
         assert all(torch.equal(a, b) for a, b in zip(o, outs[0]))
 
 
+@pytest.mark.parametrize("kw", [
+    dict(gran="token", F=1, H=16, W=16, C=128, heads=2, head_dim=64, dtype="bf16", n_ctx=5),
+    dict(gran="block", F=9, H=8, W=8, C=128, heads=2, head_dim=64, dtype="bf16"),
+    dict(gran="frame_token", F=7, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r_frame=0.3, planted=True),
+], ids=["token_ctx", "block_dh64", "frame_token"])
+def test_graph_replay_matches_eager(kw):
+    """A warm cached step captured once in a HIP graph and replayed, with the
+    program's own eager work and synchronisations between the replays: every
+    replay leaves the same layer output as the eager step (the step is
+    idempotent on a warm cache: retained rows are rewritten, cached ones kept)."""
+    from paper_2607_23844_amd.runner import LayerRunner
+    kw = dict(kw)
+    wl = small_workload(kw.pop("gran"), n_steps=2, seed=7, **kw)
+    sh, cf, _, _ = shapes(wl)
+    dev = torch.device("cuda:0")
+    x0, x1 = dev_tensor(wl, wl.steps[0]), dev_tensor(wl, wl.steps[1])
+    ctx = dev_tensor(wl, wl.ctx) if wl.n_ctx else None
+    run = LayerRunner(sh, cf, weights_dev(wl), dev, ctx)
+    run(x0)
+    run(x1)
+    torch.cuda.synchronize()
+    ref = run.cache.y.view(torch.int16).clone()
+    ref_ctx = run.y_ctx.view(torch.int16).clone() if ctx is not None else None
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run.use_current_stream()
+        run(x1)
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run.use_current_stream()
+        run(x1)
+    run.use_current_stream()
+    scratch = torch.zeros(1 << 20, device=dev)
+    for i in range(4):
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(run.cache.y.view(torch.int16), ref), f"replay {i}"
+        if ref_ctx is not None:
+            assert torch.equal(run.y_ctx.view(torch.int16), ref_ctx), f"replay {i} (context rows)"
+        scratch.add_(1.0)          # eager work between the replays
+        torch.cuda.synchronize()
+        run(x1)                    # and an eager step of the layer itself
+        torch.cuda.synchronize()
+        assert torch.equal(run.cache.y.view(torch.int16), ref), f"eager step after replay {i}"
+
+
 # ---------------------------------------------------------------------------
 # full-size workloads (the shapes the benchmark times)
 # ---------------------------------------------------------------------------
