@@ -16,10 +16,12 @@
 
 namespace oc {
 
-constexpr int SEL_THREADS = 1024;
-constexpr int SEL_WAVES = SEL_THREADS / 64;
-constexpr int SEL_IPT = 16;            // candidates per thread: groups up to 16384
+constexpr int SEL_IPT = 16;            // candidates per thread: groups up to 16 x the block size
 constexpr int SEL_HISTS = 4;           // radix histograms (one per SIMD)
+// Block size: eight waves for small groups (up to 4 candidates per thread:
+// fewer waves per barrier), sixteen otherwise (up to 16384 candidates; four
+// waves with 12 candidates each measured 50% slower than sixteen at 3072)
+constexpr int SEL_SMALL = 512, SEL_LARGE = 1024;
 
 
 // One block per group.  PACKED: node_max / node_idx are unpacked from the
@@ -27,8 +29,11 @@ constexpr int SEL_HISTS = 4;           // radix histograms (one per SIMD)
 // last) and written out when node_max_out is given; otherwise they are read.
 // With kept_idx (one group per plain frame) the block then compacts its
 // frame: retained tokens in ascending id become rows [g*L, g*L+L), cached
-// ones go to cached_idx[g*Rc...] (Rc = the frame's static budget).
-template <bool PACKED>
+// ones go to cached_idx[g*Rc...] (Rc = the frame's static budget).  Block
+// Cache (tF = F > 0, one group of all N positions): the b-th retained
+// position becomes sequence b (rows b*F + f, token f*N + n), cached
+// positions ascend frame-major in cached_idx[f*Rc + rank].
+template <bool PACKED, int SEL_THREADS>
 __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict__ node_max_in,
                                                         const int32_t *__restrict__ node_idx_in,
                                                         const unsigned long long *__restrict__ node_pack,
@@ -38,7 +43,8 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
                                                         int S, int D, int32_t *__restrict__ flag,
                                                         int32_t *__restrict__ mtok, int32_t *__restrict__ kept_idx,
                                                         int32_t *__restrict__ cached_idx,
-                                                        int32_t *__restrict__ rmap, int N, int L) {
+                                                        int32_t *__restrict__ rmap, int N, int L, int tF) {
+    constexpr int SEL_WAVES = SEL_THREADS / 64;
     // digit histograms, one per SIMD (waves w, w+4, ... share one),
     // double-buffered across radix passes
     __shared__ int hist[2][SEL_HISTS][256];
@@ -303,7 +309,20 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
         const int crank = wcnt[j * SEL_WAVES + wave] + __builtin_popcountll(b & below);
         const int krank = n - crank;
         const int pid = (int)(fbase + n);
-        if (c) {
+        if (tF > 0) {
+            // Block Cache: the position's F tokens
+            for (int f = 0; f < tF; ++f) {
+                const int tok = f * N + n;
+                if (c) {
+                    if (crank < n_c) cached_idx[(long)f * n_c + crank] = tok;
+                    rmap[tok] = -1;
+                } else {
+                    const int row = krank * tF + f;
+                    if (krank < L) kept_idx[row] = tok;
+                    rmap[tok] = krank < L ? row : -2;
+                }
+            }
+        } else if (c) {
             if (crank < n_c) cached_idx[(long)g * n_c + crank] = pid;
             rmap[pid] = -1;
         } else {
@@ -314,13 +333,25 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
     }
 }
 
+// the small block while the candidates fit 4 per thread and the
+// compaction's (slab, wave) counts fit one per thread
+static bool select_small(const Plan &p, bool compact) {
+    return p.n_src_max <= SEL_SMALL * 4 && (!compact || p.N <= SEL_SMALL * 64);
+}
+
 hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_max, const int32_t *node_idx,
                          int32_t *flag, int32_t *mtok, hipStream_t st) {
     {
         StageScope _stage(st, "select");
-        launch_k(k_select<false>, p.n_groups, SEL_THREADS, (size_t)p.n_src_max * 4, st, node_max, node_idx, nullptr, nullptr, nullptr, nullptr,
-                                                            group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max,
-                                                            flag, mtok, nullptr, nullptr, nullptr, p.N, p.seq_len);
+        const size_t lds = (size_t)p.n_src_max * 4;
+        if (select_small(p, false))
+            launch_k(k_select<false, SEL_SMALL>, p.n_groups, SEL_SMALL, lds, st, node_max, node_idx, nullptr, nullptr,
+                     nullptr, nullptr, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok, nullptr,
+                     nullptr, nullptr, p.N, p.seq_len, 0);
+        else
+            launch_k(k_select<false, SEL_LARGE>, p.n_groups, SEL_LARGE, lds, st, node_max, node_idx, nullptr, nullptr,
+                     nullptr, nullptr, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok, nullptr,
+                     nullptr, nullptr, p.N, p.seq_len, 0);
     }
     return hipGetLastError();
 }
@@ -330,12 +361,20 @@ hipError_t launch_select_packed(const Plan &p, const int32_t *units, const unsig
                                 int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap, hipStream_t st) {
     const bool compact = kept_idx != nullptr;
     if (compact && !select_compacts(p)) return hipErrorInvalidValue;
+    // Block Cache: sequences of F tokens, n_seq of them
+    const int tF = compact && p.kind == KIND_BLOCK ? p.F : 0;
+    const int L = tF > 0 ? p.n_seq : p.seq_len;
     {
         StageScope _stage(st, "select");
-        launch_k(k_select<true>, p.n_groups, SEL_THREADS, (size_t)p.n_src_max * 4, st, nullptr, nullptr, node_pack, inv, node_max, node_idx,
-                                                           group_map(p, units), p.n_groups, p.n_src_max,
-                                                           p.n_dst_max, flag, mtok, kept_idx, cached_idx, rmap, p.N,
-                                                           p.seq_len);
+        const size_t lds = (size_t)p.n_src_max * 4;
+        if (select_small(p, compact))
+            launch_k(k_select<true, SEL_SMALL>, p.n_groups, SEL_SMALL, lds, st, nullptr, nullptr, node_pack, inv,
+                     node_max, node_idx, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok,
+                     kept_idx, cached_idx, rmap, p.N, L, tF);
+        else
+            launch_k(k_select<true, SEL_LARGE>, p.n_groups, SEL_LARGE, lds, st, nullptr, nullptr, node_pack, inv,
+                     node_max, node_idx, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok,
+                     kept_idx, cached_idx, rmap, p.N, L, tF);
     }
     return hipGetLastError();
 }

@@ -109,9 +109,10 @@ hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, cha
 hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_max, const int32_t *node_idx,
                          int32_t *flag, int32_t *mtok, hipStream_t st);
 // selection straight from node_pack; node_max / node_idx are written as
-// well when non-null.  With kept_idx given (plain frames, patch_k == 1: one
-// group per frame) the same launch also compacts the frame into kept_idx,
-// cached_idx and rmap, as launch_compact would.
+// well when non-null.  With kept_idx given (plain frames or Block Cache,
+// patch_k == 1: one group per frame, or one group of all positions) the same
+// launch also compacts into kept_idx, cached_idx and rmap, as
+// launch_compact would.
 hipError_t launch_select_packed(const Plan &p, const int32_t *units, const unsigned long long *node_pack,
                                 const float *inv, float *node_max, int32_t *node_idx, int32_t *flag, int32_t *mtok,
                                 int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap, hipStream_t st);
@@ -119,7 +120,7 @@ hipError_t launch_select_packed(const Plan &p, const int32_t *units, const unsig
 // flags are staged in LDS: N below SEL_COMPACT_MAX_N)
 constexpr int SEL_COMPACT_MAX_N = 24576;
 inline bool select_compacts(const Plan &p) {
-    return p.kind == KIND_TOKEN && p.gran != 3 && p.k == 1 && p.N < SEL_COMPACT_MAX_N;
+    return (p.kind == KIND_TOKEN || p.kind == KIND_BLOCK) && p.gran != 3 && p.k == 1 && p.N < SEL_COMPACT_MAX_N;
 }
 hipError_t launch_compact(const Plan &p, const int32_t *units, const int32_t *flag, const int32_t *mtok,
                           int32_t *fcnt, int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap,
