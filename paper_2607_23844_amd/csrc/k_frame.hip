@@ -7,6 +7,8 @@
 #include "oc_internal.h"
 #include "oc_launch.h"
 #include "oc_device.h"
+#include "oc_mfma_tile.h"
+#include <algorithm>
 
 namespace oc {
 
@@ -14,11 +16,14 @@ constexpr int GRAM_WAVES = 4;
 constexpr int GRAM_TARGET_BLOCKS = 1024;
 constexpr int FMAX = 32;   // frames supported by the frame stage
 
+// K range of one wave: a multiple of 64, and of C when the Gram launch also
+// computes the token norms (each wave then covers whole tokens)
 inline int gram_kw(const Plan &p) {
     const long D = (long)p.N * p.C;
+    const long unit = gram_norms(p) ? p.C : 64;
     long kw = (D + (long)GRAM_WAVES * GRAM_TARGET_BLOCKS - 1) / ((long)GRAM_WAVES * GRAM_TARGET_BLOCKS);
-    kw = ((kw + 63) / 64) * 64;
-    return (int)(kw < 64 ? 64 : kw);
+    kw = ((kw + unit - 1) / unit) * unit;
+    return (int)(kw < unit ? unit : kw);
 }
 int gram_blocks(const Plan &p) {
     const long D = (long)p.N * p.C;
@@ -31,10 +36,26 @@ int gram_blocks(const Plan &p) {
 // [g*16+8, g*16+16) of each 64-wide step (g = l / 16); the same fragment is
 // both MFMA operands, so the result is X X^T.  Entry (m, n) of block b goes
 // to part[(m*F + n) * n_blocks + b]: one entry's partials are contiguous.
+// The launch also does the token-level preparation that would otherwise
+// read x again (inv non-null: every wave covers whole tokens of C elements,
+// C a multiple of 64, and writes inv[f*N + n] = 1/||token||, the sum of
+// squares of the 16 lanes' fp32 partials in a fixed order), clears pack[0,
+// n_pack) for the arg-max atomics, and converts wo to fp16 in the blocks
+// past the Gram's (blockIdx.x >= gram_blocks).
 template <bool TWO>
 __global__ __launch_bounds__(256) void k_frame_gram(const uint16_t *__restrict__ x, int F, long D, int kw,
-                                                     float *__restrict__ part) {
+                                                     float *__restrict__ part, int gram_blocks, float *__restrict__ inv,
+                                                     int C, unsigned long long *__restrict__ pack, long n_pack,
+                                                     const uint4 *__restrict__ wo, long n8, uint4 *__restrict__ wo16) {
     __shared__ float red[GRAM_WAVES][FMAX * FMAX];
+    if ((int)blockIdx.x >= gram_blocks) {
+        const long nb = gridDim.x - gram_blocks;
+        for (long i = (long)(blockIdx.x - gram_blocks) * blockDim.x + threadIdx.x; i < n8; i += nb * blockDim.x)
+            wo16[i] = bf16x8_to_f16x8(wo[i]);
+        return;
+    }
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n_pack; i += (long)gram_blocks * blockDim.x)
+        pack[i] = 0ull;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const long k_begin = ((long)blockIdx.x * GRAM_WAVES + wave) * kw;
     const long k_end = min(k_begin + kw, D);
@@ -42,8 +63,12 @@ __global__ __launch_bounds__(256) void k_frame_gram(const uint16_t *__restrict__
     const uint16_t *row0 = fr < F ? x + (long)fr * D : nullptr;
     const uint16_t *row1 = (TWO && fr + 16 < F) ? x + (long)(fr + 16) * D : nullptr;
     f32x4 acc00 = {0, 0, 0, 0}, acc01 = {0, 0, 0, 0}, acc10 = {0, 0, 0, 0}, acc11 = {0, 0, 0, 0};
+    const int csteps = C / 64;   // steps per token (norms)
+    int left = csteps;
+    float ss0 = 0.f, ss1 = 0.f;
     for (long k = k_begin; k < k_end; k += 64) {
         bf16x8 a0[2], a1[2];
+        uint4 r0[2], r1[2];
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
             const long kk = k + g * 16 + t * 8;
@@ -52,8 +77,43 @@ __global__ __launch_bounds__(256) void k_frame_gram(const uint16_t *__restrict__
                 if (row0) v0 = *reinterpret_cast<const uint4 *>(row0 + kk);
                 if (TWO && row1) v1 = *reinterpret_cast<const uint4 *>(row1 + kk);
             }
+            r0[t] = v0;
+            r1[t] = v1;
             a0[t] = *reinterpret_cast<bf16x8 *>(&v0);
             a1[t] = *reinterpret_cast<bf16x8 *>(&v1);
+        }
+        if (inv != nullptr) {
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const uint16_t *e0 = reinterpret_cast<const uint16_t *>(&r0[t]);
+                const uint16_t *e1 = reinterpret_cast<const uint16_t *>(&r1[t]);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const float f0 = bf2f(e0[j]);
+                    ss0 = fmaf(f0, f0, ss0);
+                    if (TWO) {
+                        const float f1 = bf2f(e1[j]);
+                        ss1 = fmaf(f1, f1, ss1);
+                    }
+                }
+            }
+            if (--left == 0) {
+                // token k / C complete: lanes fr, fr+16, fr+32, fr+48 hold its partials
+                left = csteps;
+                float s0 = ss0 + __shfl_xor(ss0, 16, 64);
+                s0 += __shfl_xor(s0, 32, 64);
+                float s1 = 0.f;
+                if (TWO) {
+                    s1 = ss1 + __shfl_xor(ss1, 16, 64);
+                    s1 += __shfl_xor(s1, 32, 64);
+                }
+                ss0 = ss1 = 0.f;
+                const long n = k / C, N = D / C;
+                if (g == 0) {
+                    if (fr < F) inv[fr * N + n] = s0 > 0.f ? (float)(1.0 / sqrt((double)s0)) : 0.f;
+                    if (TWO && fr + 16 < F) inv[(fr + 16) * N + n] = s1 > 0.f ? (float)(1.0 / sqrt((double)s1)) : 0.f;
+                }
+            }
         }
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
@@ -86,7 +146,7 @@ __global__ __launch_bounds__(256) void k_frame_gram(const uint16_t *__restrict__
         float s = red[0][src];
 #pragma unroll
         for (int w = 1; w < GRAM_WAVES; ++w) s += red[w][src];
-        part[(long)e * gridDim.x + blockIdx.x] = s;
+        part[(long)e * gram_blocks + blockIdx.x] = s;
     }
 }
 
@@ -237,7 +297,8 @@ __global__ __launch_bounds__(1024) void k_frame_final(const double *__restrict__
 }
 
 hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, char *ws, float *node_max,
-                              int32_t *node_idx, int32_t *flag, int32_t *mtok, hipStream_t st) {
+                              int32_t *node_idx, int32_t *flag, int32_t *mtok, float *inv,
+                              unsigned long long *pack, long n_pack, const void *wo, void *wo16, hipStream_t st) {
     const long D = (long)p.N * p.C;
     int nb = gram_blocks(p);
     float *part = (float *)(ws + L.gram_part);
@@ -247,16 +308,18 @@ hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, cha
             StageScope _stage(st, "frame_gram");
             launch_k(k_frame_gram_f32, p.F * p.F, 256, 0, st, (const float *)x, p.F, D, part);
         }
-    } else if (p.F > 16)
-        {
-            StageScope _stage(st, "frame_gram");
-            launch_k(k_frame_gram<true>, nb, 256, 0, st, (const uint16_t *)x, p.F, D, gram_kw(p), part);
-        }
-    else
-        {
-            StageScope _stage(st, "frame_gram");
-            launch_k(k_frame_gram<false>, nb, 256, 0, st, (const uint16_t *)x, p.F, D, gram_kw(p), part);
-        }
+    } else {
+        if (inv != nullptr && !gram_norms(p)) return hipErrorInvalidValue;
+        const long n8 = (wo != nullptr && wo16 != nullptr) ? (long)p.C * p.hd / 8 : 0;
+        const int cvt_blocks = n8 > 0 ? (int)std::min<long>((n8 + 255) / 256, 1024) : 0;
+        StageScope _stage(st, "frame_gram");
+        if (p.F > 16)
+            launch_k(k_frame_gram<true>, nb + cvt_blocks, 256, 0, st, (const uint16_t *)x, p.F, D, gram_kw(p), part,
+                     nb, inv, p.C, pack, pack ? n_pack : 0, (const uint4 *)wo, n8, (uint4 *)wo16);
+        else
+            launch_k(k_frame_gram<false>, nb + cvt_blocks, 256, 0, st, (const uint16_t *)x, p.F, D, gram_kw(p), part,
+                     nb, inv, p.C, pack, pack ? n_pack : 0, (const uint4 *)wo, n8, (uint4 *)wo16);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     double *gram = (double *)(ws + L.fgram);

@@ -235,24 +235,32 @@ const int32_t *units_of(const Plan &p, const Layout &L, void *ws) {
 // Match stage.  With reduce, (node_max, node_idx) are produced; without,
 // only the packed arg-max is left in ws for launch_select_packed (frame
 // granularity always produces node_max / node_idx).  Leaves the frame stage
-// and norms in ws; wo / wo16, when given, are converted in the norm launch.
+// and norms in ws; wo / wo16, when given (bf16), are converted in the first
+// launch that reads x (the frame Gram, else the norms).
 oc_status run_match(const Plan &p, const Layout &L, const void *x, float *node_max, int32_t *node_idx, bool reduce,
                     void *ws, hipStream_t st, const void *wo = nullptr, void *wo16 = nullptr) {
     char *w = (char *)ws;
     const bool frames = p.gran == OC_GRAN_FRAME || p.gran == OC_GRAN_FRAME_TOKEN;
+    unsigned long long *pack = at<unsigned long long>(ws, L.node_pack);
+    const long n_pack = (long)p.n_groups * p.n_src_max;
+    // Frame+Token Cache: the Gram launch also writes the token norms and clears pack
+    const bool gram_prep = frames && gram_norms(p);
     if (frames) {
         float *fm = p.gran == OC_GRAN_FRAME ? node_max : at<float>(ws, L.fmax);
         int32_t *fi = p.gran == OC_GRAN_FRAME ? node_idx : at<int32_t>(ws, L.fidx);
         // Frame Cache: the frame stage also writes the per-frame selection
         const bool fsel = p.gran == OC_GRAN_FRAME;
+        const bool cvt = p.bf16 && (fsel || gram_prep);
         HIP_TRY(launch_frame_stage(p, L, x, w, fm, fi, fsel ? at<int32_t>(ws, L.flag) : nullptr,
-                                   fsel ? at<int32_t>(ws, L.mtok) : nullptr, st),
+                                   fsel ? at<int32_t>(ws, L.mtok) : nullptr,
+                                   gram_prep ? at<float>(ws, L.inv) : nullptr, gram_prep ? pack : nullptr, n_pack,
+                                   cvt ? wo : nullptr, cvt ? wo16 : nullptr, st),
                 "frame stage");
     }
     if (p.kind == KIND_FRAME) return OC_OK;
-    unsigned long long *pack = at<unsigned long long>(ws, L.node_pack);
-    HIP_TRY(launch_inv_norm(p, x, at<float>(ws, L.inv), pack, (long)p.n_groups * p.n_src_max, wo, wo16,
-                            (long)p.C * p.hd, st), "inv_norm");
+    if (!gram_prep)
+        HIP_TRY(launch_inv_norm(p, x, at<float>(ws, L.inv), pack, n_pack, wo, wo16, (long)p.C * p.hd, st),
+                "inv_norm");
     HIP_TRY(launch_match(p, x, at<float>(ws, L.inv), units_of(p, L, ws), pack, at<float>(ws, L.mpart),
                          reduce ? node_max : nullptr,
                          reduce ? node_idx : nullptr, st),
@@ -473,8 +481,8 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
     float *nm = at<float>(ws, L.node_max);
     int32_t *ni = at<int32_t>(ws, L.node_idx);
     const AttnWs aw = attn_ws(p, p.n_seq, p.seq_len, L.attn);
-    // bf16 layers: the fp16 copy of wo is made in the norm launch of the match stage
-    const bool wo_early = p.bf16 && p.kind != KIND_FRAME;
+    // bf16 layers: the fp16 copy of wo is made by the first launch of the match stage
+    const bool wo_early = p.bf16;
     if ((s = run_match(p, L, x, nm, ni, false, ws, stream, wo_early ? w->wo : nullptr,
                        wo_early ? at<char>(ws, aw.wo16) : nullptr)) != OC_OK)
         return s;

@@ -46,6 +46,10 @@ struct Layout {
 struct AttnWs { size_t q, k, o, v, wo16, bytes; int lpad; };
 AttnWs attn_ws(const Plan &p, int n_seq, int L, size_t base);
 int gram_blocks(const Plan &p);
+// Whether the frame Gram launch also computes the token norms that token
+// matching needs (Frame+Token Cache, bf16, C a multiple of 64), so that x is
+// read once for both.
+inline bool gram_norms(const Plan &p) { return p.bf16 && p.gran == 3 && p.C % 64 == 0; }
 
 // Stage timing: while a timer is attached to the calling thread, the
 // kernels launched (launch_k, oc_launch.h) inside a StageScope are timed
@@ -103,9 +107,12 @@ hipError_t launch_match(const Plan &p, const void *x, const float *inv, const in
                         unsigned long long *node_pack, float *part, float *node_max, int32_t *node_idx,
                         hipStream_t st);
 // flag / mtok given (Frame Cache): the frame stage also writes the per-frame
-// selection, so no selection launch is needed
-hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, char *ws,
-                              float *node_max, int32_t *node_idx, int32_t *flag, int32_t *mtok, hipStream_t st);
+// selection, so no selection launch is needed.  bf16 layers: inv given
+// (gram_norms), the Gram launch writes the token norms; pack given, it clears
+// pack[0, n_pack); wo / wo16 given, it converts wo to fp16.
+hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, char *ws, float *node_max,
+                              int32_t *node_idx, int32_t *flag, int32_t *mtok, float *inv,
+                              unsigned long long *pack, long n_pack, const void *wo, void *wo16, hipStream_t st);
 hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_max, const int32_t *node_idx,
                          int32_t *flag, int32_t *mtok, hipStream_t st);
 // selection straight from node_pack; node_max / node_idx are written as
