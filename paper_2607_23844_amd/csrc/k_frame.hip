@@ -66,21 +66,35 @@ __global__ __launch_bounds__(256) void k_frame_gram(const uint16_t *__restrict__
     const int csteps = C / 64;   // steps per token (norms)
     int left = csteps;
     float ss0 = 0.f, ss1 = 0.f;
+    // this lane's 16-byte chunks of one 64-wide step (zero past the range)
+    auto load = [&](long k, uint4 *v0, uint4 *v1) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const long kk = k + g * 16 + t * 8;
+            v0[t] = make_uint4(0, 0, 0, 0);
+            v1[t] = make_uint4(0, 0, 0, 0);
+            if (kk < k_end) {
+                if (row0) v0[t] = *reinterpret_cast<const uint4 *>(row0 + kk);
+                if (TWO && row1) v1[t] = *reinterpret_cast<const uint4 *>(row1 + kk);
+            }
+        }
+    };
+    // one step of loads ahead: step k+64 is in flight while step k is used
+    uint4 nx0[2], nx1[2];
+    if (k_begin < k_end) load(k_begin, nx0, nx1);
     for (long k = k_begin; k < k_end; k += 64) {
         bf16x8 a0[2], a1[2];
         uint4 r0[2], r1[2];
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-            const long kk = k + g * 16 + t * 8;
-            uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
-            if (kk < k_end) {
-                if (row0) v0 = *reinterpret_cast<const uint4 *>(row0 + kk);
-                if (TWO && row1) v1 = *reinterpret_cast<const uint4 *>(row1 + kk);
-            }
-            r0[t] = v0;
-            r1[t] = v1;
-            a0[t] = *reinterpret_cast<bf16x8 *>(&v0);
-            a1[t] = *reinterpret_cast<bf16x8 *>(&v1);
+            r0[t] = nx0[t];
+            r1[t] = nx1[t];
+        }
+        if (k + 64 < k_end) load(k + 64, nx0, nx1);
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            a0[t] = *reinterpret_cast<bf16x8 *>(&r0[t]);
+            a1[t] = *reinterpret_cast<bf16x8 *>(&r1[t]);
         }
         if (inv != nullptr) {
 #pragma unroll
