@@ -205,22 +205,28 @@ __global__ __launch_bounds__(256) void k_match_mfma(const uint16_t *__restrict__
 // its candidates again, from L2) through one continuous double-buffered
 // LDS-DMA pipeline (small enough for two blocks per CU), keeps each
 // candidate's best (value, position) in registers and publishes it once (one
-// 64-bit atomic maximum per candidate; no other block touches it).  The
-// group's representative norms are staged in LDS first (D <= SWEEP_MAX_D).
+// 64-bit atomic maximum per candidate).  The representative tiles of one
+// candidate tile are split over n_part consecutive blocks (adjacent logical
+// blocks run on one XCD at the same time, so they share the candidate rows
+// in its L2 instead of each block re-reading its own tile from memory for
+// every representative tile); their atomics merge the parts.  The group's
+// representative norms are staged in LDS first (D <= SWEEP_MAX_D).
 template <int BA, int BB, int WA, int WB>
 __global__ __launch_bounds__(256) void k_match_sweep(const uint16_t *__restrict__ x, const float *__restrict__ inv,
                                                       GroupMap gm, int G, int S, int D, int K, int seg_len,
                                                       long sub_stride, long item_stride, int n_bt, int n_at,
-                                                      unsigned long long *__restrict__ node_pack) {
+                                                      int n_part, unsigned long long *__restrict__ node_pack) {
     using T = DmaTile<BA, BB, WA, WB, false, 2>;
     extern __shared__ __align__(16) uint16_t lds[];
     float *const snorm = reinterpret_cast<float *>(lds + T::LDS_BYTES / 2);   // n_at * BA norms after the ring
     __shared__ float sv[WA * BB];
     __shared__ int si[WA * BB];
-    const int lid = xcd_remap(blockIdx.x, n_bt * G);
-    const int bt = lid % n_bt, g = lid / n_bt;
+    const int lid = xcd_remap(blockIdx.x, n_bt * G * n_part);
+    const int part = lid % n_part, tl = lid / n_part;
+    const int bt = tl % n_bt, g = tl / n_bt;
+    const int u0 = part * n_at / n_part, u1 = (part + 1) * n_at / n_part;   // this block's representative tiles
     const GroupMap::Grp gr = gm.group(g);
-    if (bt * BB >= gr.nsrc) return;
+    if (bt * BB >= gr.nsrc || u0 >= u1) return;
     for (int a = threadIdx.x; a < n_at * BA; a += 256) {
         const int id = a < D ? gm.dst_id(gr, a) : -1;
         snorm[a] = id >= 0 ? inv[id] : -1.f;
@@ -244,7 +250,7 @@ __global__ __launch_bounds__(256) void k_match_sweep(const uint16_t *__restrict_
     }
     T tile;
     auto rows_a = [&](int u, int i) -> const uint16_t * {
-        const int a = u * BA + T::chunk_row(i);
+        const int a = (u0 + u) * BA + T::chunk_row(i);
         const int id = a < D ? gm.dst_id(gr, a) : -1;
         return id >= 0 ? x + (long)id * item_stride : nullptr;
     };
@@ -254,7 +260,8 @@ __global__ __launch_bounds__(256) void k_match_sweep(const uint16_t *__restrict_
     // equal value never replaces an earlier one); the lane halves are merged
     // once at the end
     const int d_full = D - BA;   // tiles starting at or below this have only valid representatives
-    auto epi = [&](int u) {
+    auto epi = [&](int ul) {
+        const int u = u0 + ul;
         const bool full = u * BA <= d_full && gm.dst_id(gr, u * BA + BA - 1) >= 0;
 #pragma unroll
         for (int j = 0; j < T::TB; ++j)
@@ -286,7 +293,7 @@ __global__ __launch_bounds__(256) void k_match_sweep(const uint16_t *__restrict_
                 }
             }
     };
-    tile.run_tiles(lds, rows_a, rowsB, x, x, K, seg_len, sub_stride, n_at, epi);
+    tile.run_tiles(lds, rows_a, rowsB, x, x, K, seg_len, sub_stride, u1 - u0, epi);
 #pragma unroll
     for (int j = 0; j < T::TB; ++j) argmax_merge(bv[j], bi[j], __shfl_xor(bv[j], 32, WAVE), __shfl_xor(bi[j], 32, WAVE));
     if (lane < 32) {
@@ -480,8 +487,13 @@ static hipError_t go_sweep(const Plan &p, const uint16_t *x, const float *inv, c
     static bool attr = false;
     hipError_t e = allow_lds(k_match_sweep<BA, BB, WA, WB>, lds, attr);
     if (e != hipSuccess) return e;
-    launch_k(k_match_sweep<BA, BB, WA, WB>, n_bt * G, 256, lds, st, x, inv, gm, G, S, D, K, seg_len,
-             sub_stride, item_stride, n_bt, n_at, node_pack);
+    // two blocks per candidate tile once each keeps three or more
+    // representative tiles (SVD-XT-like frames: 8x less memory traffic than
+    // one block, 203 against 1627 MiB per launch, at the same time; three or
+    // six parts measured no faster)
+    const int n_part = n_at >= 6 ? 2 : 1;
+    launch_k(k_match_sweep<BA, BB, WA, WB>, n_bt * G * n_part, 256, lds, st, x, inv, gm, G, S, D, K, seg_len,
+             sub_stride, item_stride, n_bt, n_at, n_part, node_pack);
     return hipGetLastError();
 }
 
