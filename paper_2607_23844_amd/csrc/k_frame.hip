@@ -200,13 +200,20 @@ __global__ __launch_bounds__(256) void k_frame_reduce(const float *__restrict__ 
 // similarity first, smallest frame on ties), and then either the Frame Cache
 // flags (flag / mtok per frame, when given) or, in pairing mode, the greedy
 // one-to-one pairing in selection order (a wave arg-max over the free even
-// frames per step) and the attention-unit table.  One block, F <= 32.
+// frames per step) and the attention-unit table.  One block, F <= 32.  With
+// kept_idx given (Frame Cache) the block also compacts: retained frames in
+// ascending order become rows [k*N, k*N+N) (k = the frame's rank among the
+// retained ones, at most n_seq), cached frames fill cached_idx in ascending
+// order, and rmap maps every token to its row (-1 cached, -2 past n_seq).
 __global__ __launch_bounds__(1024) void k_frame_final(const double *__restrict__ gram, int F, int R_f,
                                                       int pairing, double *__restrict__ fsim,
                                                       float *__restrict__ node_max, int32_t *__restrict__ node_idx,
                                                       int32_t *__restrict__ forder, int32_t *__restrict__ pairs,
                                                       int32_t *__restrict__ units, int32_t *__restrict__ flag,
-                                                      int32_t *__restrict__ mtok) {
+                                                      int32_t *__restrict__ mtok, int N, int n_seq,
+                                                      int32_t *__restrict__ kept_idx, int32_t *__restrict__ cached_idx,
+                                                      int32_t *__restrict__ rmap) {
+    __shared__ int fcached[FMAX], frank[FMAX];
     __shared__ double G[FMAX * FMAX];
     __shared__ double cs[FMAX * FMAX];
     __shared__ double bm[FMAX / 2];
@@ -268,6 +275,30 @@ __global__ __launch_bounds__(1024) void k_frame_final(const double *__restrict__
         }
         flag[t] = c ? 1 : 0;
         mtok[t] = m;
+        fcached[t] = c ? 1 : 0;
+    }
+    if (flag != nullptr && kept_idx != nullptr) {
+        __syncthreads();
+        if (t == 0) {
+            // rank of each frame among the retained, or among the cached, frames
+            int k = 0, c = 0;
+            for (int f = 0; f < F; ++f) frank[f] = fcached[f] ? c++ : k++;
+        }
+        __syncthreads();
+        const int n_cf = F - n_seq;
+        const long total = (long)F * N;
+        for (long q = t; q < total; q += blockDim.x) {
+            const int f = (int)(q / N), n = (int)(q - (long)f * N);
+            const int r = frank[f];
+            if (fcached[f]) {
+                if (r < n_cf) cached_idx[(long)r * N + n] = (int)q;
+                rmap[q] = -1;
+            } else {
+                const bool ok = r < n_seq;
+                if (ok) kept_idx[(long)r * N + n] = (int)q;
+                rmap[q] = ok ? r * N + n : -2;
+            }
+        }
     }
     if (!pairing) return;
     __syncthreads();
@@ -312,7 +343,9 @@ __global__ __launch_bounds__(1024) void k_frame_final(const double *__restrict__
 
 hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, char *ws, float *node_max,
                               int32_t *node_idx, int32_t *flag, int32_t *mtok, float *inv,
-                              unsigned long long *pack, long n_pack, const void *wo, void *wo16, hipStream_t st) {
+                              unsigned long long *pack, long n_pack, const void *wo, void *wo16, int32_t *kept_idx,
+                              int32_t *cached_idx, int32_t *rmap, hipStream_t st) {
+    if (kept_idx != nullptr && (flag == nullptr || cached_idx == nullptr || rmap == nullptr)) return hipErrorInvalidValue;
     const long D = (long)p.N * p.C;
     int nb = gram_blocks(p);
     float *part = (float *)(ws + L.gram_part);
@@ -347,7 +380,7 @@ hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, cha
         StageScope _stage(st, "frame_final");
         launch_k(k_frame_final, 1, 1024, 0, st, (const double *)gram, p.F, p.R_f, p.gran == 3 ? 1 : 0,
                  (double *)(ws + L.fsim), node_max, node_idx, (int32_t *)(ws + L.forder), (int32_t *)(ws + L.pairs),
-                 (int32_t *)(ws + L.units), flag, mtok);
+                 (int32_t *)(ws + L.units), flag, mtok, p.N, p.n_seq, kept_idx, cached_idx, rmap);
     }
     return hipGetLastError();
 }

@@ -238,7 +238,8 @@ const int32_t *units_of(const Plan &p, const Layout &L, void *ws) {
 // and norms in ws; wo / wo16, when given (bf16), are converted in the first
 // launch that reads x (the frame Gram, else the norms).
 oc_status run_match(const Plan &p, const Layout &L, const void *x, float *node_max, int32_t *node_idx, bool reduce,
-                    void *ws, hipStream_t st, const void *wo = nullptr, void *wo16 = nullptr) {
+                    void *ws, hipStream_t st, const void *wo = nullptr, void *wo16 = nullptr,
+                    bool frame_compact = false) {
     char *w = (char *)ws;
     const bool frames = p.gran == OC_GRAN_FRAME || p.gran == OC_GRAN_FRAME_TOKEN;
     unsigned long long *pack = at<unsigned long long>(ws, L.node_pack);
@@ -251,10 +252,15 @@ oc_status run_match(const Plan &p, const Layout &L, const void *x, float *node_m
         // Frame Cache: the frame stage also writes the per-frame selection
         const bool fsel = p.gran == OC_GRAN_FRAME;
         const bool cvt = p.bf16 && (fsel || gram_prep);
+        // (a layer call's Frame Cache: the compaction as well)
+        const bool fcomp = fsel && frame_compact;
         HIP_TRY(launch_frame_stage(p, L, x, w, fm, fi, fsel ? at<int32_t>(ws, L.flag) : nullptr,
                                    fsel ? at<int32_t>(ws, L.mtok) : nullptr,
                                    gram_prep ? at<float>(ws, L.inv) : nullptr, gram_prep ? pack : nullptr, n_pack,
-                                   cvt ? wo : nullptr, cvt ? wo16 : nullptr, st),
+                                   cvt ? wo : nullptr, cvt ? wo16 : nullptr,
+                                   fcomp ? at<int32_t>(ws, L.kept) : nullptr,
+                                   fcomp ? at<int32_t>(ws, L.cached) : nullptr,
+                                   fcomp ? at<int32_t>(ws, L.rmap) : nullptr, st),
                 "frame stage");
     }
     if (p.kind == KIND_FRAME) return OC_OK;
@@ -287,9 +293,15 @@ oc_status run_select(const Plan &p, const Layout &L, float *node_max, int32_t *n
             return OC_OK;
         }
     } else if (!(from_pack && p.kind == KIND_FRAME)) {
-        // (Frame Cache in a layer call: the frame stage wrote the selection)
         HIP_TRY(launch_select(p, units, node_max, node_idx, at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok), st),
                 "select");
+    } else {
+        // Frame Cache in a layer call: the frame stage wrote the selection
+        // and the compaction
+        if (map_matched)
+            HIP_TRY(launch_map_matched(p, at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok), rmap, st),
+                    "map matched");
+        return OC_OK;
     }
     HIP_TRY(launch_compact(p, at<int32_t>(ws, L.units), at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok),
                            at<int32_t>(ws, L.fcnt), kept, cached, rmap, map_matched, st),
@@ -484,7 +496,7 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
     // bf16 layers: the fp16 copy of wo is made by the first launch of the match stage
     const bool wo_early = p.bf16;
     if ((s = run_match(p, L, x, nm, ni, false, ws, stream, wo_early ? w->wo : nullptr,
-                       wo_early ? at<char>(ws, aw.wo16) : nullptr)) != OC_OK)
+                       wo_early ? at<char>(ws, aw.wo16) : nullptr, true)) != OC_OK)
         return s;
     int32_t *kept = at<int32_t>(ws, L.kept), *cached = at<int32_t>(ws, L.cached), *rmap = at<int32_t>(ws, L.rmap);
     if ((s = run_select(p, L, nm, ni, true, kept, cached, rmap, map_matched, ws, stream)) != OC_OK) return s;

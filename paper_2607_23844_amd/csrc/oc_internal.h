@@ -107,12 +107,14 @@ hipError_t launch_match(const Plan &p, const void *x, const float *inv, const in
                         unsigned long long *node_pack, float *part, float *node_max, int32_t *node_idx,
                         hipStream_t st);
 // flag / mtok given (Frame Cache): the frame stage also writes the per-frame
-// selection, so no selection launch is needed.  bf16 layers: inv given
+// selection, so no selection launch is needed, and with kept_idx /
+// cached_idx / rmap given also the compaction.  bf16 layers: inv given
 // (gram_norms), the Gram launch writes the token norms; pack given, it clears
 // pack[0, n_pack); wo / wo16 given, it converts wo to fp16.
 hipError_t launch_frame_stage(const Plan &p, const Layout &L, const void *x, char *ws, float *node_max,
                               int32_t *node_idx, int32_t *flag, int32_t *mtok, float *inv,
-                              unsigned long long *pack, long n_pack, const void *wo, void *wo16, hipStream_t st);
+                              unsigned long long *pack, long n_pack, const void *wo, void *wo16, int32_t *kept_idx,
+                              int32_t *cached_idx, int32_t *rmap, hipStream_t st);
 hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_max, const int32_t *node_idx,
                          int32_t *flag, int32_t *mtok, hipStream_t st);
 // selection straight from node_pack; node_max / node_idx are written as
