@@ -45,8 +45,7 @@ namespace oc {
 
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
-constexpr float REBASE = 8.f;
-constexpr int FLASH_CUS = 256;   // compute units of the MI355X   // P = exp2(s - m) stays below 2^REBASE on the fast path
+constexpr float REBASE = 8.f;   // P = exp2(s - m) stays below 2^REBASE on the fast path
 
 template <int DH, bool DMA>
 struct FlashCfg {
@@ -557,7 +556,7 @@ static hipError_t go_dh(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st
             // a grid of four-wave blocks that would not fill two per CU:
             // eight-wave blocks (256 queries share each K/V tile)
             const long blocks4 = (long)cdiv(Lk, 128) * p.heads * a.n_seq;
-            if (blocks4 <= 2L * FLASH_CUS) return go<DH, 8, true>(p, a, Lk, st);
+            if (blocks4 <= 2L * N_CUS) return go<DH, 8, true>(p, a, Lk, st);
             return go<DH, 4, true>(p, a, Lk, st);
         }
     }

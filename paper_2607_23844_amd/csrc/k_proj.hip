@@ -112,22 +112,36 @@ static hipError_t allow_lds(KernelPtr k, size_t bytes, bool &done) {
 // zeroed separately.  The DMA engine runs double-buffered (two blocks per
 // CU).
 // ---------------------------------------------------------------------------
-template <bool DMA>
-using QKVTile = typename std::conditional<DMA, DmaTile<128, 128, 2, 2, false, 2>, MfmaTile<128, 128, 2, 2>>::type;
+// Tile shapes: 128 x 128, or with WIDE 192 x 128 (192 rows of the A side:
+// weight rows in the row tiles, batch rows in the V tiles; 80 KB of LDS,
+// still two blocks per CU) where that needs fewer block rounds for the work.
+template <bool DMA, bool WIDE>
+struct QKVShape {
+    static constexpr int BA = 128, BB = 128;
+    using Tile = MfmaTile<128, 128, 2, 2>;
+};
+template <bool WIDE>
+struct QKVShape<true, WIDE> {
+    static constexpr int BA = WIDE ? 192 : 128, BB = 128;
+    using Tile = DmaTile<BA, BB, 2, 2, false, 2>;
+};
+template <bool DMA, bool WIDE = false>
+using QKVTile = typename QKVShape<DMA, WIDE>::Tile;
 
-template <bool DMA>
+template <bool DMA, bool WIDE>
 __global__ __launch_bounds__(256) void k_proj_qkv(RowMap rm, const uint16_t *__restrict__ wq,
                                                   const uint16_t *__restrict__ wk, const uint16_t *__restrict__ wv,
-                                                  int hd, int dh, float qscale, int nw, int n_qk_at, int n_v_bt, int n_bt,
-                                                  int n_seq, int L, int lpad, int zero_pad,
+                                                  int hd, int dh, float qscale, int nw, int n_qk_at, int n_bt,
+                                                  int n_v_at, int n_v_bt, int n_seq, int L, int lpad, int zero_pad,
                                                   uint16_t *__restrict__ Q, uint16_t *__restrict__ K,
                                                   uint16_t *__restrict__ Vt) {
-    using T = QKVTile<DMA>;
+    using T = QKVTile<DMA, WIDE>;
     using Rows = typename std::conditional<DMA, DmaRows, RegRows>::type;
-    constexpr int BA = 128, BB = 128;
+    constexpr int BA = QKVShape<DMA, WIDE>::BA, BB = QKVShape<DMA, WIDE>::BB;
+    static_assert((size_t)BB * (BA + 8) * 2 <= T::LDS_BYTES, "staged rows fit in the ring");
     extern __shared__ __align__(16) uint16_t lds[];
     const int n_qk = n_qk_at * n_bt;
-    const int total = n_qk + n_bt * n_v_bt;
+    const int total = n_qk + n_v_at * n_v_bt;
     const int lid = xcd_remap(blockIdx.x, total);
     const uint16_t *rowsA[T::CA], *rowsB[T::CB];
     T t;
@@ -160,7 +174,7 @@ __global__ __launch_bounds__(256) void k_proj_qkv(RowMap rm, const uint16_t *__r
     }
     // V tile: at over batch rows, bt over features
     int at, bt;
-    tile_order(lid - n_qk, n_bt, n_v_bt, at, bt);
+    tile_order(lid - n_qk, n_v_at, n_v_bt, at, bt);
 #pragma unroll
     for (int i = 0; i < T::CA; ++i) rowsA[i] = rm.row(at * BA + T::chunk_row(i));
 #pragma unroll
@@ -203,10 +217,10 @@ __global__ __launch_bounds__(256) void k_proj_qkv(RowMap rm, const uint16_t *__r
                 }
     }
     // zero the padded key positions [Lk, lpad) of this block's features, for
-    // the sequences s = at, at + n_bt, ... (the DMA-staged attention reads them)
+    // the sequences s = at, at + n_v_at, ... (the DMA-staged attention reads them)
     const int npad = lpad - Lk;
     if (zero_pad && npad > 0) {
-        for (int sq = at; sq < n_seq; sq += n_bt)
+        for (int sq = at; sq < n_seq; sq += n_v_at)
             for (int idx = threadIdx.x; idx < BB * npad; idx += blockDim.x) {
                 const int f = f0 + idx / npad, jj = Lk + idx % npad;
                 if (f >= hd) continue;
@@ -216,6 +230,27 @@ __global__ __launch_bounds__(256) void k_proj_qkv(RowMap rm, const uint16_t *__r
     }
 }
 
+// tiles of a BA x BB launch over rows
+static long qkv_tiles(const Plan &p, int rows, int nw, int BA, int BB) {
+    return (long)cdiv(nw * p.hd, BA) * cdiv(rows, BB) + (nw == 3 ? 0L : (long)cdiv(rows, BA) * cdiv(p.hd, BB));
+}
+
+template <bool DMA, bool WIDE>
+static hipError_t launch_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, float qscale, int nw, int zero_pad,
+                             hipStream_t st) {
+    constexpr int BA = QKVShape<DMA, WIDE>::BA, BB = QKVShape<DMA, WIDE>::BB;
+    static bool lds_ok = false;
+    const hipError_t e = allow_lds(k_proj_qkv<DMA, WIDE>, QKVTile<DMA, WIDE>::LDS_BYTES, lds_ok);
+    if (e != hipSuccess) return e;
+    const int n_qk_at = cdiv(nw * p.hd, BA), n_bt = cdiv(rm.n_rows, BB);
+    const int n_v_at = nw == 3 ? 0 : cdiv(rm.n_rows, BA), n_v_bt = nw == 3 ? 0 : cdiv(p.hd, BB);
+    const int total = n_qk_at * n_bt + n_v_at * n_v_bt;
+    launch_k(k_proj_qkv<DMA, WIDE>, total, 256, QKVTile<DMA, WIDE>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
+             (const uint16_t *)a.wk, (const uint16_t *)a.wv, p.hd, p.dh, qscale, nw, n_qk_at, n_bt, n_v_at, n_v_bt,
+             a.n_seq, a.L, a.lpad, zero_pad, (uint16_t *)a.q, (uint16_t *)a.k, (uint16_t *)a.vt);
+    return hipGetLastError();
+}
+
 hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, hipStream_t st) {
     const float qscale = (float)(1.4426950408889634 / sqrt((double)p.dh));
     StageScope _stage(st, "proj_qkv");
@@ -223,18 +258,19 @@ hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, h
     const int zero_pad = flash_uses_dma(p.dh, Lk, p.hd) ? 1 : 0;
     // short sequences: V rows from the Q/K tiles (nw = 3), no V tiles
     const int nw = attn_short(Lk) ? 3 : 2;
-    const int n_qk_at = cdiv(nw * p.hd, 128), n_v_bt = nw == 3 ? 0 : cdiv(p.hd, 128), n_bt = cdiv(rm.n_rows, 128);
-    const int total = n_qk_at * n_bt + n_bt * n_v_bt;
-    if (p.C % 64 == 0) {
-        launch_k(k_proj_qkv<true>, total, 256, QKVTile<true>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
-                 (const uint16_t *)a.wk, (const uint16_t *)a.wv, p.hd, p.dh, qscale, nw, n_qk_at, n_v_bt, n_bt, a.n_seq,
-                 a.L, a.lpad, zero_pad, (uint16_t *)a.q, (uint16_t *)a.k, (uint16_t *)a.vt);
-    } else {
-        launch_k(k_proj_qkv<false>, total, 256, QKVTile<false>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
-                 (const uint16_t *)a.wk, (const uint16_t *)a.wv, p.hd, p.dh, qscale, nw, n_qk_at, n_v_bt, n_bt, a.n_seq,
-                 a.L, a.lpad, zero_pad, (uint16_t *)a.q, (uint16_t *)a.k, (uint16_t *)a.vt);
-    }
-    return hipGetLastError();
+    if (p.C % 64 != 0) return launch_qkv<false, false>(p, rm, a, qscale, nw, zero_pad, st);
+    // block rounds (two blocks per CU) times the work of one tile: a 192 x 128
+    // tile is 1.5 units (the SD3-like layer at r = 0.5: 460 wide tiles in one
+    // round, 44 us, against 684 tiles in two, 51 us; one round either way, or
+    // two either way, keeps the smaller tiles).  Wide V tiles must stay whole
+    // runs of one sequence (else Vt is stored element by element: 58 against
+    // 42 us on the Latte-like spatial layer, 256-token sequences).
+    const long slots = 2L * N_CUS;
+    const long r128 = (qkv_tiles(p, rm.n_rows, nw, 128, 128) + slots - 1) / slots;
+    const long r192 = (qkv_tiles(p, rm.n_rows, nw, 192, 128) + slots - 1) / slots;
+    const bool v_rows = nw == 3 || a.n_seq == 1 || a.L % 192 == 0;
+    if (v_rows && 3 * r192 < 2 * r128) return launch_qkv<true, true>(p, rm, a, qscale, nw, zero_pad, st);
+    return launch_qkv<true, false>(p, rm, a, qscale, nw, zero_pad, st);
 }
 
 // ---------------------------------------------------------------------------

@@ -68,6 +68,9 @@ inline bool flash_uses_dma(int dh, int Lk, int hd) {
 // fp16) instead of as Vt.
 inline bool attn_short(int Lk) { return Lk <= 64; }
 
+// Compute units of the MI355X (launch shapes that count block rounds).
+constexpr int N_CUS = 256;
+
 // Q/K/V projection and attention fused for short sequences of head dim 64
 // (k_short.hip); O is then projected by launch_proj_out.
 bool qkv_attn_short_applies(const Plan &p, const AttnArgs &a);
