@@ -79,6 +79,12 @@ SMALL = [
     # context) are computed
     dict(gran="token", F=1, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r=0.99, n_ctx=3),
     dict(gran="block", F=4, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r=0.99),
+    # Block Cache over 4096 positions: 3072 candidates, selected and
+    # compacted by the 1024-thread selection block
+    dict(gran="block", F=2, H=64, W=64, C=64, heads=2, head_dim=32, dtype="bf16"),
+    # Frame Cache at its largest frame count (32), compacted by the frame
+    # stage's final block
+    dict(gran="frame", F=32, H=4, W=4, C=64, heads=2, head_dim=32, dtype="bf16", planted=True, r_frame=0.4),
 ]
 
 
