@@ -112,32 +112,34 @@ static hipError_t allow_lds(KernelPtr k, size_t bytes, bool &done) {
 // zeroed separately.  The DMA engine runs double-buffered (two blocks per
 // CU).
 // ---------------------------------------------------------------------------
-// Tile shapes: 128 x 128, or with WIDE 192 x 128 (192 rows of the A side:
-// weight rows in the row tiles, batch rows in the V tiles; 80 KB of LDS,
-// still two blocks per CU) where that needs fewer block rounds for the work.
-template <bool DMA, bool WIDE>
+// Tile shapes (SH): 0 = 128 x 128; 1 = 192 x 128 (192 rows of the A side:
+// weight rows in the row tiles, batch rows in the V tiles); 2 = 128 x 192
+// (192 of the B side: batch rows in the row tiles, rows of wv in the V
+// tiles).  The wide ones take 80 KB of LDS, still two blocks per CU, and run
+// where they need fewer block rounds for the work.
+template <bool DMA, int SH>
 struct QKVShape {
     static constexpr int BA = 128, BB = 128;
     using Tile = MfmaTile<128, 128, 2, 2>;
 };
-template <bool WIDE>
-struct QKVShape<true, WIDE> {
-    static constexpr int BA = WIDE ? 192 : 128, BB = 128;
+template <int SH>
+struct QKVShape<true, SH> {
+    static constexpr int BA = SH == 1 ? 192 : 128, BB = SH == 2 ? 192 : 128;
     using Tile = DmaTile<BA, BB, 2, 2, false, 2>;
 };
-template <bool DMA, bool WIDE = false>
-using QKVTile = typename QKVShape<DMA, WIDE>::Tile;
+template <bool DMA, int SH = 0>
+using QKVTile = typename QKVShape<DMA, SH>::Tile;
 
-template <bool DMA, bool WIDE>
+template <bool DMA, int SH>
 __global__ __launch_bounds__(256) void k_proj_qkv(RowMap rm, const uint16_t *__restrict__ wq,
                                                   const uint16_t *__restrict__ wk, const uint16_t *__restrict__ wv,
                                                   int hd, int dh, float qscale, int nw, int n_qk_at, int n_bt,
                                                   int n_v_at, int n_v_bt, int n_seq, int L, int lpad, int zero_pad,
                                                   uint16_t *__restrict__ Q, uint16_t *__restrict__ K,
                                                   uint16_t *__restrict__ Vt) {
-    using T = QKVTile<DMA, WIDE>;
+    using T = QKVTile<DMA, SH>;
     using Rows = typename std::conditional<DMA, DmaRows, RegRows>::type;
-    constexpr int BA = QKVShape<DMA, WIDE>::BA, BB = QKVShape<DMA, WIDE>::BB;
+    constexpr int BA = QKVShape<DMA, SH>::BA, BB = QKVShape<DMA, SH>::BB;
     static_assert((size_t)BB * (BA + 8) * 2 <= T::LDS_BYTES, "staged rows fit in the ring");
     extern __shared__ __align__(16) uint16_t lds[];
     const int n_qk = n_qk_at * n_bt;
@@ -235,17 +237,17 @@ static long qkv_tiles(const Plan &p, int rows, int nw, int BA, int BB) {
     return (long)cdiv(nw * p.hd, BA) * cdiv(rows, BB) + (nw == 3 ? 0L : (long)cdiv(rows, BA) * cdiv(p.hd, BB));
 }
 
-template <bool DMA, bool WIDE>
+template <bool DMA, int SH>
 static hipError_t launch_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, float qscale, int nw, int zero_pad,
                              hipStream_t st) {
-    constexpr int BA = QKVShape<DMA, WIDE>::BA, BB = QKVShape<DMA, WIDE>::BB;
+    constexpr int BA = QKVShape<DMA, SH>::BA, BB = QKVShape<DMA, SH>::BB;
     static bool lds_ok = false;
-    const hipError_t e = allow_lds(k_proj_qkv<DMA, WIDE>, QKVTile<DMA, WIDE>::LDS_BYTES, lds_ok);
+    const hipError_t e = allow_lds(k_proj_qkv<DMA, SH>, QKVTile<DMA, SH>::LDS_BYTES, lds_ok);
     if (e != hipSuccess) return e;
     const int n_qk_at = cdiv(nw * p.hd, BA), n_bt = cdiv(rm.n_rows, BB);
     const int n_v_at = nw == 3 ? 0 : cdiv(rm.n_rows, BA), n_v_bt = nw == 3 ? 0 : cdiv(p.hd, BB);
     const int total = n_qk_at * n_bt + n_v_at * n_v_bt;
-    launch_k(k_proj_qkv<DMA, WIDE>, total, 256, QKVTile<DMA, WIDE>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
+    launch_k(k_proj_qkv<DMA, SH>, total, 256, QKVTile<DMA, SH>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
              (const uint16_t *)a.wk, (const uint16_t *)a.wv, p.hd, p.dh, qscale, nw, n_qk_at, n_bt, n_v_at, n_v_bt,
              a.n_seq, a.L, a.lpad, zero_pad, (uint16_t *)a.q, (uint16_t *)a.k, (uint16_t *)a.vt);
     return hipGetLastError();
@@ -258,19 +260,22 @@ hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, h
     const int zero_pad = flash_uses_dma(p.dh, Lk, p.hd) ? 1 : 0;
     // short sequences: V rows from the Q/K tiles (nw = 3), no V tiles
     const int nw = attn_short(Lk) ? 3 : 2;
-    if (p.C % 64 != 0) return launch_qkv<false, false>(p, rm, a, qscale, nw, zero_pad, st);
-    // block rounds (two blocks per CU) times the work of one tile: a 192 x 128
-    // tile is 1.5 units (the SD3-like layer at r = 0.5: 460 wide tiles in one
-    // round, 44 us, against 684 tiles in two, 51 us; one round either way, or
-    // two either way, keeps the smaller tiles).  Wide V tiles must stay whole
-    // runs of one sequence (else Vt is stored element by element: 58 against
-    // 42 us on the Latte-like spatial layer, 256-token sequences).
+    if (p.C % 64 != 0) return launch_qkv<false, 0>(p, rm, a, qscale, nw, zero_pad, st);
+    // block rounds (two blocks per CU) times the work of one tile, a wide
+    // tile being 1.5 units (the SD3-like layer at r = 0.5: 460 tiles of 192 x
+    // 128 in one round, 44 us, against 684 of 128 x 128 in two, 51 us; one
+    // round either way, or two either way, keeps the smaller tiles).  192-row
+    // V tiles must stay whole runs of one sequence (else Vt is stored element
+    // by element: 58 against 42 us on the Latte-like spatial layer, 256-token
+    // sequences), which 128 x 192 keeps at 128 rows.
     const long slots = 2L * N_CUS;
-    const long r128 = (qkv_tiles(p, rm.n_rows, nw, 128, 128) + slots - 1) / slots;
-    const long r192 = (qkv_tiles(p, rm.n_rows, nw, 192, 128) + slots - 1) / slots;
-    const bool v_rows = nw == 3 || a.n_seq == 1 || a.L % 192 == 0;
-    if (v_rows && 3 * r192 < 2 * r128) return launch_qkv<true, true>(p, rm, a, qscale, nw, zero_pad, st);
-    return launch_qkv<true, false>(p, rm, a, qscale, nw, zero_pad, st);
+    const long c128 = 2 * ((qkv_tiles(p, rm.n_rows, nw, 128, 128) + slots - 1) / slots);
+    const long c192a = 3 * ((qkv_tiles(p, rm.n_rows, nw, 192, 128) + slots - 1) / slots);
+    const long c192b = 3 * ((qkv_tiles(p, rm.n_rows, nw, 128, 192) + slots - 1) / slots);
+    const bool rows192 = nw == 3 || a.n_seq == 1 || a.L % 192 == 0;
+    if (rows192 && c192a < c128 && c192a <= c192b) return launch_qkv<true, 1>(p, rm, a, qscale, nw, zero_pad, st);
+    if (c192b < c128) return launch_qkv<true, 2>(p, rm, a, qscale, nw, zero_pad, st);
+    return launch_qkv<true, 0>(p, rm, a, qscale, nw, zero_pad, st);
 }
 
 // ---------------------------------------------------------------------------
