@@ -542,6 +542,11 @@ hipError_t launch_match(const Plan &p, const void *x, const float *inv, const in
                 // many candidate tiles: each block sweeps all representative tiles
                 e = go_sweep<128, 128, 2, 2>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride, node_pack,
                                                    st);
+            } else if (D > 64 && dma && (long)cdiv(D, 128) * cdiv(S, 64) * G < 2L * N_CUS) {
+                // a 128 x 64 grid under two blocks per CU: 64 x 64 tiles, three
+                // to five per CU (the SD3-like layer: 768 blocks, 20 against 23 us)
+                e = go_match<64, 64, 2, 2, true>(p, xb, inv, gm, K, seg_len, sub_stride, item_stride, node_pack,
+                                                 st);
             } else if (D > 64) {
                 // representative tile height by group size: 128, 64 or 32; large
                 // groups stream by LDS DMA when the K steps allow it
