@@ -383,8 +383,20 @@ __global__ __launch_bounds__(256) void k_match_part_reduce(const float *__restri
     for (int a0 = 0; a0 < D; a0 += 64) {
         const int a = a0 + lane;
         float sum = 0.f;
-        if (a < D)
-            for (int sp = q; sp < n_split; sp += 4) sum += part[(((long)sp * G + g) * S + b) * D + a];
+        if (a < D) {
+            // splits q, q+4, ... added in ascending order; the loads of eight
+            // of them are issued before the first is added
+            const long stride = 4L * G * S * D;
+            const float *pp = part + (((long)q * G + g) * S + b) * D + a;
+            for (int sp0 = q; sp0 < n_split; sp0 += 32, pp += 8 * stride) {
+                float v[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) v[u] = sp0 + 4 * u < n_split ? pp[u * stride] : 0.f;
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (sp0 + 4 * u < n_split) sum += v[u];
+            }
+        }
         red[q][lane] = sum;
         __syncthreads();
         if (q == 0 && a < D) {
