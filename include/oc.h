@@ -22,9 +22,25 @@
  *    wq, wk, wv are [heads*head_dim, C] and wo is [C, heads*head_dim];
  *    q = x wq^T etc.  Same element type as x.
  *  - All device pointers are caller-owned device memory, 16-byte aligned.
- *    The library allocates no device memory, keeps no device state and no
- *    global mutable host state; scratch space is the caller's workspace of
- *    at least oc_plan_info.workspace_bytes.
+ *    The library allocates no device memory and keeps no device state;
+ *    scratch space is the caller's workspace of at least
+ *    oc_plan_info.workspace_bytes.  Its only shared host state is a
+ *    mutex-guarded record of the kernels whose dynamic-LDS limit it has
+ *    raised on each device (plus the thread-local error message and stage
+ *    timer), so concurrent calls from several threads are safe.
+ *  - Numeric range: inside the attention the projections q, k, v, the
+ *    probabilities and the per-head outputs are held in fp16 (11
+ *    significant bits, fp32 accumulation everywhere).  Two limits follow,
+ *    and neither is reported (the call returns OC_OK):
+ *      precision: a logit q.k/sqrt(head_dim) carries a relative error of
+ *      about 2^-11, so outputs stay within 1% of their RMS while the largest
+ *      |logit| of a sequence is below about 100; larger logits (e.g. input
+ *      channels 50x or more above the rest, with no normalisation before
+ *      the layer) make the softmax ill-conditioned at 16-bit q and k, and
+ *      the error grows with the logits (measured 1.7% of RMS at 2e2, 12-19%
+ *      at 8e4 for 256-token sequences);
+ *      range: q, k, v or per-head outputs beyond 65504 in magnitude are
+ *      saturated to +-65504.
  *  - All work is enqueued on the caller's stream; calls are asynchronous.
  *    Results are deterministic: the same inputs give bit-identical outputs.
  *  - Every function validates its arguments on the host first.  On any
@@ -136,7 +152,12 @@ typedef struct {
 
 /*
  * oc_plan — host only, no device work.  Validates shape and cfg and returns
- * the static sizes of one call (they depend only on shape and cfg).
+ * the static sizes of one call (they depend only on shape and cfg): the
+ * matching groups of each cache (§3.2.1 2x2 block groups, §3.2.2 the
+ * alternating odd / even frame sets, §3.2.3 2x2 token neighbourhoods and
+ * 2x2x2 cubes of frame pairs, all inside k x k patches per §3.3), the
+ * skip budgets that the ratios r_b, r_f and r_t of §3.2 give each group,
+ * and the reduced attention batch.
  * Requirements (OC_ERR_SHAPE otherwise): F, H, W, C, heads, head_dim >= 1;
  * H and W divisible by 2*patch_k; C % 8 == 0; head_dim % 8 == 0 and
  * head_dim <= 128; F >= 2 for FRAME and FRAME_TOKEN; patch_k == 1 for
@@ -234,10 +255,14 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
                           oc_trace *trace, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
- * oc_attn_full — the uncached layer on the same input: spatial attention
- * per frame over all N tokens (+ context) for TOKEN/FRAME/FRAME_TOKEN, or
- * temporal attention per position over all F frames for BLOCK.  y is
- * [F, N, C]; ws_bytes >= oc_plan_info.workspace_bytes.
+ * oc_attn_full — the uncached baseline: the layer as it runs without any
+ * cache, i.e. the computation every cache of §3.2 skips part of (the
+ * denominator of a cached layer's speed-up).  Spatial attention per frame
+ * over all N tokens (+ context) for TOKEN/FRAME/FRAME_TOKEN, or temporal
+ * attention per position over all F frames for BLOCK (§3.2.1: the temporal
+ * layer's H*W sequences of length T).  Same kernels and numerics as the
+ * reduced attention.  y is [F, N, C]; ws_bytes >=
+ * oc_plan_info.workspace_bytes.  Errors as for oc_layer_cached.
  */
 oc_status oc_attn_full(const oc_shape *shape, const oc_cfg *cfg, const void *x, const void *ctx,
                        const oc_attn_weights *w, void *y, void *y_ctx,

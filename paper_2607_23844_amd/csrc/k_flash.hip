@@ -532,13 +532,8 @@ static hipError_t go(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
     const int n_qt = cdiv(Lk, 32 * NW);
     const int total = n_qt * p.heads * a.n_seq;
     const size_t lds = FlashCfg<DH, DMA>::LDS_BYTES;
-    static bool attr = false;   // one attribute call per instantiation (idempotent)
-    if (!attr) {
-        const hipError_t e = hipFuncSetAttribute((const void *)k_flash<DH, NW, DMA>,
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        attr = true;
-    }
+    const hipError_t e = raise_lds_limit((const void *)k_flash<DH, NW, DMA>, lds);
+    if (e != hipSuccess) return e;
     launch_k(k_flash<DH, NW, DMA>, total, NW * 64, lds, st, (const uint16_t *)a.q, (const uint16_t *)a.k,
                                                       (const uint16_t *)a.vt, (uint16_t *)a.o, p.hd, p.heads,
                                                       a.n_seq, a.L, Lk, a.lpad, n_qt);

@@ -464,11 +464,8 @@ __global__ void k_match_unpack(const unsigned long long *__restrict__ node_pack,
 }
 
 template <typename KernelPtr>
-static hipError_t allow_lds(KernelPtr k, size_t lds, bool &done) {
-    if (done || lds <= 65536) return hipSuccess;
-    const hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e == hipSuccess) done = true;
-    return e;
+static hipError_t allow_lds(KernelPtr k, size_t lds) {
+    return raise_lds_limit((const void *)k, lds);
 }
 
 template <int BA, int BB, int WA, int WB, bool DMA>
@@ -479,8 +476,7 @@ static hipError_t go_match(const Plan &p, const uint16_t *x, const float *inv, c
     const int G = p.n_groups, S = p.n_src_max, D = p.n_dst_max;
     const int n_bt = cdiv(S, BB), n_at = cdiv(D, BA);
     const size_t lds = T::LDS_BYTES;
-    static bool attr = false;
-    hipError_t e = allow_lds(k_match_mfma<BA, BB, WA, WB, DMA>, lds, attr);
+    hipError_t e = allow_lds(k_match_mfma<BA, BB, WA, WB, DMA>, lds);
     if (e != hipSuccess) return e;
     launch_k(k_match_mfma<BA, BB, WA, WB, DMA>, n_bt * n_at * G, 256, lds, st, x, inv, gm, G, S, D, K, seg_len,
              sub_stride, item_stride, n_bt, n_at, node_pack);
@@ -496,8 +492,7 @@ static hipError_t go_sweep(const Plan &p, const uint16_t *x, const float *inv, c
     const int n_bt = cdiv(S, BB), n_at = cdiv(D, BA);
     if (n_at * BA > SWEEP_MAX_D) return hipErrorInvalidValue;
     const size_t lds = T::LDS_BYTES + (size_t)n_at * BA * 4;
-    static bool attr = false;
-    hipError_t e = allow_lds(k_match_sweep<BA, BB, WA, WB>, lds, attr);
+    hipError_t e = allow_lds(k_match_sweep<BA, BB, WA, WB>, lds);
     if (e != hipSuccess) return e;
     // two blocks per candidate tile once each keeps three or more
     // representative tiles (SVD-XT-like frames: 8x less memory traffic than
@@ -517,8 +512,7 @@ static hipError_t go_split(const Plan &p, const MatchSplit &ms, const uint16_t *
     const int G = p.n_groups, S = p.n_src_max, D = p.n_dst_max;
     const int n_bt = cdiv(S, BB), n_at = cdiv(D, BA);
     const size_t lds = T::LDS_BYTES;
-    static bool attr = false;
-    hipError_t e = allow_lds(k_match_part<BA, BB, WA, WB, DMA>, lds, attr);
+    hipError_t e = allow_lds(k_match_part<BA, BB, WA, WB, DMA>, lds);
     if (e != hipSuccess) return e;
     launch_k(k_match_part<BA, BB, WA, WB, DMA>, n_bt * n_at * G * ms.n_split, 256, lds, st, x, gm, G, S, D, ms.kc,
              seg_len, sub_stride, item_stride, n_bt, n_at, ms.n_split, part);

@@ -90,11 +90,8 @@ __device__ __forceinline__ void run_tile(T &t, uint16_t *lds, const uint16_t *co
 }
 
 template <typename KernelPtr>
-static hipError_t allow_lds(KernelPtr k, size_t bytes, bool &done) {
-    if (done || bytes <= 65536) return hipSuccess;
-    const hipError_t e = hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-    if (e == hipSuccess) done = true;
-    return e;
+static hipError_t allow_lds(KernelPtr k, size_t bytes) {
+    return raise_lds_limit((const void *)k, bytes);
 }
 
 // ---------------------------------------------------------------------------
@@ -241,8 +238,7 @@ template <bool DMA, int SH>
 static hipError_t launch_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, float qscale, int nw, int zero_pad,
                              hipStream_t st) {
     constexpr int BA = QKVShape<DMA, SH>::BA, BB = QKVShape<DMA, SH>::BB;
-    static bool lds_ok = false;
-    const hipError_t e = allow_lds(k_proj_qkv<DMA, SH>, QKVTile<DMA, SH>::LDS_BYTES, lds_ok);
+    const hipError_t e = allow_lds(k_proj_qkv<DMA, SH>, QKVTile<DMA, SH>::LDS_BYTES);
     if (e != hipSuccess) return e;
     const int n_qk_at = cdiv(nw * p.hd, BA), n_bt = cdiv(rm.n_rows, BB);
     const int n_v_at = nw == 3 ? 0 : cdiv(rm.n_rows, BA), n_v_bt = nw == 3 ? 0 : cdiv(p.hd, BB);
@@ -348,13 +344,11 @@ hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStre
     };
     if (p.hd % 64 == 0) {
         if (p.C % 160 == 0 && p.C % 128 != 0) {
-            static bool attr = false;
-            hipError_t e = allow_lds(k_proj_out<true, 160>, OTile<true, 160>::LDS_BYTES, attr);
+            hipError_t e = allow_lds(k_proj_out<true, 160>, OTile<true, 160>::LDS_BYTES);
             if (e != hipSuccess) return e;
             go(k_proj_out<true, 160>, OTile<true, 160>::LDS_BYTES, 160, 128);
         } else {
-            static bool attr = false;
-            hipError_t e = allow_lds(k_proj_out<true, 128>, OTile<true, 128>::LDS_BYTES, attr);
+            hipError_t e = allow_lds(k_proj_out<true, 128>, OTile<true, 128>::LDS_BYTES);
             if (e != hipSuccess) return e;
             go(k_proj_out<true, 128>, OTile<true, 128>::LDS_BYTES, 128, 64);
         }

@@ -184,14 +184,8 @@ hipError_t launch_qkv_attn_short(const Plan &p, const RowMap &rm, const AttnArgs
     const int s_t = 128 / a.L;
     const int n_tiles = cdiv(a.n_seq, s_t);
     const float qscale = (float)(1.4426950408889634 / sqrt((double)p.dh));
-    static bool attr = false;
-    if (!attr) {
-        const hipError_t e = hipFuncSetAttribute((const void *)k_qkv_attn_short,
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                 (int)ShortTile::LDS_BYTES);
-        if (e != hipSuccess) return e;
-        attr = true;
-    }
+    const hipError_t e = raise_lds_limit((const void *)k_qkv_attn_short, ShortTile::LDS_BYTES);
+    if (e != hipSuccess) return e;
     launch_k(k_qkv_attn_short, (unsigned)(n_tiles * p.heads), 256, ShortTile::LDS_BYTES, st, rm,
              (const uint16_t *)a.wq, (const uint16_t *)a.wk, (const uint16_t *)a.wv, p.hd, p.heads, a.n_seq, a.L,
              s_t, n_tiles, qscale, (uint16_t *)a.o);

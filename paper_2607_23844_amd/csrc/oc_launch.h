@@ -13,6 +13,10 @@ namespace oc {
 // An event pair for the next launch on st when a stage is being timed.
 bool timed_launch_events(hipStream_t st, hipEvent_t *start, hipEvent_t *stop);
 
+// Allows `kernel` `bytes` of dynamic LDS on the current device (a no-op up to
+// 64 KB; once per kernel and device above, thread-safe).
+hipError_t raise_lds_limit(const void *kernel, size_t bytes);
+
 template <typename... KArgs, typename... Args>
 inline void launch_k(void (*k)(KArgs...), dim3 grid, dim3 block, size_t lds, hipStream_t st, Args... args) {
     hipEvent_t a = nullptr, b = nullptr;

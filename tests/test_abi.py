@@ -231,3 +231,38 @@ def test_workspace_covers_cold_full_steps():
         need = oc.plan(shape, cfg).workspace_bytes
         full = oc.plan(shape, oc.Cfg(cfg.gran, 0.0, 0.0, cfg.patch_k)).workspace_bytes
         assert need >= full, name
+
+
+def test_plan_and_errors_from_many_threads():
+    """Host entry points called concurrently from several threads: every
+    thread gets the same plan for the same arguments, and each thread's
+    oc_last_error() holds the message of its own last failure (the error
+    text is thread-local; the library's shared host state is guarded)."""
+    import threading
+    lib = L.lib()
+    good_cf = oc.Cfg("token", r=0.5)
+    ref = oc.plan(GOOD, good_cf)
+    bad = oc.Shape(1, 8, 8, 30, 2, 16, 0, "bf16")           # C not a multiple of 8
+    errors, results = [], []
+
+    def worker(i):
+        try:
+            for it in range(200):
+                if (i + it) % 2:
+                    info = oc.plan(GOOD, good_cf)
+                    results.append(info == ref)
+                else:
+                    sh, cf, info = bad.c(), good_cf.c(), L.oc_plan_info()
+                    st = lib.oc_plan(C.byref(sh), C.byref(cf), C.byref(info))
+                    msg = lib.oc_last_error().decode()
+                    results.append(st == L.OC_ERR_SHAPE and "C=30" in msg)
+        except Exception as e:   # pragma: no cover - reported below
+            errors.append(repr(e))
+
+    th = [threading.Thread(target=worker, args=(i,)) for i in range(8)]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    assert not errors, errors
+    assert len(results) == 8 * 200 and all(results)

@@ -15,8 +15,8 @@ from oc_synth import make_workload, small_workload
 from oracle import oc_oracle as O
 import paper_2607_23844_amd as oc
 
-from parity import (TOL, dev_tensor, layer_step_parity, layer_step_sampled_parity, rel_err, shapes, to_f64,
-                    weights_dev, weights_f64, check_match, group_margins)
+from parity import (TOL, RAW_TOL, check_output_bars, dev_tensor, layer_step_parity, layer_step_sampled_parity,
+                    rel_err, shapes, to_f64, weights_dev, weights_f64, check_match, group_margins)
 
 pytestmark = pytest.mark.gpu
 
@@ -98,6 +98,35 @@ def test_small_layer_chain(case, cold):
     chain(wl, 3, cold=cold)
 
 
+@pytest.mark.parametrize("scale", [10, 30])
+@pytest.mark.parametrize("gran,head_dim,F", [("token", 64, 1), ("block", 72, 8)])
+def test_heavy_tailed_activations_chain(gran, head_dim, F, scale):
+    """Activations with three outlier channels scaled by 10 or 30 over the
+    rest (heavy-tailed channels of transformer activations): both output
+    bars still hold with fp16 attention intermediates.  The limit is the
+    attention logits, not fp16's range: a logit carries a relative error of
+    about 2^-11 from the fp16 q and k, so the bars hold while the largest
+    |q.k|/sqrt(head_dim) stays below about 100 (82 at scale 30 here); at
+    scale 50 and beyond (logits of 2e2-1e5) the error grows past the bars,
+    which the library's header states as its supported range."""
+    from oc_synth import bf16_bits
+    wl = small_workload(gran, F=F, H=16, W=16, C=256, heads=4, head_dim=head_dim, dtype="bf16", r=0.5,
+                        n_steps=2, seed=61)
+    steps = []
+    for st in wl.steps:
+        x = wl.to_f32(st).copy()
+        x[..., [3, 77, 200]] *= np.float32(scale)
+        steps.append(bf16_bits(x))
+    wl.steps = steps
+    x64 = wl.f64(wl.steps[0]).reshape(-1, wl.C)
+    q, k = x64 @ wl.f64(wl.wq).T, x64 @ wl.f64(wl.wk).T
+    top = max(float(np.abs(q[:, h * head_dim:(h + 1) * head_dim] @ k[:, h * head_dim:(h + 1) * head_dim].T).max())
+              for h in range(wl.heads)) / np.sqrt(head_dim)
+    _say(f"heavy-tailed {gran} x{scale}: largest |logit| {top:.3g}")
+    assert top < 100
+    chain(wl, 2)
+
+
 # ---------------------------------------------------------------------------
 # individual entry points
 # ---------------------------------------------------------------------------
@@ -125,11 +154,11 @@ def test_attn_reduced_vs_oracle(dtype, dh, n_seq, L, n_ctx):
                             ctx=dev_tensor(wl, ctx_s) if n_ctx else None)
     torch.cuda.synchronize()
     yk64, yc64 = O.attn_reduced(wl.f64(xk_s), wl.f64(ctx_s) if n_ctx else None, weights_f64(wl), heads, dh)
-    e = rel_err(to_f64(y), yk64, dtype)
-    _say(f"  err {e:.3g} (raw {rel_err(to_f64(y), yk64):.3g})")
-    assert e <= TOL[dtype]
+    e, raw = rel_err(to_f64(y), yk64, dtype), rel_err(to_f64(y), yk64)
     if n_ctx:
-        assert rel_err(to_f64(yc), yc64, dtype) <= TOL[dtype]
+        e, raw = max(e, rel_err(to_f64(yc), yc64, dtype)), max(raw, rel_err(to_f64(yc), yc64))
+    _say(f"  err {e:.3g} (raw {raw:.3g})")
+    check_output_bars(e, raw, dtype, "attention output", case=f"attn {dtype} dh{dh} {n_seq}x{L}+{n_ctx}")
 
 
 def test_gather_restore_bit_exact():
@@ -293,6 +322,15 @@ def test_latte_spatial_planted_chain():
     chain(wl, 3)
 
 
+def test_latte_spatial_chain():
+    """The unplanted Latte-like spatial layer the benchmark times: its eight
+    candidate frames' best similarities lie within 1e-4 of each other, so the
+    frame decisions are in the band and the oracle takes the library's
+    choices; the maps and outputs are then checked in full."""
+    wl = make_workload("latte_spatial", 3)
+    chain(wl, 3)
+
+
 def test_latte_temporal_chain():
     wl = make_workload("latte_temporal", 2)
     chain(wl, 2)
@@ -344,6 +382,6 @@ def test_svdxt_level_temporal_full_sampled():
     got = to_f64(y).reshape(wl.F, wl.H * wl.W, wl.C)[:, ns, :]
     ref = np.stack([O.multi_head_attention(x64[:, n, :], W64["wq"], W64["wk"], W64["wv"], W64["wo"], wl.heads,
                                            wl.head_dim) for n in ns], axis=1)
-    err = rel_err(got, ref, wl.dtype)
-    _say(f"  temporal layer sampled error {err:.3g}")
-    assert err <= TOL[wl.dtype]
+    err, raw = rel_err(got, ref, wl.dtype), rel_err(got, ref)
+    _say(f"  temporal layer sampled error {err:.3g} (raw {raw:.3g})")
+    check_output_bars(err, raw, wl.dtype, "temporal layer output")

@@ -17,6 +17,7 @@ import torch
 from oracle import oc_oracle as O
 from oracle import brute as B
 from oc_synth import small_workload
+import goldens
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -29,13 +30,11 @@ def _shape(wl):
     return O.LayerShape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, wl.n_ctx)
 
 
-def _frac(s):
-    if s.startswith("sqrt1/2"):
-        return math.sqrt(0.5)
-    if "/" in s:
-        a, b = s.split("/")
-        return int(a) / int(b)
-    return float(s)
+_frac = goldens.value
+
+
+def load_golden(name):
+    return goldens.load(name)
 
 
 # ----------------------------------------------------------------------------
@@ -85,6 +84,47 @@ def test_golden_block_variant_matches_token_example():
     seqs = O.build_sequences(shape, cfg, dec)
     assert [s[0] for s in seqs] == g["r0.5"]["kept_idx"]
     assert all(s == [s[0], s[0] + H * W] for s in seqs)
+
+
+@pytest.mark.parametrize("name,gran,ratio_key", [("frame_6x2x2_worked.json", O.FRAME, "r_frame"),
+                                                  ("block_2x2x4_worked.json", O.BLOCK, "r")])
+def test_golden_frame_and_block_matching_selection_and_maps(name, gran, ratio_key):
+    """Hand-worked Frame Cache (§3.2.2) and Block Cache (§3.2.1) examples:
+    similarities, matches (exact ties, a zero-norm block, a best match of 0
+    beside a -1), the selection at every ratio of the file, and kept_idx and
+    both restore maps, including the cold "matched" map that sends a skipped
+    frame (block) to its representative frame (block) position by position."""
+    g, x = load_golden(name)
+    F, H, W, C = g["F"], g["H"], g["W"], g["C"]
+    shape = O.LayerShape(F, H, W, C, 1, 4)
+    for r, expect in g["cached"].items():
+        cfg = O.CacheCfg(gran, **{ratio_key: float(r)})
+        dec = O.decide(x, shape, cfg)
+        assert len(dec.groups) == 1
+        grp = dec.groups[0]
+        assert grp.dst == g["representatives"] and grp.src == g["candidates"]
+        np.testing.assert_allclose(dec.node_max[0], [_frac(s) for s in g["node_max"]], rtol=0, atol=1e-15)
+        assert list(dec.node_idx[0]) == g["node_idx"]
+        assert O.selection_order(dec.node_max[0], grp.src) == g["selection_order"]
+        assert dec.cached[0] == expect, r
+    for key in (k for k in g if k.startswith("r0")):
+        cfg = O.CacheCfg(gran, **{ratio_key: float(key[1:])})
+        dec = O.decide(x, shape, cfg)
+        seqs = O.build_sequences(shape, cfg, dec)
+        kept, cached, rmap = O.kept_and_map(shape, cfg, dec, seqs, cache_valid=True)
+        assert list(kept) == g[key]["kept_idx"]
+        assert list(rmap) == g[key]["restore_map_valid_cache"]
+        _, _, cmap = O.kept_and_map(shape, cfg, dec, seqs, cache_valid=False)
+        assert list(cmap) == g[key]["restore_map_cold_matched"]
+
+
+def test_golden_expression_parser():
+    assert _frac("7/(2*sqrt(13))") == 7 / (2 * math.sqrt(13))
+    assert abs(_frac("1/sqrt(2)") - math.sqrt(0.5)) <= 2.3e-16
+    assert _frac("-3/4") == -0.75
+    assert _frac("0") == 0.0 and _frac("63/65") == 63 / 65
+    with pytest.raises(ValueError):
+        _frac("__import__('os')")
 
 
 # ----------------------------------------------------------------------------
@@ -485,17 +525,39 @@ def test_restore_identities():
         np.testing.assert_array_equal(y[p], yk[m[p]] if m[p] >= 0 else cache[p])
 
 
-def test_cold_matched_rows_equal_their_representative():
-    wl = small_workload(O.TOKEN, F=1, H=8, W=8, C=16, heads=2, head_dim=8, seed=13)
+@pytest.mark.parametrize("gran,F,k", [(O.TOKEN, 1, 1), (O.TOKEN, 2, 2), (O.FRAME, 6, 1), (O.BLOCK, 3, 1),
+                                      (O.BLOCK, 4, 2), (O.FRAME_TOKEN, 7, 1)])
+def test_cold_matched_rows_equal_their_representative(gran, F, k):
+    """On a cold "matched" step every skipped position carries, bit for bit,
+    the fresh output of the position its matched representative occupies
+    (§3.1: a copy, never an average).  The expected position is rebuilt here
+    from the per-candidate best matches and the grid geometry alone, not
+    from the oracle's own restore-map helper: a token takes its rep token, a
+    frame's token n takes token n of its rep frame, a block's frame-f token
+    takes frame f of its rep block."""
+    wl = small_workload(gran, F=F, H=8, W=8, C=16, heads=2, head_dim=8, seed=13, r=0.5, r_frame=0.35,
+                        planted=gran in (O.FRAME, O.FRAME_TOKEN))
     shape = _shape(wl)
     w = _w(wl)
     x = wl.f64(wl.steps[0])
-    cfg = O.CacheCfg(O.TOKEN, r=0.5)
+    cfg = O.CacheCfg(gran, r=0.5, r_frame=0.35, patch_k=k)
     res = O.layer_step(x, None, w, shape, cfg, None, cache_valid=False)
-    mt = O.matched_token(shape, cfg, res.decisions)
+    N = shape.N
+    expect = {}
+    for g, ni, c in zip(res.decisions.groups, res.decisions.node_idx, res.decisions.cached):
+        best = dict(zip(g.src, (int(v) for v in ni)))
+        for item in c:
+            if g.kind == "token":
+                expect[item] = best[item]
+            elif g.kind == "frame":
+                expect.update({item * N + n: best[item] * N + n for n in range(N)})
+            else:
+                expect.update({f * N + item: f * N + best[item] for f in range(shape.F)})
+    assert sorted(expect) == list(res.cached_idx) and len(expect) > 0
     y = res.y.reshape(-1, shape.C)
-    for p in res.cached_idx:
-        np.testing.assert_array_equal(y[p], y[mt[int(p)]])
+    for p, q in expect.items():
+        assert q not in expect
+        np.testing.assert_array_equal(y[p], y[q])
 
 
 def test_cache_chain_full_cold_then_reuse():
