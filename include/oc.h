@@ -255,6 +255,28 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
                           oc_trace *trace, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * oc_layer_cached_static — oc_layer_cached without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc).  Same arguments,
+ * results and errors as oc_layer_cached; the scratch is a library-owned
+ * device array of oc_static_scratch_bytes() (96 MiB) per device, which every
+ * device the library runs on holds until the process ends.  Allocates
+ * nothing.  A layer whose oc_plan_info.workspace_bytes exceeds that size is
+ * rejected with OC_ERR_WORKSPACE before anything is enqueued (the SD3-1024
+ * and Latte-sized layers fit; the SVD-XT-sized level, 576 MiB, does not).
+ * The stream must belong to the current device.  All calls on one device
+ * share that device's array, and each call rewrites what it reads of it:
+ * calls that overlap on one device (different streams or threads without
+ * ordering between them) race on it and must be serialised by the caller.
+ */
+oc_status oc_layer_cached_static(const oc_shape *shape, const oc_cfg *cfg, const void *x, const void *ctx,
+                                 const oc_attn_weights *w, oc_cache *cache, void *y_ctx, oc_trace *trace,
+                                 hipStream_t stream);
+
+/* Size in bytes of the static scratch oc_layer_cached_static uses. */
+size_t oc_static_scratch_bytes(void);
+
+/*
  * oc_attn_full — the uncached baseline: the layer as it runs without any
  * cache, i.e. the computation every cache of §3.2 skips part of (the
  * denominator of a cached layer's speed-up).  Spatial attention per frame

@@ -20,9 +20,11 @@ from .api import (  # noqa: F401
     attn_workspace_bytes,
     gather,
     layer_cached,
+    layer_cached_static,
     match,
     plan,
     restore,
     select,
+    static_scratch_bytes,
     workspace,
 )

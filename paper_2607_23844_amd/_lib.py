@@ -72,6 +72,9 @@ _SIGS = {
     "oc_restore": (C.c_int, [P(oc_shape), C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]),
     "oc_layer_cached": (C.c_int, [P(oc_shape), P(oc_cfg), C.c_void_p, C.c_void_p, P(oc_attn_weights), P(oc_cache),
                                   C.c_void_p, P(oc_trace), C.c_void_p, C.c_size_t, C.c_void_p]),
+    "oc_layer_cached_static": (C.c_int, [P(oc_shape), P(oc_cfg), C.c_void_p, C.c_void_p, P(oc_attn_weights),
+                                         P(oc_cache), C.c_void_p, P(oc_trace), C.c_void_p]),
+    "oc_static_scratch_bytes": (C.c_size_t, []),
     "oc_attn_full": (C.c_int, [P(oc_shape), P(oc_cfg), C.c_void_p, C.c_void_p, P(oc_attn_weights), C.c_void_p,
                                C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
     "oc_status_string": (C.c_char_p, [C.c_int]),

@@ -206,50 +206,77 @@ def restore(y_kept: torch.Tensor, restore_map: torch.Tensor, shape: Shape, cache
     return y
 
 
-def layer_cached(x: torch.Tensor, weights: Dict[str, torch.Tensor], cache: LayerCache, shape: Shape, cfg: Cfg,
-                 ctx: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, trace: bool = False):
-    """One cached layer call; returns (cache.y, y_ctx, trace dict or None)."""
+def _trace(shape: Shape, cfg: Cfg, cache: LayerCache, pl: PlanInfo, dev):
+    """Device buffers for a layer call's decisions and the oc_trace pointing
+    at them (a cold "full" step runs with every ratio at 0)."""
+    cold_full = cache.valid == 0 and cfg.cold == "full"
+    tp = plan(shape, Cfg(cfg.gran, 0.0, 0.0, cfg.patch_k, cfg.cold)) if cold_full else pl
+    n_kept, n_cached = tp.n_kept, tp.n_cached
+    out = dict(node_max=torch.empty((tp.n_groups, tp.n_src_max), dtype=torch.float32, device=dev),
+               node_idx=torch.empty((tp.n_groups, tp.n_src_max), dtype=torch.int32, device=dev),
+               kept_idx=torch.empty(max(n_kept, 1), dtype=torch.int32, device=dev),
+               cached_idx=torch.empty(max(n_cached, 1), dtype=torch.int32, device=dev),
+               restore_map=torch.empty(shape.F * shape.N, dtype=torch.int32, device=dev),
+               frame_max=torch.empty(max(pl.n_frame_src, 1), dtype=torch.float32, device=dev),
+               frame_idx=torch.empty(max(pl.n_frame_src, 1), dtype=torch.int32, device=dev),
+               pairs=torch.empty((max(pl.n_frame_cached, 1), 2), dtype=torch.int32, device=dev))
+    fi = L.oc_frame_info(out["frame_max"].data_ptr(), out["frame_idx"].data_ptr(), out["pairs"].data_ptr())
+    tr = L.oc_trace(out["node_max"].data_ptr(), out["node_idx"].data_ptr(), out["kept_idx"].data_ptr(),
+                    out["cached_idx"].data_ptr(), out["restore_map"].data_ptr(), fi)
+    out["kept_idx"] = out["kept_idx"][:n_kept]
+    out["cached_idx"] = out["cached_idx"][:n_cached]
+    out["frame_max"] = out["frame_max"][:pl.n_frame_src]
+    out["frame_idx"] = out["frame_idx"][:pl.n_frame_src]
+    out["pairs"] = out["pairs"][:tp.n_frame_cached]
+    return tr, out
+
+
+def _layer_args(x, weights, cache, shape, cfg, ctx, trace):
     _need(x, shape.torch_dtype, "x")
     _need(cache.y, shape.torch_dtype, "cache.y")
     w = _weights(weights, shape)
     dev = x.device
     pl = plan(shape, cfg)
-    if ws is None:
-        ws = workspace(shape, cfg, dev)
     y_ctx = None
     if shape.n_ctx > 0:
         _need(ctx, shape.torch_dtype, "ctx")
         y_ctx = torch.empty((shape.n_ctx, shape.C), dtype=x.dtype, device=dev)
-    tr = None
-    out = None
-    if trace:
-        cold_full = cache.valid == 0 and cfg.cold == "full"
-        # a cold "full" step runs with every ratio at 0
-        tp = plan(shape, Cfg(cfg.gran, 0.0, 0.0, cfg.patch_k, cfg.cold)) if cold_full else pl
-        n_kept, n_cached = tp.n_kept, tp.n_cached
-        out = dict(node_max=torch.empty((tp.n_groups, tp.n_src_max), dtype=torch.float32, device=dev),
-                   node_idx=torch.empty((tp.n_groups, tp.n_src_max), dtype=torch.int32, device=dev),
-                   kept_idx=torch.empty(max(n_kept, 1), dtype=torch.int32, device=dev),
-                   cached_idx=torch.empty(max(n_cached, 1), dtype=torch.int32, device=dev),
-                   restore_map=torch.empty(shape.F * shape.N, dtype=torch.int32, device=dev),
-                   frame_max=torch.empty(max(pl.n_frame_src, 1), dtype=torch.float32, device=dev),
-                   frame_idx=torch.empty(max(pl.n_frame_src, 1), dtype=torch.int32, device=dev),
-                   pairs=torch.empty((max(pl.n_frame_cached, 1), 2), dtype=torch.int32, device=dev))
-        fi = L.oc_frame_info(out["frame_max"].data_ptr(), out["frame_idx"].data_ptr(), out["pairs"].data_ptr())
-        tr = L.oc_trace(out["node_max"].data_ptr(), out["node_idx"].data_ptr(), out["kept_idx"].data_ptr(),
-                        out["cached_idx"].data_ptr(), out["restore_map"].data_ptr(), fi)
-        out["kept_idx"] = out["kept_idx"][:n_kept]
-        out["cached_idx"] = out["cached_idx"][:n_cached]
-        out["frame_max"] = out["frame_max"][:pl.n_frame_src]
-        out["frame_idx"] = out["frame_idx"][:pl.n_frame_src]
-        out["pairs"] = out["pairs"][:tp.n_frame_cached]
+    tr, out = _trace(shape, cfg, cache, pl, dev) if trace else (None, None)
     c = L.oc_cache(cache.y.data_ptr(), cache.valid, cache.step)
+    return w, pl, y_ctx, tr, out, c
+
+
+def layer_cached(x: torch.Tensor, weights: Dict[str, torch.Tensor], cache: LayerCache, shape: Shape, cfg: Cfg,
+                 ctx: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, trace: bool = False):
+    """One cached layer call; returns (cache.y, y_ctx, trace dict or None)."""
+    w, pl, y_ctx, tr, out, c = _layer_args(x, weights, cache, shape, cfg, ctx, trace)
+    if ws is None:
+        ws = workspace(shape, cfg, x.device)
     sh, cf = shape.c(), cfg.c()
     L.check(L.lib().oc_layer_cached(C.byref(sh), C.byref(cf), x.data_ptr(), _ptr(ctx), C.byref(w), C.byref(c),
                                     _ptr(y_ctx), C.byref(tr) if tr is not None else None, ws.data_ptr(), ws.numel(),
                                     _stream(x)))
     cache.valid, cache.step = c.valid, c.step
     return cache.y, y_ctx, out
+
+
+def layer_cached_static(x: torch.Tensor, weights: Dict[str, torch.Tensor], cache: LayerCache, shape: Shape,
+                        cfg: Cfg, ctx: Optional[torch.Tensor] = None, trace: bool = False):
+    """oc_layer_cached_static: the same layer call with the library's own
+    device scratch instead of a workspace (the library allocates nothing;
+    the binding allocates only the outputs it returns: y_ctx and the trace
+    buffers when asked for)."""
+    w, pl, y_ctx, tr, out, c = _layer_args(x, weights, cache, shape, cfg, ctx, trace)
+    sh, cf = shape.c(), cfg.c()
+    L.check(L.lib().oc_layer_cached_static(C.byref(sh), C.byref(cf), x.data_ptr(), _ptr(ctx), C.byref(w),
+                                           C.byref(c), _ptr(y_ctx), C.byref(tr) if tr is not None else None,
+                                           _stream(x)))
+    cache.valid, cache.step = c.valid, c.step
+    return cache.y, y_ctx, out
+
+
+def static_scratch_bytes() -> int:
+    return int(L.lib().oc_static_scratch_bytes())
 
 
 def attn_full(x: torch.Tensor, weights: Dict[str, torch.Tensor], shape: Shape, cfg: Cfg,

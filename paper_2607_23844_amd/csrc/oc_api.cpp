@@ -533,6 +533,25 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
     return ok();
 }
 
+oc_status oc_layer_cached_static(const oc_shape *shape, const oc_cfg *cfg, const void *x, const void *ctx,
+                                 const oc_attn_weights *w, oc_cache *cache, void *y_ctx, oc_trace *trace,
+                                 hipStream_t stream) {
+    Plan p;
+    oc_status s = make_plan(shape, cfg, false, p);
+    if (s != OC_OK) return s;
+    const size_t need = workspace_for(shape, cfg);
+    if (need > OC_STATIC_SCRATCH_BYTES)
+        return fail(OC_ERR_WORKSPACE,
+                    "this layer needs %zu bytes of scratch, more than the library's static scratch of %zu bytes: "
+                    "call oc_layer_cached with a workspace instead",
+                    need, (size_t)OC_STATIC_SCRATCH_BYTES);
+    void *ws = nullptr;
+    HIP_TRY(static_scratch(&ws), "static scratch address");
+    return oc_layer_cached(shape, cfg, x, ctx, w, cache, y_ctx, trace, ws, OC_STATIC_SCRATCH_BYTES, stream);
+}
+
+size_t oc_static_scratch_bytes(void) { return OC_STATIC_SCRATCH_BYTES; }
+
 oc_status oc_attn_full(const oc_shape *shape, const oc_cfg *cfg, const void *x, const void *ctx,
                        const oc_attn_weights *w, void *y, void *y_ctx, void *ws, size_t ws_bytes,
                        hipStream_t stream) {

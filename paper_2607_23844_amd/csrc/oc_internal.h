@@ -163,6 +163,11 @@ struct AttnArgs {
     int tF, tN;                       // no index lists: row r = n*tF + f is token f*tN + n (tF > 0)
 };
 hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st);
+
+// Library-owned device scratch of oc_layer_cached_static: size, and the
+// current device's address (looked up once per device).
+constexpr size_t OC_STATIC_SCRATCH_BYTES = (size_t)96 << 20;
+hipError_t static_scratch(void **out);
 bool attn_head_dim_supported(int dh);
 
 }  // namespace oc

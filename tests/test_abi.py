@@ -266,3 +266,23 @@ def test_plan_and_errors_from_many_threads():
         t.join()
     assert not errors, errors
     assert len(results) == 8 * 200 and all(results)
+
+
+def test_static_entry_point_rejects_layers_beyond_its_scratch():
+    """oc_layer_cached_static refuses, before any device work, a layer whose
+    workspace exceeds the library's static scratch (the SVD-XT-sized level
+    needs 576 MiB against 96 MiB), with a message naming both sizes."""
+    lib = L.lib()
+    big = oc.Shape(25, 72, 128, 320, 5, 64, 0, "bf16")
+    cfg = oc.Cfg("frame_token", r=0.5, r_frame=0.2)
+    need = oc.plan(big, cfg).workspace_bytes
+    assert need > oc.static_scratch_bytes() == 96 << 20
+    sh, cf = big.c(), cfg.c()
+    w = L.oc_attn_weights(FAKE, FAKE, FAKE, FAKE)
+    cache = L.oc_cache(FAKE * 2, 0, 0)
+    st = lib.oc_layer_cached_static(C.byref(sh), C.byref(cf), FAKE, None, C.byref(w), C.byref(cache), None, None,
+                                    None)
+    assert st == L.OC_ERR_WORKSPACE
+    msg = lib.oc_last_error().decode()
+    assert str(need) in msg and str(96 << 20) in msg
+    assert cache.valid == 0 and cache.step == 0
