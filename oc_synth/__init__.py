@@ -10,6 +10,7 @@ from .workloads import (  # noqa: F401
     Workload,
     bf16_bits,
     bf16_bits_to_f32,
+    ffn_weights,
     make_workload,
     small_workload,
 )

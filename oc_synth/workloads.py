@@ -273,6 +273,16 @@ WORKLOADS = {
 }
 
 
+def ffn_weights(C: int, hidden: int, dtype: str, seed: int = 2000) -> Dict[str, np.ndarray]:
+    """Feed-forward weights of a layer of width C: w1 [hidden, C] ~ N(0, 1/C)
+    then w2 [C, hidden] ~ N(0, 1/hidden), drawn from their own seeded
+    generator (so adding them leaves every attention workload unchanged)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    w1 = rng.standard_normal((hidden, C), dtype=np.float32) * np.float32(1.0 / math.sqrt(C))
+    w2 = rng.standard_normal((C, hidden), dtype=np.float32) * np.float32(1.0 / math.sqrt(hidden))
+    return dict(w1=_store(w1, dtype), w2=_store(w2, dtype))
+
+
 def make_workload(name: str, n_steps: int = 4) -> Workload:
     return WORKLOADS[name](n_steps)
 

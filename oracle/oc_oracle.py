@@ -38,6 +38,14 @@ readings (the same list, with reasons, is kept with the design notes):
   R15 The retained tokens of a pair form one attention sequence.
   R16 Text-context tokens are appended to the (single) image sequence and
       never cached.
+  R21 The feed-forward sublayer (cached under the same selection as the
+      attention of its block, as the SD3 experiments do, §4.2 "Design
+      choices") is two linear maps with a tanh-approximated GELU between
+      them and no bias: y = GELU(x W1^T) W2^T, W1 [hidden, C], W2 [C,
+      hidden].  Retained positions are computed; cached positions keep the
+      previous step's FFN output at the same position, or, on a step with
+      no valid cache under the "matched" policy, the fresh output of the
+      position their best match occupies (the attention call's restore map).
 
 Group order (used to lay out per-candidate results):
   token        : frame-major, then k x k patches row-major
@@ -71,6 +79,7 @@ __all__ = [
     "frame_group", "pair_token_groups", "decide", "build_sequences",
     "kept_and_map", "multi_head_attention", "attn_reduced", "restore",
     "layer_step", "full_attention", "descriptors", "flatten_match",
+    "gelu_tanh", "feed_forward", "ffn_step",
 ]
 
 
@@ -635,3 +644,32 @@ def flatten_match(dec: Decisions) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
         ni[gi, :n] = dec.node_idx[gi]
         ids[gi, :n] = g.src
     return nm, ni, ids
+
+
+# ----------------------------------------------------------------------------
+# feed-forward sublayer under the same selection (R21)
+# ----------------------------------------------------------------------------
+
+def gelu_tanh(u: np.ndarray) -> np.ndarray:
+    """GELU with the tanh approximation:
+    0.5 u (1 + tanh(sqrt(2/pi) (u + 0.044715 u^3)))."""
+    u = np.asarray(u, dtype=np.float64)
+    return 0.5 * u * (1.0 + np.tanh(math.sqrt(2.0 / math.pi) * (u + 0.044715 * u ** 3)))
+
+
+def feed_forward(X: np.ndarray, w1: np.ndarray, w2: np.ndarray) -> np.ndarray:
+    """The feed-forward map of rows X [n, C]: GELU(X W1^T) W2^T (R21)."""
+    return gelu_tanh(X @ w1.T) @ w2.T
+
+
+def ffn_step(x: np.ndarray, kept_idx: np.ndarray, restore_map: np.ndarray, w1: np.ndarray, w2: np.ndarray,
+             cache_y: Optional[np.ndarray]) -> np.ndarray:
+    """One cached FFN call under a selection made by the attention sublayer:
+    the retained rows x[kept_idx] go through the feed-forward map (row i of
+    the reduced batch is token kept_idx[i]) and every position is then
+    restored through the same restore map as the attention output (§3.2.3
+    restoration at original positions; R9 on a cold step).  x is [F*N, C]."""
+    x = np.asarray(x, dtype=np.float64).reshape(-1, w1.shape[1])
+    y_kept = feed_forward(x[np.asarray(kept_idx, dtype=np.int64)], w1, w2)
+    cy = None if cache_y is None else np.asarray(cache_y, dtype=np.float64).reshape(-1, w1.shape[1])
+    return restore(y_kept, np.asarray(restore_map), cy)
