@@ -255,6 +255,44 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
                           oc_trace *trace, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Feed-forward sublayer under the same selection.  The SD3 experiments cache
+ * attention and feed-forward layers alike (§4.2 "Design choices"): the
+ * tokens the attention sublayer retained also go through the FFN, and the
+ * rest are restored at their positions.  The FFN is two linear maps with a
+ * tanh-approximated GELU between them and no bias.
+ */
+typedef struct {
+    const void *w1;           /* [hidden, C]: first linear map, out x in      */
+    const void *w2;           /* [C, hidden]: second linear map, out x in     */
+    int32_t hidden;           /* inner width (SD3: 4 C)                       */
+    int32_t reserved;         /* must be 0                                     */
+} oc_ffn_weights;
+
+/*
+ * oc_ffn_reduced — for the n_rows retained tokens t_i = kept_idx[i] (or
+ * t_i = i when kept_idx is NULL):
+ *   z_i = GELU(x[t_i] W1^T) W2^T,  GELU(v) = 0.5 v (1 + tanh(sqrt(2/pi)(v + 0.044715 v^3)));
+ * x is [F, N, C] bf16 (the FFN input of every position; only retained rows
+ * are read).  scatter = 1: y is [F, N, C] and z_i is written to y[t_i],
+ * every other row of y is left untouched (y holding the previous step's FFN
+ * output, that is restoration in place, as oc_layer_cached does for the
+ * attention); scatter = 0: y is [n_rows, C] and z_i goes to row i (then
+ * oc_restore with the attention call's restore map covers the cold step).
+ * bf16 only (OC_ERR_DTYPE otherwise); C and hidden multiples of 64
+ * (OC_ERR_SHAPE); kept_idx entries outside [0, F*N) are not read and their
+ * rows not written.  ws_bytes >= oc_ffn_workspace_bytes(shape, hidden,
+ * n_rows): the [n_rows, hidden] activations between the two maps, held in
+ * fp16 (range and precision as stated for the attention intermediates),
+ * and an fp16 copy of W2 made by the same call.
+ * y must not alias x.
+ */
+oc_status oc_ffn_reduced(const oc_shape *shape, const void *x, const int32_t *kept_idx, int32_t n_rows,
+                         const oc_ffn_weights *w, void *y, int32_t scatter, void *ws, size_t ws_bytes,
+                         hipStream_t stream);
+
+size_t oc_ffn_workspace_bytes(const oc_shape *shape, int32_t hidden, int32_t n_rows);
+
+/*
  * oc_layer_cached_static — oc_layer_cached without a workspace argument, for
  * callers that cannot allocate device memory (code under HIP graph capture,
  * tight serving loops, harnesses that forbid hipMalloc).  Same arguments,

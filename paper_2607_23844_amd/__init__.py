@@ -18,6 +18,8 @@ from .api import (  # noqa: F401
     attn_full,
     attn_reduced,
     attn_workspace_bytes,
+    ffn_reduced,
+    ffn_workspace_bytes,
     gather,
     layer_cached,
     layer_cached_static,

@@ -275,6 +275,43 @@ def layer_cached_static(x: torch.Tensor, weights: Dict[str, torch.Tensor], cache
     return cache.y, y_ctx, out
 
 
+def ffn_workspace_bytes(shape: Shape, hidden: int, n_rows: int) -> int:
+    sh = shape.c()
+    return int(L.lib().oc_ffn_workspace_bytes(C.byref(sh), hidden, n_rows))
+
+
+def ffn_reduced(x: torch.Tensor, weights: Dict[str, torch.Tensor], shape: Shape,
+                kept_idx: Optional[torch.Tensor] = None, n_rows: Optional[int] = None,
+                y: Optional[torch.Tensor] = None, scatter: bool = True,
+                ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """oc_ffn_reduced: GELU(x[t] W1^T) W2^T for the retained tokens t of
+    kept_idx (all tokens when None).  scatter: written into y [F, N, C] at
+    their positions (other rows untouched); else y is [n_rows, C]."""
+    _need(x, shape.torch_dtype, "x")
+    w1, w2 = weights["w1"], weights["w2"]
+    hidden = w1.shape[0]
+    for k, t, s in (("w1", w1, (hidden, shape.C)), ("w2", w2, (shape.C, hidden))):
+        _need(t, shape.torch_dtype, k)
+        if tuple(t.shape) != s:
+            raise L.OmniCacheError(L.OC_ERR_SHAPE, f"{k} has shape {tuple(t.shape)}, expected {s}")
+    if kept_idx is not None:
+        _need(kept_idx, torch.int32, "kept_idx")
+        n = kept_idx.numel() if n_rows is None else n_rows
+    else:
+        n = shape.F * shape.N if n_rows is None else n_rows
+    dev = x.device
+    if y is None:
+        y = torch.empty((shape.F, shape.N, shape.C) if scatter else (max(n, 1), shape.C), dtype=x.dtype, device=dev)
+    _need(y, shape.torch_dtype, "y")
+    if ws is None:
+        ws = torch.empty(max(ffn_workspace_bytes(shape, hidden, n), 256), dtype=torch.uint8, device=dev)
+    fw = L.oc_ffn_weights(w1.data_ptr(), w2.data_ptr(), hidden, 0)
+    sh = shape.c()
+    L.check(L.lib().oc_ffn_reduced(C.byref(sh), x.data_ptr(), _ptr(kept_idx), n, C.byref(fw), y.data_ptr(),
+                                   1 if scatter else 0, ws.data_ptr(), ws.numel(), _stream(x)))
+    return y if scatter else y[:n]
+
+
 def static_scratch_bytes() -> int:
     return int(L.lib().oc_static_scratch_bytes())
 

@@ -533,6 +533,43 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
     return ok();
 }
 
+size_t oc_ffn_workspace_bytes(const oc_shape *shape, int32_t hidden, int32_t n_rows) {
+    if (check_shape(shape) != OC_OK || hidden < 0 || n_rows < 0) return 0;
+    return ffn_workspace_bytes(n_rows, hidden, shape->C);
+}
+
+oc_status oc_ffn_reduced(const oc_shape *shape, const void *x, const int32_t *kept_idx, int32_t n_rows,
+                         const oc_ffn_weights *w, void *y, int32_t scatter, void *ws, size_t ws_bytes,
+                         hipStream_t stream) {
+    oc_status s = check_shape(shape);
+    if (s != OC_OK) return s;
+    if (shape->dtype != OC_BF16) return fail(OC_ERR_DTYPE, "the feed-forward path takes bf16 tensors only");
+    if (!w || !w->w1 || !w->w2) return fail(OC_ERR_INVALID_ARG, "weights NULL");
+    if (w->reserved != 0) return fail(OC_ERR_INVALID_ARG, "oc_ffn_weights.reserved must be 0");
+    if (w->hidden < 64 || w->hidden % 64 || shape->C % 64)
+        return fail(OC_ERR_SHAPE, "feed-forward needs C=%d and hidden=%d to be positive multiples of 64", shape->C,
+                    w->hidden);
+    const long long FN = (long long)shape->F * shape->H * shape->W;
+    if (n_rows < 0 || n_rows > FN) return fail(OC_ERR_SHAPE, "n_rows=%d outside [0, F*N=%lld]", n_rows, FN);
+    if ((long long)w->hidden * shape->C >= (1LL << 31) || (long long)n_rows * w->hidden >= (1LL << 31))
+        return fail(OC_ERR_SHAPE, "feed-forward too large for 32-bit element offsets");
+    if (scatter != 0 && scatter != 1) return fail(OC_ERR_INVALID_ARG, "scatter must be 0 or 1");
+    if (!x || !y) return fail(OC_ERR_INVALID_ARG, "NULL x / y");
+    if (!aligned16(x) || !aligned16(y) || !aligned16(w->w1) || !aligned16(w->w2))
+        return fail(OC_ERR_INVALID_ARG, "x, y and the weights must be 16-byte aligned");
+    if (x == y) return fail(OC_ERR_INVALID_ARG, "y must not alias x");
+    if ((s = check_ws(ws, ws_bytes, ffn_workspace_bytes(n_rows, w->hidden, shape->C))) != OC_OK) return s;
+    if (n_rows == 0) return ok();
+    FfnArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.x = x; a.idx = kept_idx; a.n_rows = n_rows; a.FN = (int)FN; a.C = shape->C; a.hidden = w->hidden;
+    a.w1 = w->w1; a.w2 = w->w2; a.h = ws;
+    a.scatter = scatter;
+    a.y = y;
+    HIP_TRY(launch_ffn(a, stream), "feed-forward");
+    return ok();
+}
+
 oc_status oc_layer_cached_static(const oc_shape *shape, const oc_cfg *cfg, const void *x, const void *ctx,
                                  const oc_attn_weights *w, oc_cache *cache, void *y_ctx, oc_trace *trace,
                                  hipStream_t stream) {

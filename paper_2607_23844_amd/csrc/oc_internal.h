@@ -164,6 +164,18 @@ struct AttnArgs {
 };
 hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st);
 
+// Feed-forward sublayer over retained rows (k_ffn.hip).
+struct FfnArgs {
+    const void *x; const int32_t *idx;   // batch row r -> token idx[r] (idx == nullptr: r)
+    int n_rows, FN, C, hidden;
+    const void *w1, *w2;                 // [hidden, C], [C, hidden]
+    void *h;                             // scratch: H [n_rows, hidden] fp16, then W2 as fp16
+    int scatter;                         // 1: row r -> y row idx[r] (or r); 0: y row r
+    void *y;
+};
+size_t ffn_workspace_bytes(int n_rows, int hidden, int C);
+hipError_t launch_ffn(const FfnArgs &a, hipStream_t st);
+
 // Library-owned device scratch of oc_layer_cached_static: size, and the
 // current device's address (looked up once per device).
 constexpr size_t OC_STATIC_SCRATCH_BYTES = (size_t)96 << 20;

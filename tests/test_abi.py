@@ -69,6 +69,7 @@ def test_struct_sizes_match_the_header_layout():
     assert C.sizeof(L.oc_attn_weights) == 32
     assert C.sizeof(L.oc_plan_info) == 48
     assert C.sizeof(L.oc_trace) == 64
+    assert C.sizeof(L.oc_ffn_weights) == 24
 
 
 WORKLOAD_SHAPES = [
@@ -286,3 +287,32 @@ def test_static_entry_point_rejects_layers_beyond_its_scratch():
     msg = lib.oc_last_error().decode()
     assert str(need) in msg and str(96 << 20) in msg
     assert cache.valid == 0 and cache.step == 0
+
+
+def test_ffn_entry_point_validates_before_launching():
+    lib = L.lib()
+    sh = oc.Shape(1, 8, 8, 64, 2, 32, 0, "bf16").c()
+    need = lib.oc_ffn_workspace_bytes(C.byref(sh), 256, 32)
+    assert need == 32 * 256 * 2 + 64 * 256 * 2
+    w = L.oc_ffn_weights(FAKE, FAKE, 256, 0)
+    ok_args = (C.byref(sh), FAKE, FAKE, 32, C.byref(w), FAKE * 2, 1, FAKE, need, None)
+    assert lib.oc_ffn_reduced(*ok_args[:8], need - 1, None) == L.OC_ERR_WORKSPACE
+    bad = L.oc_ffn_weights(FAKE, FAKE, 96, 0)                       # hidden not a multiple of 64
+    assert lib.oc_ffn_reduced(C.byref(sh), FAKE, FAKE, 32, C.byref(bad), FAKE * 2, 1, FAKE, need, None) == \
+        L.OC_ERR_SHAPE
+    res = L.oc_ffn_weights(FAKE, FAKE, 256, 1)
+    assert lib.oc_ffn_reduced(C.byref(sh), FAKE, FAKE, 32, C.byref(res), FAKE * 2, 1, FAKE, need, None) == \
+        L.OC_ERR_INVALID_ARG
+    assert lib.oc_ffn_reduced(C.byref(sh), FAKE, FAKE, 65, C.byref(w), FAKE * 2, 1, FAKE, 1 << 30, None) == \
+        L.OC_ERR_SHAPE                                                # more rows than tokens
+    assert lib.oc_ffn_reduced(C.byref(sh), FAKE, FAKE, 32, C.byref(w), FAKE, 1, FAKE, need, None) == \
+        L.OC_ERR_INVALID_ARG                                          # y aliases x
+    assert lib.oc_ffn_reduced(C.byref(sh), FAKE, FAKE, 32, C.byref(w), FAKE * 2, 2, FAKE, need, None) == \
+        L.OC_ERR_INVALID_ARG
+    f32 = oc.Shape(1, 8, 8, 64, 2, 32, 0, "f32").c()
+    assert lib.oc_ffn_reduced(C.byref(f32), FAKE, FAKE, 32, C.byref(w), FAKE * 2, 1, FAKE, need, None) == \
+        L.OC_ERR_DTYPE
+    c72 = oc.Shape(1, 8, 8, 72, 2, 32, 0, "bf16").c()
+    assert lib.oc_ffn_reduced(C.byref(c72), FAKE, FAKE, 32, C.byref(w), FAKE * 2, 1, FAKE, need, None) == \
+        L.OC_ERR_SHAPE
+    assert lib.oc_ffn_reduced(C.byref(sh), FAKE, FAKE, 0, C.byref(w), FAKE * 2, 1, FAKE, 0, None) == L.OC_OK
