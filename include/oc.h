@@ -328,6 +328,28 @@ oc_status oc_attn_full(const oc_shape *shape, const oc_cfg *cfg, const void *x, 
                        const oc_attn_weights *w, void *y, void *y_ctx,
                        void *ws, size_t ws_bytes, hipStream_t stream);
 
+/*
+ * Layered Cache schedule proposal (§3.4, Alg. 1), host only.  For each
+ * candidate layer-timestep pair (l, t) the caller gives the latency L[l,t]
+ * that reusing the cache there saves and the quality loss Q[l,t] it costs
+ * (row-major [n_layers, n_steps] tables); mask (may be NULL: every pair)
+ * marks the candidates.  Pairs are scored w = Q/L, taken from the lowest
+ * score up and written to out as (l, t, interval) until the saved latency
+ * is at least (1 - 1/target_speedup) times the summed latency of all
+ * candidates (or no candidate is left).  Candidates are enumerated
+ * layer-major; equal scores keep that order and sums run in that order.
+ * Requirements (OC_ERR_INVALID_ARG otherwise): target_speedup >= 1,
+ * interval >= 1, every candidate's L finite and > 0 and Q finite, and
+ * capacity at least the number of pairs chosen (n_layers * n_steps always
+ * suffices).  *n_out receives the count; saved / budget (may be NULL) the
+ * saved latency and the budget.
+ */
+typedef struct { int32_t layer, step, interval; } oc_cache_entry;
+
+oc_status oc_layered_schedule(int32_t n_layers, int32_t n_steps, const double *latency, const double *quality,
+                              const uint8_t *mask, double target_speedup, int32_t interval, oc_cache_entry *out,
+                              int32_t capacity, int32_t *n_out, double *saved, double *budget);
+
 const char *oc_status_string(oc_status s);
 const char *oc_last_error(void);
 

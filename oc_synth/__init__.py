@@ -11,6 +11,7 @@ from .workloads import (  # noqa: F401
     bf16_bits,
     bf16_bits_to_f32,
     ffn_weights,
+    layered_tables,
     make_workload,
     small_workload,
 )

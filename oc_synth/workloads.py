@@ -283,6 +283,22 @@ def ffn_weights(C: int, hidden: int, dtype: str, seed: int = 2000) -> Dict[str, 
     return dict(w1=_store(w1, dtype), w2=_store(w2, dtype))
 
 
+def layered_tables(n_layers: int = 24, n_steps: int = 28, seed: int = 3000):
+    """Synthetic per-(layer, timestep) tables for the Layered Cache schedule,
+    shaped like SD3-medium (24 transformer blocks, 28 sampling steps; §4.1):
+    latency saved by caching a pair ~ 1 ms with 10% spread (blocks of one
+    width cost alike), and quality loss log-normal, four times larger in the
+    first and last four blocks and larger at early timesteps (§4.2 finds early
+    and late layers most sensitive).  Returns (latency, quality), fp64
+    [n_layers, n_steps]."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    lat = np.clip(1.0 + 0.1 * rng.standard_normal((n_layers, n_steps)), 0.5, None)
+    edge = np.array([4.0 if (l < 4 or l >= n_layers - 4) else 1.0 for l in range(n_layers)])
+    early = 1.0 + 2.0 * np.exp(-np.arange(n_steps) / 4.0)
+    qual = np.exp(0.5 * rng.standard_normal((n_layers, n_steps))) * edge[:, None] * early[None, :]
+    return lat, qual
+
+
 def make_workload(name: str, n_steps: int = 4) -> Workload:
     return WORKLOADS[name](n_steps)
 

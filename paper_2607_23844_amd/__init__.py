@@ -23,6 +23,7 @@ from .api import (  # noqa: F401
     gather,
     layer_cached,
     layer_cached_static,
+    layered_schedule,
     match,
     plan,
     restore,

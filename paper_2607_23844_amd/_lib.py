@@ -53,6 +53,10 @@ class oc_ffn_weights(C.Structure):
     _fields_ = [("w1", C.c_void_p), ("w2", C.c_void_p), ("hidden", C.c_int32), ("reserved", C.c_int32)]
 
 
+class oc_cache_entry(C.Structure):
+    _fields_ = [("layer", C.c_int32), ("step", C.c_int32), ("interval", C.c_int32)]
+
+
 class oc_frame_info(C.Structure):
     _fields_ = [("frame_max", C.c_void_p), ("frame_idx", C.c_void_p), ("pairs", C.c_void_p)]
 
@@ -79,6 +83,9 @@ _SIGS = {
     "oc_ffn_reduced": (C.c_int, [P(oc_shape), C.c_void_p, C.c_void_p, C.c_int32, P(oc_ffn_weights), C.c_void_p,
                                  C.c_int32, C.c_void_p, C.c_size_t, C.c_void_p]),
     "oc_ffn_workspace_bytes": (C.c_size_t, [P(oc_shape), C.c_int32, C.c_int32]),
+    "oc_layered_schedule": (C.c_int, [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_double,
+                                      C.c_int32, P(oc_cache_entry), C.c_int32, P(C.c_int32), P(C.c_double),
+                                      P(C.c_double)]),
     "oc_layer_cached_static": (C.c_int, [P(oc_shape), P(oc_cfg), C.c_void_p, C.c_void_p, P(oc_attn_weights),
                                          P(oc_cache), C.c_void_p, P(oc_trace), C.c_void_p]),
     "oc_static_scratch_bytes": (C.c_size_t, []),

@@ -312,6 +312,27 @@ def ffn_reduced(x: torch.Tensor, weights: Dict[str, torch.Tensor], shape: Shape,
     return y if scatter else y[:n]
 
 
+def layered_schedule(latency, quality, target_speedup: float, interval: int, mask=None):
+    """oc_layered_schedule (§3.4, Alg. 1) on host tables [n_layers, n_steps]:
+    returns ([(layer, step, interval), ...] in selection order, saved, budget)."""
+    import numpy as np
+    lat = np.ascontiguousarray(latency, dtype=np.float64)
+    qual = np.ascontiguousarray(quality, dtype=np.float64)
+    if lat.ndim != 2 or qual.shape != lat.shape:
+        raise L.OmniCacheError(L.OC_ERR_SHAPE, "latency and quality must be equal-shaped 2-D tables")
+    m = None if mask is None else np.ascontiguousarray(mask, dtype=np.uint8)
+    if m is not None and m.shape != lat.shape:
+        raise L.OmniCacheError(L.OC_ERR_SHAPE, "mask must have the tables' shape")
+    n_l, n_t = lat.shape
+    cap = max(n_l * n_t, 1)
+    out = (L.oc_cache_entry * cap)()
+    n, saved, budget = C.c_int32(), C.c_double(), C.c_double()
+    L.check(L.lib().oc_layered_schedule(n_l, n_t, lat.ctypes.data, qual.ctypes.data,
+                                        None if m is None else m.ctypes.data, float(target_speedup), int(interval),
+                                        out, cap, C.byref(n), C.byref(saved), C.byref(budget)))
+    return [(out[i].layer, out[i].step, out[i].interval) for i in range(n.value)], saved.value, budget.value
+
+
 def static_scratch_bytes() -> int:
     return int(L.lib().oc_static_scratch_bytes())
 

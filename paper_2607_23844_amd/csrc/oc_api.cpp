@@ -324,6 +324,14 @@ oc_status copy_d2d(void *dst, const void *src, size_t bytes, hipStream_t st) {
 
 }  // namespace
 
+namespace oc {
+// Status and message for the host-only entry points in other sources.
+oc_status record_error(oc_status s, const char *msg) {
+    if (s == OC_OK) return ok();
+    return fail(s, "%s", msg);
+}
+}  // namespace oc
+
 extern "C" {
 
 const char *oc_status_string(oc_status s) {

@@ -70,6 +70,7 @@ def test_struct_sizes_match_the_header_layout():
     assert C.sizeof(L.oc_plan_info) == 48
     assert C.sizeof(L.oc_trace) == 64
     assert C.sizeof(L.oc_ffn_weights) == 24
+    assert C.sizeof(L.oc_cache_entry) == 12
 
 
 WORKLOAD_SHAPES = [
