@@ -255,6 +255,37 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
                           oc_trace *trace, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * oc_residual_add — h = x + y elementwise over [F, N, C] (added in fp32,
+ * rounded once to the tensor's type, bf16: round to nearest even): the
+ * residual connection that feeds a block's spatial-layer output to its
+ * temporal layer.  h may alias x or y.
+ */
+oc_status oc_residual_add(const oc_shape *shape, const void *x, const void *y, void *h, hipStream_t stream);
+
+/*
+ * oc_block_cached — one spatial + temporal block of a video denoiser with all
+ * three caches at once (§3.2: Frame and Token Cache on the spatial layer,
+ * Block Cache on the temporal layer; §4.2 runs them together at ratios
+ * r_f / r_b / r_t such as 50/40/50 for SVD-XT and 30/40/20 for Latte):
+ *   spatial layer:  oc_layer_cached(shape, spatial, x) -> cache_spatial->y;
+ *   residual:       h = x + cache_spatial->y (oc_residual_add);
+ *   temporal layer: oc_layer_cached(shape, temporal, h) -> cache_temporal->y,
+ * each layer with its own weights and its own layer cache (the temporal
+ * layer's cached blocks are matched on h).  spatial->gran is TOKEN, FRAME or
+ * FRAME_TOKEN, temporal->gran is BLOCK; n_ctx must be 0.  x, h and the two
+ * caches are distinct [F, N, C] buffers; the traces may be NULL.  Every
+ * argument of both layers is validated before anything is enqueued.
+ * ws_bytes >= oc_block_workspace_bytes(shape, spatial, temporal) (the two
+ * layers run one after the other on the stream and share it).
+ */
+oc_status oc_block_cached(const oc_shape *shape, const oc_cfg *spatial, const oc_cfg *temporal, const void *x,
+                          const oc_attn_weights *w_spatial, const oc_attn_weights *w_temporal,
+                          oc_cache *cache_spatial, oc_cache *cache_temporal, void *h, oc_trace *trace_spatial,
+                          oc_trace *trace_temporal, void *ws, size_t ws_bytes, hipStream_t stream);
+
+size_t oc_block_workspace_bytes(const oc_shape *shape, const oc_cfg *spatial, const oc_cfg *temporal);
+
+/*
  * Feed-forward sublayer under the same selection.  The SD3 experiments cache
  * attention and feed-forward layers alike (§4.2 "Design choices"): the
  * tokens the attention sublayer retained also go through the FFN, and the

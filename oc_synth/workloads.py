@@ -261,6 +261,34 @@ def _svdxt(n_steps, planted=False, patch_k=1):
                     steps, None, *w, t_weights=dict(wq=tw[0], wk=tw[1], wv=tw[2], wo=tw[3]))
 
 
+def _latte_block(n_steps):
+    """Latte-like spatial + temporal block with all three caches at the
+    paper's Latte ratios (r_f / r_b / r_t = 30 / 40 / 20 %): 16 frames of
+    16x16 tokens, C=1152, 16 heads x 72, bf16; the Latte generator with the
+    0.5 token-per-frame translation (frame and motion redundancy both
+    present); spatial and temporal layers with their own weights."""
+    rng = np.random.Generator(np.random.PCG64(1006))
+    F, H, W, C, heads, dh = 16, 16, 16, 1152, 16, 72
+    x0 = _latte_frames(rng, F, H, W, C, shift_per_frame=0.5)
+    w = _weights(rng, C, heads, dh, "bf16")
+    tw = _weights(rng, C, heads, dh, "bf16")
+    steps = _step_chain(rng, x0, n_steps, "bf16")
+    return Workload("latte_block", F, H, W, C, heads, dh, 0, "bf16", "frame_token", 0.2, 0.3, 1,
+                    steps, None, *w, t_weights=dict(wq=tw[0], wk=tw[1], wv=tw[2], wo=tw[3]),
+                    extra=dict(r_block=0.4, block_patch_k=1))
+
+
+def _svdxt_block(n_steps):
+    """SVD-XT-like spatial + temporal block at the paper's SVD-XT ratios
+    (r_f / r_b / r_t = 50 / 40 / 50 %): the SVD-XT-like level's inputs and
+    weights, token and block matching patch-local in 4x4 patches (§3.3)."""
+    wl = _svdxt(n_steps, patch_k=4)
+    wl.name = "svdxt_block"
+    wl.r, wl.r_frame = 0.5, 0.5
+    wl.extra = dict(r_block=0.4, block_patch_k=4)
+    return wl
+
+
 WORKLOADS = {
     "tok16_f32": _tok16,
     "sd3_1024": _sd3,
@@ -270,6 +298,8 @@ WORKLOADS = {
     "svdxt_level": _svdxt,
     "svdxt_level_k4": lambda n: _svdxt(n, patch_k=4),
     "svdxt_level_planted": lambda n: _svdxt(n, planted=True),
+    "latte_block": _latte_block,
+    "svdxt_block": _svdxt_block,
 }
 
 

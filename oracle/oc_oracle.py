@@ -38,6 +38,10 @@ readings (the same list, with reasons, is kept with the design notes):
   R15 The retained tokens of a pair form one attention sequence.
   R16 Text-context tokens are appended to the (single) image sequence and
       never cached.
+  R20 In a spatial + temporal block the temporal layer's input is the
+      residual x + y_spatial; each layer has its own weights and its own
+      layer cache (Frame / Token Cache on the spatial layer, Block Cache on
+      the temporal one, §3.2).
   R21 The feed-forward sublayer (cached under the same selection as the
       attention of its block, as the SD3 experiments do, §4.2 "Design
       choices") is two linear maps with a tanh-approximated GELU between
@@ -79,7 +83,7 @@ __all__ = [
     "frame_group", "pair_token_groups", "decide", "build_sequences",
     "kept_and_map", "multi_head_attention", "attn_reduced", "restore",
     "layer_step", "full_attention", "descriptors", "flatten_match",
-    "gelu_tanh", "feed_forward", "ffn_step",
+    "gelu_tanh", "feed_forward", "ffn_step", "block_step",
 ]
 
 
@@ -673,3 +677,26 @@ def ffn_step(x: np.ndarray, kept_idx: np.ndarray, restore_map: np.ndarray, w1: n
     y_kept = feed_forward(x[np.asarray(kept_idx, dtype=np.int64)], w1, w2)
     cy = None if cache_y is None else np.asarray(cache_y, dtype=np.float64).reshape(-1, w1.shape[1])
     return restore(y_kept, np.asarray(restore_map), cy)
+
+
+# ----------------------------------------------------------------------------
+# a spatial + temporal block with all three caches (R20)
+# ----------------------------------------------------------------------------
+
+def block_step(x: np.ndarray, w_spatial: Dict[str, np.ndarray], w_temporal: Dict[str, np.ndarray],
+               shape: LayerShape, spatial: CacheCfg, temporal: CacheCfg,
+               cache_s: Optional[np.ndarray], valid_s: bool, cache_t: Optional[np.ndarray], valid_t: bool,
+               forced_s: Optional[dict] = None, forced_t: Optional[dict] = None,
+               h: Optional[np.ndarray] = None) -> Tuple[StepResult, np.ndarray, StepResult]:
+    """The spatial layer (Frame / Token Cache) on x, the residual
+    h = x + y_spatial, then the temporal layer (Block Cache) on h.  ``h``,
+    when given, replaces the residual as the temporal layer's input (a
+    caller comparing a library that stores h rounded to its tensor type
+    passes that stored h, so that each layer is checked on its exact input).
+    Returns (spatial result, h, temporal result)."""
+    assert temporal.gran == BLOCK and spatial.gran != BLOCK
+    rs = layer_step(x, None, w_spatial, shape, spatial, cache_s, valid_s, forced=forced_s)
+    hh = np.asarray(x, dtype=np.float64).reshape(rs.y.shape) + rs.y if h is None else \
+        np.asarray(h, dtype=np.float64).reshape(rs.y.shape)
+    rt = layer_step(hh, None, w_temporal, shape, temporal, cache_t, valid_t, forced=forced_t)
+    return rs, hh, rt

@@ -16,6 +16,8 @@ from .api import (  # noqa: F401
     Shape,
     StageTimer,
     attn_full,
+    block_cached,
+    block_workspace,
     attn_reduced,
     attn_workspace_bytes,
     ffn_reduced,
@@ -26,6 +28,7 @@ from .api import (  # noqa: F401
     layered_schedule,
     match,
     plan,
+    residual_add,
     restore,
     select,
     static_scratch_bytes,

@@ -86,6 +86,11 @@ _SIGS = {
     "oc_layered_schedule": (C.c_int, [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_double,
                                       C.c_int32, P(oc_cache_entry), C.c_int32, P(C.c_int32), P(C.c_double),
                                       P(C.c_double)]),
+    "oc_residual_add": (C.c_int, [P(oc_shape), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]),
+    "oc_block_cached": (C.c_int, [P(oc_shape), P(oc_cfg), P(oc_cfg), C.c_void_p, P(oc_attn_weights),
+                                  P(oc_attn_weights), P(oc_cache), P(oc_cache), C.c_void_p, P(oc_trace), P(oc_trace),
+                                  C.c_void_p, C.c_size_t, C.c_void_p]),
+    "oc_block_workspace_bytes": (C.c_size_t, [P(oc_shape), P(oc_cfg), P(oc_cfg)]),
     "oc_layer_cached_static": (C.c_int, [P(oc_shape), P(oc_cfg), C.c_void_p, C.c_void_p, P(oc_attn_weights),
                                          P(oc_cache), C.c_void_p, P(oc_trace), C.c_void_p]),
     "oc_static_scratch_bytes": (C.c_size_t, []),

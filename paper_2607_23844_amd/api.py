@@ -333,6 +333,48 @@ def layered_schedule(latency, quality, target_speedup: float, interval: int, mas
     return [(out[i].layer, out[i].step, out[i].interval) for i in range(n.value)], saved.value, budget.value
 
 
+def residual_add(x: torch.Tensor, y: torch.Tensor, shape: Shape, h: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """oc_residual_add: h = x + y over [F, N, C]."""
+    _need(x, shape.torch_dtype, "x")
+    _need(y, shape.torch_dtype, "y")
+    if h is None:
+        h = torch.empty_like(x)
+    _need(h, shape.torch_dtype, "h")
+    sh = shape.c()
+    L.check(L.lib().oc_residual_add(C.byref(sh), x.data_ptr(), y.data_ptr(), h.data_ptr(), _stream(x)))
+    return h
+
+
+def block_workspace(shape: Shape, spatial: Cfg, temporal: Cfg, device) -> torch.Tensor:
+    sh, cs, ct = shape.c(), spatial.c(), temporal.c()
+    n = int(L.lib().oc_block_workspace_bytes(C.byref(sh), C.byref(cs), C.byref(ct)))
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+
+
+def block_cached(x: torch.Tensor, w_spatial: Dict[str, torch.Tensor], w_temporal: Dict[str, torch.Tensor],
+                 cache_spatial: LayerCache, cache_temporal: LayerCache, shape: Shape, spatial: Cfg, temporal: Cfg,
+                 h: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, trace: bool = False):
+    """oc_block_cached: the spatial layer (Frame / Token Cache), the residual
+    h = x + y_spatial and the temporal layer (Block Cache) in one call.
+    Returns (cache_temporal.y, h, spatial trace, temporal trace)."""
+    wsc, _, _, tr_s, out_s, c_s = _layer_args(x, w_spatial, cache_spatial, shape, spatial, None, trace)
+    wtc, _, _, tr_t, out_t, c_t = _layer_args(x, w_temporal, cache_temporal, shape, temporal, None, trace)
+    if h is None:
+        h = torch.empty_like(x)
+    _need(h, shape.torch_dtype, "h")
+    if ws is None:
+        ws = block_workspace(shape, spatial, temporal, x.device)
+    sh, cs, ct = shape.c(), spatial.c(), temporal.c()
+    L.check(L.lib().oc_block_cached(C.byref(sh), C.byref(cs), C.byref(ct), x.data_ptr(), C.byref(wsc), C.byref(wtc),
+                                    C.byref(c_s), C.byref(c_t), h.data_ptr(),
+                                    C.byref(tr_s) if tr_s is not None else None,
+                                    C.byref(tr_t) if tr_t is not None else None, ws.data_ptr(), ws.numel(),
+                                    _stream(x)))
+    cache_spatial.valid, cache_spatial.step = c_s.valid, c_s.step
+    cache_temporal.valid, cache_temporal.step = c_t.valid, c_t.step
+    return cache_temporal.y, h, out_s, out_t
+
+
 def static_scratch_bytes() -> int:
     return int(L.lib().oc_static_scratch_bytes())
 

@@ -115,6 +115,47 @@ static void launch_rows(long rows, int cpr, G4 four, G1 one) {
     else one(units, wide);
 }
 
+// Residual connection between the spatial and the temporal layer of a
+// block: h = x + y elementwise, added in fp32 and rounded once (bf16: RNE),
+// 16 bytes per operand and thread.
+__global__ void k_add_bf16(const uint4 *__restrict__ x, const uint4 *__restrict__ y, uint4 *__restrict__ h, long n8) {
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += (long)gridDim.x * blockDim.x) {
+        const uint4 a = x[i], b = y[i];
+        const uint32_t *pa = reinterpret_cast<const uint32_t *>(&a), *pb = reinterpret_cast<const uint32_t *>(&b);
+        uint4 o;
+        uint32_t *po = reinterpret_cast<uint32_t *>(&o);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float lo = __uint_as_float(pa[j] << 16) + __uint_as_float(pb[j] << 16);
+            const float hi = __uint_as_float(pa[j] & 0xFFFF0000u) + __uint_as_float(pb[j] & 0xFFFF0000u);
+            po[j] = (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+        }
+        h[i] = o;
+    }
+}
+
+__global__ void k_add_f32(const float4 *__restrict__ x, const float4 *__restrict__ y, float4 *__restrict__ h, long n4) {
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long)gridDim.x * blockDim.x) {
+        const float4 a = x[i], b = y[i];
+        h[i] = make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+    }
+}
+
+hipError_t launch_add(const Plan &p, const void *x, const void *y, void *h, hipStream_t st) {
+    StageScope _stage(st, "residual");
+    const long n = (long)p.F * p.N * p.C;
+    if (p.bf16) {
+        const long n8 = n / 8;
+        const long blocks = std::min<long>((n8 + 255) / 256, 4L * 1024);
+        launch_k(k_add_bf16, (unsigned)blocks, 256, 0, st, (const uint4 *)x, (const uint4 *)y, (uint4 *)h, n8);
+    } else {
+        const long n4 = n / 4;
+        const long blocks = std::min<long>((n4 + 255) / 256, 4L * 1024);
+        launch_k(k_add_f32, (unsigned)blocks, 256, 0, st, (const float4 *)x, (const float4 *)y, (float4 *)h, n4);
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_gather(const Plan &p, const void *x, const int32_t *kept_idx, int n_rows, void *x_kept,
                          hipStream_t st) {
     const int cpr = p.C * p.esz / 16;

@@ -578,6 +578,57 @@ oc_status oc_ffn_reduced(const oc_shape *shape, const void *x, const int32_t *ke
     return ok();
 }
 
+oc_status oc_residual_add(const oc_shape *shape, const void *x, const void *y, void *h, hipStream_t stream) {
+    oc_status s = check_shape(shape);
+    if (s != OC_OK) return s;
+    if (!x || !y || !h) return fail(OC_ERR_INVALID_ARG, "NULL pointer");
+    if (!aligned16(x) || !aligned16(y) || !aligned16(h)) return fail(OC_ERR_INVALID_ARG, "buffers must be 16-byte aligned");
+    Plan p;
+    std::memset(&p, 0, sizeof(p));
+    p.F = shape->F; p.N = shape->H * shape->W; p.C = shape->C; p.bf16 = shape->dtype == OC_BF16;
+    HIP_TRY(launch_add(p, x, y, h, stream), "residual add");
+    return ok();
+}
+
+oc_status oc_block_cached(const oc_shape *shape, const oc_cfg *spatial, const oc_cfg *temporal, const void *x,
+                          const oc_attn_weights *w_spatial, const oc_attn_weights *w_temporal, oc_cache *cache_spatial,
+                          oc_cache *cache_temporal, void *h, oc_trace *trace_spatial, oc_trace *trace_temporal,
+                          void *ws, size_t ws_bytes, hipStream_t stream) {
+    // everything is validated before the first launch
+    Plan ps, pt;
+    oc_status s;
+    if ((s = make_plan(shape, spatial, false, ps)) != OC_OK) return s;
+    if ((s = make_plan(shape, temporal, false, pt)) != OC_OK) return s;
+    if (spatial->gran == OC_GRAN_BLOCK) return fail(OC_ERR_INVALID_ARG, "the spatial layer's cache cannot be BLOCK");
+    if (temporal->gran != OC_GRAN_BLOCK) return fail(OC_ERR_INVALID_ARG, "the temporal layer's cache must be BLOCK");
+    if (shape->n_ctx != 0) return fail(OC_ERR_SHAPE, "a spatial+temporal block takes no context tokens");
+    if (!x || !h) return fail(OC_ERR_INVALID_ARG, "NULL x / h");
+    if ((s = check_weights(w_spatial)) != OC_OK || (s = check_weights(w_temporal)) != OC_OK) return s;
+    for (const oc_cache *c : {cache_spatial, cache_temporal}) {
+        if (!c || !c->y) return fail(OC_ERR_CACHE_STATE, "cache or cache->y is NULL");
+        if (c->valid != 0 && c->valid != 1) return fail(OC_ERR_CACHE_STATE, "cache->valid must be 0 or 1");
+    }
+    if (!aligned16(x) || !aligned16(h) || !aligned16(cache_spatial->y) || !aligned16(cache_temporal->y))
+        return fail(OC_ERR_INVALID_ARG, "buffers must be 16-byte aligned");
+    const void *bufs[4] = {x, h, cache_spatial->y, cache_temporal->y};
+    for (int i = 0; i < 4; ++i)
+        for (int j = i + 1; j < 4; ++j)
+            if (bufs[i] == bufs[j]) return fail(OC_ERR_INVALID_ARG, "x, h and the two caches must be distinct buffers");
+    const size_t need_s = workspace_for(shape, spatial), need_t = workspace_for(shape, temporal);
+    if ((s = check_ws(ws, ws_bytes, need_s > need_t ? need_s : need_t)) != OC_OK) return s;
+    if ((s = oc_layer_cached(shape, spatial, x, nullptr, w_spatial, cache_spatial, nullptr, trace_spatial, ws, ws_bytes,
+                             stream)) != OC_OK)
+        return s;
+    if ((s = oc_residual_add(shape, x, cache_spatial->y, h, stream)) != OC_OK) return s;
+    return oc_layer_cached(shape, temporal, h, nullptr, w_temporal, cache_temporal, nullptr, trace_temporal, ws,
+                           ws_bytes, stream);
+}
+
+size_t oc_block_workspace_bytes(const oc_shape *shape, const oc_cfg *spatial, const oc_cfg *temporal) {
+    const size_t a = workspace_for(shape, spatial), b = workspace_for(shape, temporal);
+    return a > b ? a : b;
+}
+
 oc_status oc_layer_cached_static(const oc_shape *shape, const oc_cfg *cfg, const void *x, const void *ctx,
                                  const oc_attn_weights *w, oc_cache *cache, void *y_ctx, oc_trace *trace,
                                  hipStream_t stream) {

@@ -144,6 +144,7 @@ hipError_t launch_restore(const Plan &p, const void *y_kept, int n_rows, const i
 hipError_t launch_copy_matched(const Plan &p, const int32_t *cached_idx, int n_cached,
                                const int32_t *rmap, const int32_t *kept_idx, void *y, hipStream_t st);
 hipError_t launch_fill_i32(int32_t *dst, long n, int32_t value, hipStream_t st);
+hipError_t launch_add(const Plan &p, const void *x, const void *y, void *h, hipStream_t st);
 
 // Reduced attention: rows r < n_main come from x rows (row_idx[r] if row_idx,
 // else r), rows n_main..n_main+n_ctx from ctx.  Sequence s owns rows

@@ -218,27 +218,35 @@ def check_maps(tr, kept_idx, cached_idx, restore_map):
     np.testing.assert_array_equal(tr["restore_map"].cpu().numpy(), restore_map)
 
 
+def check_layer_step(x64, ctx64, W64, osh, ocf, ora_cache, valid, y, y_ctx, tr, dtype):
+    """Checks one finished layer call (its output y, context output and
+    trace) against the oracle step on the exact input x64, with the
+    library's in-band choices forced on the oracle.  Returns the oracle's
+    StepResult and statistics."""
+    x64 = np.asarray(x64, dtype=np.float64).reshape(osh.F, osh.N, osh.C)
+    _, forced, st = decision_parity(x64, osh, ocf, tr, valid)
+    res = O.layer_step(x64, ctx64, W64, osh, ocf, ora_cache, valid, forced=forced)
+    check_maps(tr, res.kept_idx, res.cached_idx, res.restore_map)
+    yg = to_f64(y).reshape(res.y.shape)
+    err, raw = rel_err(yg, res.y, dtype), rel_err(yg, res.y)
+    if ctx64 is not None:
+        yc = to_f64(y_ctx)
+        err, raw = max(err, rel_err(yc, res.y_ctx, dtype)), max(raw, rel_err(yc, res.y_ctx))
+    check_output_bars(err, raw, dtype, "layer output")
+    st.update(err=err, err_raw=raw)
+    return res, st
+
+
 def layer_step_parity(wl, x_np, sh, cf, osh, ocf, cache, ws, ora_cache, valid, ctx_dev=None, ctx64=None,
                       W=None, W64=None):
     """One oc_layer_cached step against the oracle (with in-band forcing).
-    Returns the oracle's StepResult and the max relative error."""
+    Returns the oracle's StepResult and the statistics."""
     W = W or weights_dev(wl)
     W64 = W64 or weights_f64(wl)
     x = dev_tensor(wl, x_np)
     y, y_ctx, tr = oc.layer_cached(x, W, cache, sh, cf, ctx=ctx_dev, ws=ws, trace=True)
     torch.cuda.synchronize()
-    x64 = wl.f64(x_np).reshape(osh.F, osh.N, osh.C)
-    _, forced, st = decision_parity(x64, osh, ocf, tr, valid)
-    res = O.layer_step(x64, ctx64, W64, osh, ocf, ora_cache, valid, forced=forced)
-    check_maps(tr, res.kept_idx, res.cached_idx, res.restore_map)
-    yg = to_f64(y).reshape(res.y.shape)
-    err, raw = rel_err(yg, res.y, wl.dtype), rel_err(yg, res.y)
-    if ctx64 is not None:
-        yc = to_f64(y_ctx)
-        err, raw = max(err, rel_err(yc, res.y_ctx, wl.dtype)), max(raw, rel_err(yc, res.y_ctx))
-    check_output_bars(err, raw, wl.dtype, "layer output")
-    st.update(err=err, err_raw=raw)
-    return res, st
+    return check_layer_step(wl.f64(x_np), ctx64, W64, osh, ocf, ora_cache, valid, y, y_ctx, tr, wl.dtype)
 
 
 def sampled_outputs(x64, W64, osh, seqs, kept_idx, restore_map, positions, y_prev):
@@ -271,21 +279,26 @@ def sampled_outputs(x64, W64, osh, seqs, kept_idx, restore_map, positions, y_pre
     return out
 
 
-def layer_step_sampled_parity(wl, x_np, sh, cf, osh, ocf, cache, ws, valid, W, W64, positions, y_prev):
-    """One oc_layer_cached step of a layer too large for the full oracle:
-    decisions and maps checked in full, outputs at the sampled positions.
-    Returns the oracle values there and statistics."""
-    x = dev_tensor(wl, x_np)
-    y, _, tr = oc.layer_cached(x, W, cache, sh, cf, ws=ws, trace=True)
-    torch.cuda.synchronize()
-    x64 = wl.f64(x_np).reshape(osh.F, osh.N, osh.C)
+def check_layer_step_sampled(x64, W64, osh, ocf, valid, y, tr, positions, y_prev, dtype):
+    """Checks one finished call of a layer too large for the full oracle:
+    decisions and maps in full, outputs at the sampled positions.  Returns
+    the oracle values there and statistics."""
+    x64 = np.asarray(x64, dtype=np.float64).reshape(osh.F, osh.N, osh.C)
     dec, _, st = decision_parity(x64, osh, ocf, tr, valid)
     seqs = O.build_sequences(osh, ocf, dec)
     kept_idx, cached_idx, rmap = O.kept_and_map(osh, ocf, dec, seqs, valid)
     check_maps(tr, kept_idx, cached_idx, rmap)
     ref = sampled_outputs(x64, W64, osh, seqs, kept_idx, rmap, positions, y_prev)
     got = to_f64(y).reshape(-1, osh.C)[positions]
-    err, raw = rel_err(got, ref, wl.dtype), rel_err(got, ref)
-    check_output_bars(err, raw, wl.dtype, "sampled layer output")
+    err, raw = rel_err(got, ref, dtype), rel_err(got, ref)
+    check_output_bars(err, raw, dtype, "sampled layer output")
     st.update(err=err, err_raw=raw, n_kept=len(kept_idx), n_seq=len(seqs))
     return ref, st
+
+
+def layer_step_sampled_parity(wl, x_np, sh, cf, osh, ocf, cache, ws, valid, W, W64, positions, y_prev):
+    """One oc_layer_cached step of a layer too large for the full oracle."""
+    x = dev_tensor(wl, x_np)
+    y, _, tr = oc.layer_cached(x, W, cache, sh, cf, ws=ws, trace=True)
+    torch.cuda.synchronize()
+    return check_layer_step_sampled(wl.f64(x_np), W64, osh, ocf, valid, y, tr, positions, y_prev, wl.dtype)

@@ -591,3 +591,30 @@ def test_forced_decisions_only_change_what_they_override():
     b = O.layer_step(x, None, w, shape, cfg, None, cache_valid=False, forced=forced)
     np.testing.assert_array_equal(a.y, b.y)
     np.testing.assert_array_equal(a.restore_map, b.restore_map)
+
+
+def test_block_step_composition_and_uncached_limit():
+    """The block oracle is the spatial step, the residual and the temporal
+    step; at zero ratios it is exactly the uncached block: full spatial
+    attention per frame, the residual, full temporal attention per position."""
+    wl = small_workload(O.FRAME_TOKEN, F=5, H=8, W=8, C=16, heads=2, head_dim=8, seed=71, planted=True)
+    shape = _shape(wl)
+    x = wl.f64(wl.steps[0])
+    ws = _w(wl)
+    rng = np.random.default_rng(3)
+    wt = {k: rng.standard_normal(v.shape) / 4.0 for k, v in ws.items()}
+    sp = O.CacheCfg(O.FRAME_TOKEN, r=0.0, r_frame=0.0)
+    tp = O.CacheCfg(O.BLOCK, r=0.0)
+    rs, h, rt = O.block_step(x, ws, wt, shape, sp, tp, None, False, None, False)
+    ys, _ = O.full_attention(x, None, ws, shape)
+    np.testing.assert_array_equal(rs.y, ys)
+    np.testing.assert_array_equal(h, x.reshape(ys.shape) + ys)
+    yt, _ = O.full_attention(h, None, wt, shape, temporal=True)
+    np.testing.assert_array_equal(rt.y, yt)
+    # nonzero ratios: the temporal step sees exactly x + y_spatial
+    sp = O.CacheCfg(O.FRAME_TOKEN, r=0.5, r_frame=0.4)
+    tp = O.CacheCfg(O.BLOCK, r=0.5)
+    rs, h, rt = O.block_step(x, ws, wt, shape, sp, tp, None, False, None, False)
+    ref_t = O.layer_step(x.reshape(rs.y.shape) + rs.y, None, wt, shape, tp, None, False)
+    np.testing.assert_array_equal(rt.y, ref_t.y)
+    assert len(rs.cached_idx) > 0 and len(rt.cached_idx) > 0
