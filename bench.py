@@ -27,17 +27,34 @@ sys.path.insert(0, ROOT)
 METRIC = "cached attn-layer tokens/sec & latency vs uncached at r; MFMA % / HBM GB/s"
 PEAK_MFMA_TFLOPS = 2516.6     # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
-# Counter summary of the step's kernels (rocprofv3 FETCH_SIZE / WRITE_SIZE
-# runs, scaled by a copy kernel of known size) and the sources each was taken on.
-PROFILE = os.path.join(ROOT, "profiles", "sd3_1024_r050_kernels.md")
+# Counter summaries of each workload's kernels (rocprofv3 FETCH_SIZE /
+# WRITE_SIZE runs, scaled by a copy kernel of known size) and the sources each
+# was taken on.
+PROFILES = {
+    "sd3_1024": os.path.join(ROOT, "profiles", "sd3_1024_r050_kernels.md"),
+    "latte_spatial": os.path.join(ROOT, "profiles", "latte_spatial_frame_cache_kernels.md"),
+    "latte_temporal": os.path.join(ROOT, "profiles", "latte_temporal_block_cache_kernels.md"),
+    "svdxt_level": os.path.join(ROOT, "profiles", "svdxt_level_frame_token_cache_kernels.md"),
+    "svdxt_level_k4": os.path.join(ROOT, "profiles", "svdxt_level_k4_frame_token_cache_kernels.md"),
+    "sd3_ffn": os.path.join(ROOT, "profiles", "sd3_1024_ffn_r050_kernels.md"),
+}
+PROFILE = PROFILES["sd3_1024"]
 _COMMON = ("oc_attn_common.h", "oc_device.h")
+_TILES = ("oc_dma_tile.h", "oc_mfma_tile.h", "oc_gemm_epi.h")
 KERNEL_SOURCES = {
     "flash": ("k_flash.hip",) + _COMMON,
-    "proj_qkv": ("k_proj.hip", "oc_dma_tile.h", "oc_mfma_tile.h") + _COMMON,
-    "proj_out": ("k_proj.hip", "oc_dma_tile.h", "oc_mfma_tile.h") + _COMMON,
+    "proj_qkv": ("k_proj.hip",) + _TILES + _COMMON,
+    "proj_out": ("k_proj.hip",) + _TILES + _COMMON,
     "match": ("k_match.hip", "oc_dma_tile.h", "oc_mfma_tile.h", "oc_groups.h", "oc_device.h"),
     "select": ("k_select.hip", "oc_groups.h", "oc_block.h", "oc_device.h"),
     "inv_norm": ("k_match.hip", "oc_device.h"),
+    "frame_gram": ("k_frame.hip", "oc_device.h"),
+    "frame_final": ("k_frame.hip", "oc_device.h"),
+    "attn_short": ("k_flash.hip",) + _COMMON,
+    "qkv_attn_short": ("k_short.hip",) + _TILES + _COMMON,
+    "compact": ("k_compact.hip", "oc_groups.h", "oc_device.h"),
+    "ffn_up": ("k_ffn.hip",) + _TILES + _COMMON,
+    "ffn_down": ("k_ffn.hip",) + _TILES + _COMMON,
 }
 
 
@@ -51,11 +68,11 @@ def kernel_source_hash(stage):
     return h.hexdigest()[:16]
 
 
-def kernel_traffic(stage):
-    """HBM bytes per launch of a stage's kernel from the committed counter
-    summary, or None when there is none or its sources changed since."""
+def kernel_traffic(stage, workload="sd3_1024"):
+    """HBM bytes per launch of a stage's kernel from the workload's committed
+    counter summary, or None when there is none or its sources changed since."""
     try:
-        with open(PROFILE) as fh:
+        with open(PROFILES[workload]) as fh:
             kv = dict((k.strip(), v.strip()) for k, v in
                       (l.split(":", 1) for l in fh.read().splitlines() if l.startswith(("traffic.", "sha1."))))
         if stage not in KERNEL_SOURCES or kv[f"sha1.{stage}"] != kernel_source_hash(stage):
@@ -65,24 +82,84 @@ def kernel_traffic(stage):
         return None
 
 
-def stage_work(shape, pl, n_ctx):
-    """Algorithmic work per launch of each stage: (kind, amount, unit)."""
-    C, H, dh = shape.C, shape.heads, shape.head_dim
-    hd = H * dh
-    rows = pl.n_kept + n_ctx
+def stage_work(shape, cfg, pl, n_ctx=0):
+    """Algorithmic work per launch of each stage of one layer call:
+    {stage: (flop, bytes)}, what the method itself must compute and move
+    (bf16 operands, 2 bytes; fp32 norms).  Selection, compaction and the
+    frame-stage reductions are latency-bound and have no entry."""
+    C, hd = shape.C, shape.heads * shape.head_dim
     FN = shape.F * shape.N
+    rows = pl.n_kept + n_ctx
     lk = pl.seq_len + (n_ctx if pl.n_seq == 1 else 0)
     attn_flop = 4.0 * pl.n_seq * lk * lk * hd
     S, D, G = pl.n_src_max, pl.n_dst_max, pl.n_groups
+    K = shape.F * C if cfg.gran == "block" else C
+    frames = cfg.gran in ("frame", "frame_token")
     return {
-        "proj_qkv": ("mfma", 2.0 * rows * C * 3 * hd),
-        "flash": ("mfma", attn_flop),
-        "proj_out": ("mfma", 2.0 * rows * hd * C),
-        "match": ("mfma", 2.0 * G * S * D * C),
-        "inv_norm": ("hbm", FN * C * 2.0 + FN * 4.0),
-        "gather": ("hbm", 2.0 * pl.n_kept * C * 2.0),
-        "restore": ("hbm", 2.0 * pl.n_kept * C * 2.0),
+        "proj_qkv": (2.0 * rows * C * 3 * hd, 2.0 * (rows * C + 3 * hd * C + 3 * rows * hd)),
+        "flash": (attn_flop, 2.0 * 4 * rows * hd),
+        "attn_short": (attn_flop, 2.0 * 4 * rows * hd),
+        "qkv_attn_short": (2.0 * rows * C * 3 * hd + attn_flop, 2.0 * (rows * C + 3 * hd * C + rows * hd)),
+        "proj_out": (2.0 * rows * hd * C, 2.0 * (rows * hd + hd * C + rows * C)),
+        "match": (2.0 * G * S * D * K, 2.0 * FN * C + 4.0 * FN),
+        "inv_norm": (2.0 * FN * C, 2.0 * FN * C + 4.0 * FN),
+        "frame_gram": (2.0 * shape.F * shape.F * shape.N * C if frames else 0.0,
+                       2.0 * FN * C + (4.0 * FN if cfg.gran == "frame_token" else 0.0)),
+        "gather": (0.0, 2.0 * pl.n_kept * C * 2.0),
+        "restore": (0.0, 2.0 * pl.n_kept * C * 2.0),
+        "residual": (float(FN * C), 3.0 * FN * C * 2.0),
     }
+
+
+def roofline_of(flop, nbytes, avg_us):
+    """Bound (the resource whose ideal time is longer), achieved rate and
+    fraction of MI355X peak for one launch of avg_us."""
+    t_mfma = flop / (PEAK_MFMA_TFLOPS * 1e12)
+    t_hbm = nbytes / (PEAK_HBM_GBS * 1e9)
+    sec = avg_us * 1e-6
+    if t_mfma >= t_hbm and flop > 0:
+        ach = flop / sec / 1e12
+        return dict(bound="mfma", achieved=round(ach, 2), peak=PEAK_MFMA_TFLOPS, unit="TFLOP/s",
+                    frac=round(ach / PEAK_MFMA_TFLOPS, 4))
+    ach = nbytes / sec / 1e9
+    return dict(bound="hbm", achieved=round(ach, 1), peak=PEAK_HBM_GBS, unit="GB/s", frac=round(ach / PEAK_HBM_GBS, 4))
+
+
+def kernel_table(stages, K, work, workload):
+    """Per-stage live timing (HIP events stamped at each kernel's start and
+    end) with its roofline where the stage has algorithmic work, and the
+    roofline object of the dominant stage (largest time)."""
+    kernels = {}
+    for name, (tot_ms, n) in stages.items():
+        avg_us = tot_ms * 1e3 / max(n, 1)
+        d = dict(avg_us=round(avg_us, 3), launches_per_step=round(n / K, 3))
+        tr = kernel_traffic(name, workload)
+        if tr is not None:
+            d["traffic"] = tr
+        if name in work and (work[name][0] > 0 or work[name][1] > 0):
+            d.update(roofline_of(work[name][0], work[name][1], avg_us))
+        kernels[name] = d
+    dom = max(stages, key=lambda s: stages[s][0])
+    roof = None
+    if dom in work:
+        avg_us = stages[dom][0] * 1e3 / max(stages[dom][1], 1)
+        flop, nbytes = work[dom]
+        roof = dict(kernel=dom, **roofline_of(flop, nbytes, avg_us), traffic=kernel_traffic(dom, workload),
+                    avg_us=round(avg_us, 3),
+                    algorithmic_per_launch=flop if roofline_of(flop, nbytes, avg_us)["bound"] == "mfma" else nbytes)
+    return kernels, roof
+
+
+def stage_times(fn, inputs, K):
+    """{stage: (total ms, launches)} over K calls, with the stage timer attached."""
+    import torch
+    import paper_2607_23844_amd as oc
+    timer = oc.StageTimer()
+    with timer:
+        for i in range(K):
+            fn(inputs[i % len(inputs)])
+    torch.cuda.synchronize()
+    return timer.collect()
 
 
 def step_percentiles(fn, inputs, K):
@@ -141,12 +218,18 @@ def timed_ms(fn, inputs, K, W):
     return e0.elapsed_time(e1) / K
 
 
+def _bf16_dev(a, dev):
+    import numpy as np
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+
 def run_other_configs(args):
     """The Latte-like spatial (Frame Cache) and temporal (Block Cache) layers
     and the SVD-XT-like level (Frame+Token spatial layer with whole-frame or
     patch-local token matching, uncached temporal layer): warm cached latency
-    against the uncached layer."""
-    import numpy as np
+    against the uncached layer, each kernel's live time, and the roofline of
+    the layer's dominant kernel."""
     import torch
     import paper_2607_23844_amd as oc
     from paper_2607_23844_amd.runner import FullRunner, LayerRunner
@@ -160,13 +243,11 @@ def run_other_configs(args):
     for key, name in (("latte_spatial_frame_cache", "latte_spatial"), ("latte_temporal_block_cache", "latte_temporal"),
                       ("svdxt_level_frame_token_cache", "svdxt_level"),
                       ("svdxt_level_frame_token_cache_k4", "svdxt_level_k4")):
+        if args.only and args.only != name:
+            continue
         wl = make_workload(name, 3)
-
-        def t(a):
-            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
-
-        xs = [t(s) for s in wl.steps]
-        W = {k: t(getattr(wl, k)) for k in ("wq", "wk", "wv", "wo")}
+        xs = [_bf16_dev(s, dev) for s in wl.steps]
+        W = {k: _bf16_dev(getattr(wl, k), dev) for k in ("wq", "wk", "wv", "wo")}
         shape = oc.Shape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, 0, "bf16")
         cfg = oc.Cfg(wl.gran, r=wl.r, r_frame=wl.r_frame, patch_k=wl.patch_k)
         full = FullRunner(shape, oc.Cfg(wl.gran, 0.0, 0.0, 1), W, dev)
@@ -174,15 +255,17 @@ def run_other_configs(args):
         run = LayerRunner(shape, cfg, W, dev)
         run(xs[0])
         ms = timed_ms(run, xs[1:], K, Wm)
+        stages = stage_times(run, xs[1:], K)
         pl = oc.plan(shape, cfg)
+        kernels, roof = kernel_table(stages, K, stage_work(shape, cfg, pl), name)
         tokens = wl.F * wl.H * wl.W
         d = dict(workload=f"F={wl.F}, {wl.H}x{wl.W} tokens, C={wl.C}, {wl.heads}x{wl.head_dim}, bf16, {wl.gran} "
                           f"r={wl.r} r_frame={wl.r_frame} patch_k={wl.patch_k}",
                  cached_us=round(ms * 1e3, 2), uncached_us=round(full_ms * 1e3, 2),
                  speedup_vs_uncached=round(full_ms / ms, 4), tokens_per_s=round(tokens / (ms * 1e-3), 1),
-                 retained_tokens=pl.n_kept, sequences=f"{pl.n_seq}x{pl.seq_len}")
+                 retained_tokens=pl.n_kept, sequences=f"{pl.n_seq}x{pl.seq_len}", roofline=roof, kernels=kernels)
         if wl.t_weights is not None:
-            TW = {k: t(v) for k, v in wl.t_weights.items()}
+            TW = {k: _bf16_dev(v, dev) for k, v in wl.t_weights.items()}
             temporal = FullRunner(shape, oc.Cfg("block", 0.0, 0.0, 1), TW, dev)
             t_ms = timed_ms(temporal, xs, K, Wm)
             d.update(temporal_layer_us=round(t_ms * 1e3, 2),
@@ -192,6 +275,165 @@ def run_other_configs(args):
         out[key] = d
         del run, full, xs, W
         torch.cuda.empty_cache()
+    return out
+
+
+def run_ffn(args):
+    """The feed-forward sublayer of the SD3-like block under the attention's
+    selection at r = 0.5 (2048 of 4096 image tokens, hidden 4C = 6144): the
+    cached FFN (retained rows only, written in place) against the uncached
+    one (every token), each kernel's live time and roofline."""
+    import torch
+    import paper_2607_23844_amd as oc
+    from paper_2607_23844_amd.runner import FfnRunner, LayerRunner
+    from oc_synth import ffn_weights, make_workload
+
+    dev = torch.device("cuda:0")
+    K, Wm = args.cfg_steps, 3
+    wl = make_workload("sd3_1024", 2)
+    shape = oc.Shape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, wl.n_ctx, "bf16")
+    cfg = oc.Cfg("token", r=0.5)
+    xs = [_bf16_dev(s, dev) for s in wl.steps]
+    W = {k: _bf16_dev(getattr(wl, k), dev) for k in ("wq", "wk", "wv", "wo")}
+    ctx = _bf16_dev(wl.ctx, dev)
+    hidden = 4 * wl.C
+    Wf = {k: _bf16_dev(v, dev) for k, v in ffn_weights(wl.C, hidden, "bf16").items()}
+    attn = LayerRunner(shape, cfg, W, dev, ctx)
+    attn(xs[0])
+    _, _, tr = oc.layer_cached(xs[1], W, attn.cache, shape, cfg, ctx=ctx, ws=attn.ws, trace=True)
+    kept = tr["kept_idx"].clone()
+    cached = FfnRunner(shape, Wf, kept, dev)
+    full = FfnRunner(shape, Wf, None, dev)
+    ms = timed_ms(cached, xs, K, Wm)
+    full_ms = timed_ms(full, xs, K, Wm)
+    stages = stage_times(cached, xs, K)
+    n, C = kept.numel(), wl.C
+    work = {"ffn_up": (2.0 * n * C * hidden, 2.0 * (n * C + hidden * C + n * hidden)),
+            "ffn_down": (2.0 * n * hidden * C, 2.0 * (n * hidden + C * hidden + n * C))}
+    kernels, roof = kernel_table(stages, K, work, "sd3_ffn")
+    return dict(workload=f"SD3-1024-like FFN: 4096 image tokens, C={C}, hidden {hidden}, GELU (tanh), bf16, the "
+                         f"attention's r=0.5 selection ({n} retained rows)",
+                cached_us=round(ms * 1e3, 2), uncached_us=round(full_ms * 1e3, 2),
+                speedup_vs_uncached=round(full_ms / ms, 4), retained_rows=n, roofline=roof, kernels=kernels)
+
+
+def run_blocks(args):
+    """Spatial + temporal blocks with all three caches at the paper's
+    operating points (Latte r_f/r_b/r_t = 30/40/20, SVD-XT 50/40/50, the
+    latter with patch-local 4x4 token and block matching), four denoising
+    steps: the first cold, the rest warm, against the uncached block."""
+    import torch
+    import paper_2607_23844_amd as oc
+    from paper_2607_23844_amd.runner import BlockRunner, FullBlockRunner
+    from oc_synth import make_workload
+
+    dev = torch.device("cuda:0")
+    K = args.cfg_steps
+    out = {}
+    for name in ("latte_block", "svdxt_block"):
+        if args.only and args.only != name:
+            continue
+        wl = make_workload(name, 4)
+        xs = [_bf16_dev(s, dev) for s in wl.steps]
+        Ws = {k: _bf16_dev(getattr(wl, k), dev) for k in ("wq", "wk", "wv", "wo")}
+        Wt = {k: _bf16_dev(v, dev) for k, v in wl.t_weights.items()}
+        shape = oc.Shape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, 0, "bf16")
+        cs = oc.Cfg(wl.gran, r=wl.r, r_frame=wl.r_frame, patch_k=wl.patch_k)
+        ct = oc.Cfg("block", r=wl.extra["r_block"], patch_k=wl.extra["block_patch_k"])
+        full = FullBlockRunner(shape, Ws, Wt, dev)
+        full_ms = timed_ms(full, xs, K, 3)
+        run = BlockRunner(shape, cs, ct, Ws, Wt, dev)
+        # the four-step chain, each step timed alone (the first is cold)
+        chain_us = []
+        for rep in range(3):
+            run.reset()
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+            torch.cuda.synchronize()
+            e[0].record()
+            for s in range(4):
+                run(xs[s])
+                e[s + 1].record()
+            torch.cuda.synchronize()
+            chain_us.append([e[i].elapsed_time(e[i + 1]) * 1e3 for i in range(4)])
+        steps_us = [round(sorted(c[i] for c in chain_us)[1], 2) for i in range(4)]
+        warm_ms = timed_ms(run, xs[1:], K, 3)
+        stages = stage_times(run, xs[1:], K)
+        kernels = {k: dict(avg_us=round(v[0] * 1e3 / max(v[1], 1), 3), launches_per_step=round(v[1] / K, 3))
+                   for k, v in stages.items()}
+        ps, pt = oc.plan(shape, cs), oc.plan(shape, ct)
+        out[name] = dict(
+            workload=f"F={wl.F}, {wl.H}x{wl.W} tokens, C={wl.C}, {wl.heads}x{wl.head_dim}, bf16; spatial "
+                     f"{wl.gran} r_f={wl.r_frame} r_t={wl.r} k={wl.patch_k}, temporal block r_b="
+                     f"{wl.extra['r_block']} k={wl.extra['block_patch_k']}",
+            steps_us=steps_us, warm_us=round(warm_ms * 1e3, 2), uncached_us=round(full_ms * 1e3, 2),
+            speedup_warm=round(full_ms / warm_ms, 4),
+            speedup_4_steps=round(4 * full_ms * 1e3 / sum(steps_us), 4),
+            spatial_retained=f"{ps.n_seq}x{ps.seq_len}", temporal_retained=f"{pt.n_seq}x{pt.seq_len}",
+            kernels=kernels)
+        del run, full, xs, Ws, Wt
+        torch.cuda.empty_cache()
+    return out
+
+
+def run_k_sweep(args):
+    """Token-group count at the SD3-like shape (k x k patches, k = 1, 2, 4, 8:
+    1 to 64 groups per frame, §3.3 and App. A's group counts): the step and
+    its bookkeeping kernels (norms, similarity, selection) and the standalone
+    gather and restore entry points, r = 0.5."""
+    import torch
+    import paper_2607_23844_amd as oc
+    from paper_2607_23844_amd.runner import LayerRunner
+    from oc_synth import make_workload
+
+    dev = torch.device("cuda:0")
+    K = args.cfg_steps
+    wl = make_workload("sd3_1024", 3)
+    shape = oc.Shape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, wl.n_ctx, "bf16")
+    xs = [_bf16_dev(s, dev) for s in wl.steps]
+    W = {k: _bf16_dev(getattr(wl, k), dev) for k in ("wq", "wk", "wv", "wo")}
+    ctx = _bf16_dev(wl.ctx, dev)
+    out = {}
+    for k in (1, 2, 4, 8):
+        cfg = oc.Cfg("token", r=0.5, patch_k=k)
+        run = LayerRunner(shape, cfg, W, dev, ctx)
+        run(xs[0])
+        ms = timed_ms(run, xs[1:], K, 3)
+        st = stage_times(run, xs[1:], K)
+        pl = oc.plan(shape, cfg)
+        _, _, tr = oc.layer_cached(xs[1], W, run.cache, shape, cfg, ctx=ctx, ws=run.ws, trace=True)
+        kept, rmap = tr["kept_idx"], tr["restore_map"]
+        y_kept = torch.empty((kept.numel(), shape.C), dtype=torch.bfloat16, device=dev)
+        y_out = torch.empty_like(run.cache.y)
+        mv = stage_times(lambda _x: (oc.gather(xs[2], kept, shape, cfg),
+                                     oc.restore(y_kept, rmap, shape, cache_y=y_out, y=y_out)), [None], K)
+
+        def us(d, name):
+            return round(d[name][0] * 1e3 / max(d[name][1], 1), 3) if name in d else None
+
+        out[str(k)] = dict(groups=pl.n_groups, candidates_per_group=pl.n_src_max, reps_per_group=pl.n_dst_max,
+                           step_us=round(ms * 1e3, 2), inv_norm_us=us(st, "inv_norm"), match_us=us(st, "match"),
+                           select_us=us(st, "select"), compact_us=us(st, "compact"),
+                           gather_us=us(mv, "gather"), restore_us=us(mv, "restore"),
+                           match_gflop=round(2.0 * pl.n_groups * pl.n_src_max * pl.n_dst_max * wl.C / 1e9, 3))
+        del run
+    return out
+
+
+def run_layered(args):
+    """Layered Cache schedule proposal (Alg. 1) on SD3-shaped synthetic
+    tables (24 blocks x 28 steps): host time of oc_layered_schedule and the
+    schedule it returns at the paper's SD3 speed-ups."""
+    import paper_2607_23844_amd as oc
+    from oc_synth import layered_tables
+    lat, qual = layered_tables()
+    out = {}
+    for s_r in (1.2, 1.35, 1.75, 2.32):
+        t0 = time.perf_counter()
+        for _ in range(20):
+            chosen, saved, budget = oc.layered_schedule(lat, qual, s_r, 2)
+        dt = (time.perf_counter() - t0) / 20
+        out[str(s_r)] = dict(pairs_cached=len(chosen), of_pairs=int(lat.size), saved=round(saved, 4),
+                             budget=round(budget, 4), host_us=round(dt * 1e6, 1))
     return out
 
 
@@ -310,75 +552,98 @@ def run_gpu(args):
     # (the per-kernel loop below is the last use of these kernels at this
     # shape, so a profiler trace can pick out exactly its launches)
     # live per-kernel timing: HIP events stamped by the runtime at each kernel's start and end
-    timer = oc.StageTimer()
-    with timer:
-        for i in range(K):
-            run(xs[1 + i % 3])
-    torch.cuda.synchronize()
-    stages = timer.collect()
+    stages = stage_times(run, xs[1:4], K)
     pl = oc.plan(shape, cfg)
-    work = stage_work(shape, pl, shape.n_ctx)
-    kernels = {}
-    for name, (tot_ms, n) in stages.items():
-        avg_us = tot_ms * 1e3 / max(n, 1)
-        d = dict(avg_us=round(avg_us, 3), launches_per_step=n / K)
-        tr = kernel_traffic(name)
-        if tr is not None:
-            d["traffic"] = tr
-        if name in work:
-            kind, amount = work[name]
-            if kind == "mfma":
-                ach = amount / (avg_us * 1e-6) / 1e12
-                d.update(bound="mfma", achieved_tflops=round(ach, 2), frac=round(ach / PEAK_MFMA_TFLOPS, 4))
-            else:
-                ach = amount / (avg_us * 1e-6) / 1e9
-                d.update(bound="hbm", achieved_gbs=round(ach, 1), frac=round(ach / PEAK_HBM_GBS, 4))
-        kernels[name] = d
-    dom = max(stages, key=lambda s: stages[s][0])
-    dom_avg_us = stages[dom][0] * 1e3 / stages[dom][1]
-    roof = None
-    traffic = kernel_traffic(dom)
-    if dom in work:
-        kind, amount = work[dom]
-        if kind == "mfma":
-            ach = amount / (dom_avg_us * 1e-6) / 1e12
-            roof = dict(kernel=dom, bound="mfma", achieved=round(ach, 2), peak=PEAK_MFMA_TFLOPS, unit="TFLOP/s",
-                        frac=round(ach / PEAK_MFMA_TFLOPS, 4), traffic=traffic, avg_us=round(dom_avg_us, 3),
-                        algorithmic_per_launch=amount)
-        else:
-            ach = amount / (dom_avg_us * 1e-6) / 1e9
-            roof = dict(kernel=dom, bound="hbm", achieved=round(ach, 1), peak=PEAK_HBM_GBS, unit="GB/s",
-                        frac=round(ach / PEAK_HBM_GBS, 4), traffic=traffic, avg_us=round(dom_avg_us, 3),
-                        algorithmic_per_launch=amount)
+    kernels, roof = kernel_table(stages, K, stage_work(shape, cfg, pl, shape.n_ctx), "sd3_1024")
     return dict(ms=ms, wall=wall, tokens=tokens, full_ms=full_ms, by_r=by_r, kernels=kernels, roofline=roof,
                 plan=dict(n_kept=pl.n_kept, n_cached=pl.n_cached, seq_len=pl.seq_len), pct=pct, graph_us=graph_us,
                 moves=moves)
 
 
-def run_cpu_baseline(args):
-    """The CPU oracle, unchanged, single-threaded, on a bounded sample: a cold
-    step then warm steps of the same layer."""
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def run_cpu_baselines(args):
+    """The CPU oracle, unchanged, on one thread pinned to one core: a cold step
+    (no layer cache) and a warm step of each workload, the median of three
+    runs (C1-C4).  The SVD-XT-sized level (C5) is timed on a bounded sample:
+    its decisions in full (patch-local matching, k = 4), then the attention
+    of one of its sequences, scaled to all of them.  The headline figure is
+    the SD3-like layer's warm step."""
+    import statistics
     from threadpoolctl import threadpool_limits
     from oc_synth import make_workload
     from oracle import oc_oracle as O
 
-    wl = make_workload("sd3_1024", 1 + args.cpu_steps)
-    sh = O.LayerShape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, wl.n_ctx)
-    cf = O.CacheCfg("token", r=args.r)
-    W = {k: wl.f64(getattr(wl, k)) for k in ("wq", "wk", "wv", "wo")}
-    ctx = wl.f64(wl.ctx)
+    try:
+        os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[-1]})
+        pinned = True
+    except (AttributeError, OSError):
+        pinned = False
+    out = {}
+    reps = args.cpu_reps
     with threadpool_limits(1):
-        r0 = O.layer_step(wl.f64(wl.steps[0]), ctx, W, sh, cf, None, False)
+        for key, name in (("C1_tok16_f32", "tok16_f32"), ("C2_sd3_1024", "sd3_1024"),
+                          ("C3_latte_spatial", "latte_spatial"), ("C4_latte_temporal", "latte_temporal")):
+            wl = make_workload(name, 2)
+            sh = O.LayerShape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, wl.n_ctx)
+            cf = O.CacheCfg(wl.gran, r=wl.r, r_frame=wl.r_frame, patch_k=wl.patch_k)
+            W = {k: wl.f64(getattr(wl, k)) for k in ("wq", "wk", "wv", "wo")}
+            ctx = wl.f64(wl.ctx) if wl.n_ctx else None
+            x0, x1 = wl.f64(wl.steps[0]), wl.f64(wl.steps[1])
+            cold, warm = [], []
+            for _ in range(reps):
+                t0 = time.perf_counter()
+                r0 = O.layer_step(x0, ctx, W, sh, cf, None, False)
+                t1 = time.perf_counter()
+                O.layer_step(x1, ctx, W, sh, cf, r0.y, True)
+                t2 = time.perf_counter()
+                cold.append(t1 - t0)
+                warm.append(t2 - t1)
+            tokens = wl.F * wl.N + wl.n_ctx
+            c, w = statistics.median(cold), statistics.median(warm)
+            out[key] = dict(cold_s=round(c, 4), warm_s=round(w, 4), tokens_per_s=round(tokens / w, 2),
+                            runs=reps, tokens_per_step=tokens)
+        # C5: bounded sample
+        wl = make_workload("svdxt_level_k4", 2)
+        sh = O.LayerShape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim)
+        cf = O.CacheCfg(wl.gran, r=wl.r, r_frame=wl.r_frame, patch_k=wl.patch_k)
+        W = {k: wl.f64(getattr(wl, k)) for k in ("wq", "wk", "wv", "wo")}
+        x = wl.f64(wl.steps[1]).reshape(wl.F, wl.N, wl.C)
         t0 = time.perf_counter()
-        cache = r0.y
-        for s in range(1, 1 + args.cpu_steps):
-            cache = O.layer_step(wl.f64(wl.steps[s]), ctx, W, sh, cf, cache, True).y
-        dt = (time.perf_counter() - t0) / args.cpu_steps
-    tokens = wl.F * wl.N + wl.n_ctx
-    return dict(value=round(tokens / dt, 2), unit="tokens/s", cores=1, kind="oracle",
-                sample=f"{args.cpu_steps} warm steps of the full layer (4096+333 tokens, r={args.r}), fp64 NumPy, "
-                       f"one thread; {dt:.2f} s per step; host has {os.cpu_count()} logical CPUs "
-                       f"({platform.processor() or platform.machine()})")
+        dec = O.decide(x, sh, cf)
+        seqs = O.build_sequences(sh, cf, dec)
+        kept, _, rmap = O.kept_and_map(sh, cf, dec, seqs, True)
+        t1 = time.perf_counter()
+        X = x.reshape(-1, wl.C)[seqs[0]]
+        O.multi_head_attention(X, W["wq"], W["wk"], W["wv"], W["wo"], wl.heads, wl.head_dim)
+        t2 = time.perf_counter()
+        step = (t1 - t0) + len(seqs) * (t2 - t1)
+        tokens = wl.F * wl.N
+        out["C5_svdxt_level_k4"] = dict(
+            warm_s_estimated=round(step, 3), tokens_per_s=round(tokens / step, 2), decisions_s=round(t1 - t0, 3),
+            one_sequence_s=round(t2 - t1, 3), sequences=len(seqs),
+            sample="decisions in full (frame stage, pairing, token matching in 4x4 patches, selection, maps), then "
+                   f"the attention of 1 of the {len(seqs)} sequences of {len(seqs[0])} tokens, scaled to all; the "
+                   "cold step differs only in its restore map (the same work)")
+    head = out["C2_sd3_1024"]
+    return dict(value=head["tokens_per_s"], unit="tokens/s", cores=1, kind="oracle",
+                sample=f"median of {reps} warm steps of the full SD3-like layer (4096+333 tokens, r=0.5), fp64 NumPy, "
+                       f"one thread{' pinned to one core' if pinned else ''}; {head['warm_s']:.2f} s per step; "
+                       f"1 of {os.cpu_count()} logical CPUs of the host ({_cpu_model()})",
+                configs=out)
+
+
+ONLY = ("sd3_1024", "latte_spatial", "latte_temporal", "svdxt_level", "svdxt_level_k4", "sd3_ffn", "latte_block",
+        "svdxt_block", "k_sweep")
 
 
 def main():
@@ -387,10 +652,13 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--r", type=float, default=0.5)
-    ap.add_argument("--cpu-steps", type=int, default=2)
-    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-reps", type=int, default=3, help="runs of each CPU oracle step (median)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baselines")
     ap.add_argument("--cfg-steps", type=int, default=20, help="timed steps per additional configuration")
-    ap.add_argument("--no-configs", action="store_true", help="skip the Latte and SVD-XT configurations")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip everything but the SD3-like layer (Latte, SVD-XT, FFN, blocks, group sweep)")
+    ap.add_argument("--only", choices=ONLY, default=None,
+                    help="run one workload's GPU measurement alone and print its result (for per-workload profiles)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first run a plain 256 MiB read + 256 MiB write elementwise kernel (counter calibration)")
     args = ap.parse_args()
@@ -406,11 +674,21 @@ def main():
             torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
         del src, dst
+    if args.only and args.only != "sd3_1024":
+        fn = {"sd3_ffn": run_ffn, "latte_block": run_blocks, "svdxt_block": run_blocks, "k_sweep": run_k_sweep}.get(
+            args.only, run_other_configs)
+        print(json.dumps({"only": args.only, "result": fn(args)}))
+        return
     g = run_gpu(args)
-    others = None if args.no_configs else run_other_configs(args)
-    if not args.no_configs:
+    extra = {}
+    if not args.no_configs and not args.only:
+        extra["other_configs"] = run_other_configs(args)
         g["moves"]["svdxt_level"] = run_data_movement_svdxt(args)
-    cpu = None if args.no_cpu else run_cpu_baseline(args)
+        extra["ffn_sd3"] = run_ffn(args)
+        extra["blocks"] = run_blocks(args)
+        extra["group_count_sweep_sd3"] = run_k_sweep(args)
+        extra["layered_schedule"] = run_layered(args)
+    cpu = None if (args.no_cpu or args.only) else run_cpu_baselines(args)
     ms = g["ms"]
     line = {
         "metric": METRIC,
@@ -441,7 +719,7 @@ def main():
         "roofline": g["roofline"],
         "kernels": g["kernels"],
         "data_movement": g["moves"],
-        "other_configs": others,
+        **extra,
         "paper_context": "model-level latency cuts of up to 35% / 25% / 28% (SD3 / SVD-XT / Latte) on one A100 40 GB, "
                          "precision not stated; no per-layer figure is published",
         "cpu_baseline": cpu,

@@ -79,3 +79,84 @@ class FullRunner:
         if st != 0:
             L.check(st)
         return self.y
+
+
+class BlockRunner:
+    """oc_block_cached (spatial layer with Frame / Token Cache, residual,
+    temporal layer with Block Cache) on fixed shapes, weights and caches."""
+
+    def __init__(self, shape: Shape, spatial: Cfg, temporal: Cfg, w_spatial: Dict[str, torch.Tensor],
+                 w_temporal: Dict[str, torch.Tensor], device):
+        from .api import block_workspace
+        self._ws_, self._wt_ = _weights(w_spatial, shape), _weights(w_temporal, shape)
+        self.weights = (w_spatial, w_temporal)
+        self.cache_s, self.cache_t = LayerCache(shape, device), LayerCache(shape, device)
+        self.h = torch.empty((shape.F, shape.N, shape.C), dtype=shape.torch_dtype, device=device)
+        self.ws = block_workspace(shape, spatial, temporal, device)
+        self._sh, self._cs, self._ct = shape.c(), spatial.c(), temporal.c()
+        self._c_s = L.oc_cache(self.cache_s.y.data_ptr(), 0, 0)
+        self._c_t = L.oc_cache(self.cache_t.y.data_ptr(), 0, 0)
+        self._fn = L.lib().oc_block_cached
+        self._tail = (C.byref(self._ws_), C.byref(self._wt_), C.byref(self._c_s), C.byref(self._c_t),
+                      self.h.data_ptr(), None, None, self.ws.data_ptr(), self.ws.numel(), _stream(self.h))
+
+    def reset(self):
+        for c in (self._c_s, self._c_t):
+            c.valid = 0
+            c.step = 0
+
+    def __call__(self, x: torch.Tensor) -> torch.Tensor:
+        st = self._fn(C.byref(self._sh), C.byref(self._cs), C.byref(self._ct), x.data_ptr(), *self._tail)
+        if st != 0:
+            L.check(st)
+        self.cache_s.valid, self.cache_s.step = self._c_s.valid, self._c_s.step
+        self.cache_t.valid, self.cache_t.step = self._c_t.valid, self._c_t.step
+        return self.cache_t.y
+
+
+class FullBlockRunner:
+    """The uncached block: full spatial attention, residual, full temporal
+    attention (oc_attn_full, oc_residual_add, oc_attn_full)."""
+
+    def __init__(self, shape: Shape, w_spatial: Dict[str, torch.Tensor], w_temporal: Dict[str, torch.Tensor],
+                 device):
+        self.spatial = FullRunner(shape, Cfg("token", 0.0), w_spatial, device)
+        self.temporal = FullRunner(shape, Cfg("block", 0.0), w_temporal, device)
+        self.h = torch.empty((shape.F, shape.N, shape.C), dtype=shape.torch_dtype, device=device)
+        self._sh = shape.c()
+        self._add = L.lib().oc_residual_add
+        self._stream = _stream(self.h)
+
+    def __call__(self, x: torch.Tensor) -> torch.Tensor:
+        ys = self.spatial(x)
+        st = self._add(C.byref(self._sh), x.data_ptr(), ys.data_ptr(), self.h.data_ptr(), self._stream)
+        if st != 0:
+            L.check(st)
+        return self.temporal(self.h)
+
+
+class FfnRunner:
+    """oc_ffn_reduced on fixed weights: rows kept_idx (None: every token)
+    written in place into y."""
+
+    def __init__(self, shape: Shape, weights: Dict[str, torch.Tensor], kept_idx: Optional[torch.Tensor], device):
+        from .api import ffn_workspace_bytes
+        w1, w2 = weights["w1"], weights["w2"]
+        self.hidden = w1.shape[0]
+        self.kept = kept_idx
+        self.n = kept_idx.numel() if kept_idx is not None else shape.F * shape.N
+        self.y = torch.empty((shape.F, shape.N, shape.C), dtype=shape.torch_dtype, device=device)
+        self.ws = torch.empty(max(ffn_workspace_bytes(shape, self.hidden, self.n), 256), dtype=torch.uint8,
+                              device=device)
+        self._fw = L.oc_ffn_weights(w1.data_ptr(), w2.data_ptr(), self.hidden, 0)
+        self.weights = weights
+        self._sh = shape.c()
+        self._fn = L.lib().oc_ffn_reduced
+        self._idx = kept_idx.data_ptr() if kept_idx is not None else None
+        self._tail = (C.byref(self._fw), self.y.data_ptr(), 1, self.ws.data_ptr(), self.ws.numel(), _stream(self.y))
+
+    def __call__(self, x: torch.Tensor) -> torch.Tensor:
+        st = self._fn(C.byref(self._sh), x.data_ptr(), self._idx, self.n, *self._tail)
+        if st != 0:
+            L.check(st)
+        return self.y
