@@ -38,6 +38,17 @@ readings (the same list, with reasons, is kept with the design notes):
   R15 The retained tokens of a pair form one attention sequence.
   R16 Text-context tokens are appended to the (single) image sequence and
       never cached.
+  R17 Frame Cache with k x k patches (§3.3: the frames are cut into k x k
+      patches and the frame set of every patch is matched on its own, the
+      batch becoming B*k*k): each patch is a group whose items are the
+      frames' tiles of that patch (a tile's descriptor is its tokens'
+      features in row-major order, its id the global id of its top-left
+      token); odd frames' tiles are candidates, even frames' tiles
+      representatives, and each patch caches R = min(floor(r_f F), F/2)
+      tiles.  The tokens of a cached tile skip the spatial layer; each
+      frame's retained tokens form its attention sequence, whose length
+      varies from frame to frame (it may be empty).  k = 1 is the whole-frame
+      Frame Cache.
   R20 In a spatial + temporal block the temporal layer's input is the
       residual x + y_spatial; each layer has its own weights and its own
       layer cache (Frame / Token Cache on the spatial layer, Block Cache on
@@ -83,7 +94,8 @@ __all__ = [
     "frame_group", "pair_token_groups", "decide", "build_sequences",
     "kept_and_map", "multi_head_attention", "attn_reduced", "restore",
     "layer_step", "full_attention", "descriptors", "flatten_match",
-    "gelu_tanh", "feed_forward", "ffn_step", "block_step",
+    "gelu_tanh", "feed_forward", "ffn_step", "block_step", "frame_patch_groups", "tile_tokens",
+    "tile_descriptors", "attn_reduced_varlen",
 ]
 
 
@@ -280,6 +292,32 @@ def frame_group(shape: LayerShape, ratio: float) -> Group:
     return Group(items, dst, src, skip_count(ratio, len(items), len(src)), "frame")
 
 
+def frame_patch_groups(shape: LayerShape, k: int, ratio: float) -> List[Group]:
+    """Frame Cache on k x k patches (R17): one group per patch, items are the
+    frames' tiles of the patch identified by their top-left token."""
+    N, W = shape.N, shape.W
+    h, w = shape.H // k, shape.W // k
+    out = []
+    for py in range(k):
+        for px in range(k):
+            tl = py * h * W + px * w
+            items = [f * N + tl for f in range(shape.F)]
+            dst = [f * N + tl for f in range(shape.F) if f % 2 == 0]
+            src = [f * N + tl for f in range(shape.F) if f % 2 == 1]
+            out.append(Group(items, dst, src, skip_count(ratio, shape.F, len(src)), "frame_patch"))
+    return out
+
+
+def tile_tokens(shape: LayerShape, k: int, tl: int) -> List[int]:
+    """Global ids of the tokens of the k x k patch tile whose top-left token
+    is tl, in row-major order."""
+    N, W = shape.N, shape.W
+    h, w = shape.H // k, shape.W // k
+    f, n = divmod(tl, N)
+    y0, x0 = divmod(n, W)
+    return [f * N + (y0 + y) * W + (x0 + x) for y in range(h) for x in range(w)]
+
+
 def pair_token_groups(shape: LayerShape, k: int, s: int, d: int, ratio: float) -> List[Group]:
     """Token Cache inside a matched frame pair (§3.2.3): the two frames' tokens
     of a patch form one group; each 2x2x2 cube keeps the top-left token of
@@ -316,8 +354,19 @@ def descriptors(x: np.ndarray, kind: str, ids: Sequence[int]) -> np.ndarray:
     raise ValueError(kind)
 
 
-def _match_group(x: np.ndarray, g: Group):
-    S = cosine_matrix(descriptors(x, g.kind, g.src), descriptors(x, g.kind, g.dst))
+def tile_descriptors(x: np.ndarray, shape: LayerShape, k: int, ids: Sequence[int]) -> np.ndarray:
+    """Frame-patch tiles (R17): the tile's tokens' features concatenated in
+    row-major order."""
+    xf = x.reshape(-1, x.shape[-1])
+    return np.stack([xf[tile_tokens(shape, k, t)].reshape(-1) for t in ids]) if len(ids) else \
+        np.zeros((0, x.shape[-1]))
+
+
+def _match_group(x: np.ndarray, g: Group, shape: Optional[LayerShape] = None, k: int = 1):
+    if g.kind == "frame_patch":
+        S = cosine_matrix(tile_descriptors(x, shape, k, g.src), tile_descriptors(x, shape, k, g.dst))
+    else:
+        S = cosine_matrix(descriptors(x, g.kind, g.src), descriptors(x, g.kind, g.dst))
     return S, best_match(S, g.dst)
 
 
@@ -375,6 +424,8 @@ def decide(x: np.ndarray, shape: LayerShape, cfg: CacheCfg, no_skip: bool = Fals
         groups = token_groups(shape, k, range(shape.F), ratio)
     elif cfg.gran == BLOCK:
         groups = block_groups(shape, k, ratio)
+    elif cfg.gran == FRAME and k > 1:
+        groups = frame_patch_groups(shape, k, fratio)
     elif cfg.gran == FRAME:
         groups = [frame_group(shape, fratio)]
     elif cfg.gran == FRAME_TOKEN:
@@ -403,7 +454,7 @@ def decide(x: np.ndarray, shape: LayerShape, cfg: CacheCfg, no_skip: bool = Fals
         if len(g.src) == 0:
             nm, ni = np.zeros(0), np.zeros(0, dtype=np.int64)
         else:
-            _, (nm, ni) = _match_group(x, g)
+            _, (nm, ni) = _match_group(x, g, shape, k)
         node_max.append(nm)
         node_idx.append(np.asarray(ni, dtype=np.int64))
         cached.append(select_cached(nm, g.src, g.R))
@@ -443,6 +494,9 @@ def build_sequences(shape: LayerShape, cfg: CacheCfg, dec: Decisions) -> List[Li
     cached_items = set(i for c in dec.cached for i in c)
     if cfg.gran == TOKEN:
         return [[f * N + n for n in range(N) if f * N + n not in cached_items] for f in range(F)]
+    if cfg.gran == FRAME and cfg.patch_k > 1:
+        dropped = set(p for t in cached_items for p in tile_tokens(shape, cfg.patch_k, t))
+        return [[f * N + n for n in range(N) if f * N + n not in dropped] for f in range(F)]
     if cfg.gran == FRAME:
         return [[f * N + n for n in range(N)] for f in range(F) if f not in cached_items]
     if cfg.gran == BLOCK:
@@ -475,6 +529,10 @@ def matched_token(shape: LayerShape, cfg: CacheCfg, dec: Decisions) -> Dict[int,
             elif g.kind == "block":
                 for f in range(F):
                     out[f * N + item] = f * N + rep
+            elif g.kind == "frame_patch":
+                d = rep // N                       # token n of the tile takes token n of frame d
+                for p in tile_tokens(shape, cfg.patch_k, item):
+                    out[p] = d * N + p % N
     return out
 
 
@@ -565,6 +623,16 @@ def attn_reduced(x_kept: np.ndarray, ctx: Optional[np.ndarray], w: Dict[str, np.
     return y_kept, y_ctx
 
 
+def attn_reduced_varlen(xs: Sequence[np.ndarray], w: Dict[str, np.ndarray], heads: int,
+                        head_dim: int) -> np.ndarray:
+    """Sequences of different lengths (R17), each attending within itself;
+    rows of all sequences concatenated in sequence order.  An empty
+    sequence contributes no rows."""
+    C = w["wo"].shape[0]
+    ys = [multi_head_attention(X, w["wq"], w["wk"], w["wv"], w["wo"], heads, head_dim) for X in xs if len(X)]
+    return np.concatenate(ys, axis=0) if ys else np.zeros((0, C))
+
+
 # ----------------------------------------------------------------------------
 # restoration and the layer step
 # ----------------------------------------------------------------------------
@@ -595,11 +663,17 @@ def layer_step(x: np.ndarray, ctx: Optional[np.ndarray], w: Dict[str, np.ndarray
     kept_idx, cached_idx, rmap = kept_and_map(shape, cfg, dec, seqs, cache_valid)
     xf = x.reshape(shape.F * shape.N, shape.C)
     lens = {len(s) for s in seqs}
-    assert len(lens) <= 1, "every attention sequence of one call has the same length"
-    L = lens.pop() if lens else 0
-    x_kept = xf[kept_idx].reshape(len(seqs), L, shape.C)
     c64 = None if ctx is None else np.asarray(ctx, dtype=np.float64)
-    y_kept, y_ctx = attn_reduced(x_kept, c64, w, shape.heads, shape.head_dim)
+    if len(lens) <= 1:
+        L = lens.pop() if lens else 0
+        x_kept = xf[kept_idx].reshape(len(seqs), L, shape.C)
+        y_kept, y_ctx = attn_reduced(x_kept, c64, w, shape.heads, shape.head_dim)
+    else:
+        # Frame Cache on patches (R17): sequences of different lengths
+        assert cfg.gran == FRAME and cfg.patch_k > 1 and c64 is None
+        y_kept = attn_reduced_varlen([xf[np.asarray(sq, dtype=np.int64)] for sq in seqs], w, shape.heads,
+                                     shape.head_dim)
+        y_ctx = None
     cy = None if cache_y is None else np.asarray(cache_y, dtype=np.float64).reshape(-1, shape.C)
     y = restore(y_kept, rmap, cy)
     return StepResult(y.reshape(shape.F, shape.N, shape.C), y_ctx, y_kept, kept_idx,

@@ -618,3 +618,67 @@ def test_block_step_composition_and_uncached_limit():
     ref_t = O.layer_step(x.reshape(rs.y.shape) + rs.y, None, wt, shape, tp, None, False)
     np.testing.assert_array_equal(rt.y, ref_t.y)
     assert len(rs.cached_idx) > 0 and len(rt.cached_idx) > 0
+
+
+# ----------------------------------------------------------------------------
+# Frame Cache on k x k patches (§3.3)
+# ----------------------------------------------------------------------------
+
+def test_golden_frame_patches():
+    g, x = load_golden("frame_patch_4x4x4_worked.json")
+    F, H, W, C, k = g["F"], g["H"], g["W"], g["C"], g["patch_k"]
+    shape = O.LayerShape(F, H, W, C, 1, 4)
+    for r, expect in g["cached"].items():
+        cfg = O.CacheCfg(O.FRAME, r_frame=float(r), patch_k=k)
+        dec = O.decide(x, shape, cfg)
+        assert len(dec.groups) == k * k
+        for grp, nm, ni, gg in zip(dec.groups, dec.node_max, dec.node_idx, g["groups"]):
+            assert grp.src == gg["candidates"] and grp.dst == gg["representatives"]
+            np.testing.assert_allclose(nm, [_frac(s) for s in gg["node_max"]], rtol=0, atol=1e-15)
+            assert list(ni) == gg["node_idx"]
+        assert sorted(i for c in dec.cached for i in c) == sorted(expect)
+    for key in ("r0.25", "r0.5"):
+        cfg = O.CacheCfg(O.FRAME, r_frame=float(key[1:]), patch_k=k)
+        dec = O.decide(x, shape, cfg)
+        seqs = O.build_sequences(shape, cfg, dec)
+        assert [len(s) for s in seqs] == g[key]["sequence_lengths"]
+        kept, cached, rmap = O.kept_and_map(shape, cfg, dec, seqs, cache_valid=True)
+        assert list(kept) == g[key]["kept_idx"]
+        assert list(rmap) == g[key]["restore_map_valid_cache"]
+        _, _, cmap = O.kept_and_map(shape, cfg, dec, seqs, cache_valid=False)
+        assert list(cmap) == g[key]["restore_map_cold_matched"]
+
+
+def test_frame_patches_at_k1_are_the_whole_frame_cache():
+    """One patch covering the frame: the tile is the frame, so the decisions
+    are those of the whole-frame Frame Cache (ids: frame f <-> token f*N)."""
+    wl = small_workload(O.FRAME, F=8, H=8, W=8, C=8, heads=1, head_dim=8, seed=81, planted=True)
+    shape = _shape(wl)
+    x = wl.f64(wl.steps[0])
+    g1 = O.frame_patch_groups(shape, 1, 0.3)[0]
+    gf = O.frame_group(shape, 0.3)
+    assert [i // shape.N for i in g1.src] == gf.src and g1.R == gf.R
+    S1 = O.cosine_matrix(O.tile_descriptors(x, shape, 1, g1.src), O.tile_descriptors(x, shape, 1, g1.dst))
+    Sf = O.cosine_matrix(O.descriptors(x, "frame", gf.src), O.descriptors(x, "frame", gf.dst))
+    np.testing.assert_array_equal(S1, Sf)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_frame_patches_brute_force(seed):
+    """Tile similarities against exact rational arithmetic over the tiles'
+    tokens, and the per-patch selection against an exhaustive search."""
+    wl = small_workload(O.FRAME, F=6, H=4, W=4, C=2, heads=1, head_dim=8, seed=90 + seed, frame_drift=0.3)
+    shape = _shape(wl)
+    x = wl.f64(wl.steps[0])
+    cfg = O.CacheCfg(O.FRAME, r_frame=0.34, patch_k=2)
+    dec = O.decide(x, shape, cfg)
+    xf = x.reshape(-1, shape.C)
+    for g, nm, ni, c in zip(dec.groups, dec.node_max, dec.node_idx, dec.cached):
+        for i, s in enumerate(g.src):
+            u = list(xf[O.tile_tokens(shape, 2, s)].reshape(-1))
+            sims = [B.cos_exact_order(u, list(xf[O.tile_tokens(shape, 2, d)].reshape(-1))) for d in g.dst]
+            best = max(sims)
+            assert abs(nm[i] - best) < 1e-13 and ni[i] == g.dst[sims.index(best)]
+        best_set = max(itertools.combinations(g.src, g.R),
+                       key=lambda sub: (sum(nm[g.src.index(t)] for t in sub), [-t for t in sub]))
+        assert sorted(c) == sorted(best_set)
