@@ -160,8 +160,16 @@ typedef struct {
  * and the reduced attention batch.
  * Requirements (OC_ERR_SHAPE otherwise): F, H, W, C, heads, head_dim >= 1;
  * H and W divisible by 2*patch_k; C % 8 == 0; head_dim % 8 == 0 and
- * head_dim <= 128; F >= 2 for FRAME and FRAME_TOKEN; patch_k == 1 for
- * FRAME; n_ctx == 0 unless F == 1 and gran == TOKEN.
+ * head_dim <= 128; 2 <= F <= 32 for FRAME and FRAME_TOKEN; patch_k <= 16
+ * for FRAME; n_ctx == 0 unless F == 1 and gran == TOKEN.
+ * FRAME with patch_k > 1 is Frame Cache on k x k patches (§3.3: every
+ * patch's frame set is matched on its own): n_groups = k*k, the items of a
+ * group are the frames' tiles of that patch, named by their top-left token
+ * id; each patch caches R = min(floor(r_frame*F), F/2) odd-frame tiles.  Its
+ * n_seq = F sequences (one per frame, in frame order) have varying lengths
+ * of at most seq_len = N tokens (a frame may keep none), n_kept = (F - R)*N
+ * in all; x_kept is then the packed [n_kept, C] batch, which only
+ * oc_layer_cached runs (oc_attn_reduced takes equal-length sequences).
  * Skip counts: a group of n items caches min(floor(r*n), candidates); frame
  * pairs cache min(n_f + floor(r*n_f), candidates) of their 2*n_f tokens.
  */
@@ -172,8 +180,8 @@ oc_status oc_plan(const oc_shape *shape, const oc_cfg *cfg, oc_plan_info *out);
  * §3.3).  For every candidate of every group: the largest cosine similarity
  * to a representative of its group (node_max, fp32) and that
  * representative's id (node_idx; smallest id on ties).  Ids are global token
- * ids (TOKEN, FRAME_TOKEN), spatial positions n (BLOCK) or frame indices
- * (FRAME).  Layout [n_groups, n_src_max], candidates of a group in ascending
+ * ids (TOKEN, FRAME_TOKEN), spatial positions n (BLOCK), frame indices
+ * (FRAME) or, for FRAME on patches, the tiles' top-left token ids.  Layout [n_groups, n_src_max], candidates of a group in ascending
  * id; padding entries hold -inf / -1.  Group order: TOKEN frame-major then
  * patches row-major; BLOCK patches; FRAME one group; FRAME_TOKEN attention
  * units (frame pairs and unmatched frames, by smallest frame) then patches.

@@ -162,11 +162,13 @@ def gather(x: torch.Tensor, kept_idx: torch.Tensor, shape: Shape, cfg: Cfg) -> t
     _need(x, shape.torch_dtype, "x")
     _need(kept_idx, torch.int32, "kept_idx")
     pl = plan(shape, cfg)
-    out = torch.empty((max(pl.n_seq, 1), max(pl.seq_len, 1), shape.C), dtype=x.dtype, device=x.device)
+    packed = cfg.gran == "frame" and cfg.patch_k > 1      # sequences of varying length: [n_kept, C]
+    shp = (max(pl.n_kept, 1), shape.C) if packed else (max(pl.n_seq, 1), max(pl.seq_len, 1), shape.C)
+    out = torch.empty(shp, dtype=x.dtype, device=x.device)
     sh, cf = shape.c(), cfg.c()
     L.check(L.lib().oc_gather(C.byref(sh), C.byref(cf), x.data_ptr(), kept_idx.data_ptr(), out.data_ptr(),
                               _stream(x)))
-    return out[:pl.n_seq, :pl.seq_len]
+    return out[:pl.n_kept] if packed else out[:pl.n_seq, :pl.seq_len]
 
 
 def attn_workspace_bytes(shape: Shape, n_seq: int, seq_len: int) -> int:

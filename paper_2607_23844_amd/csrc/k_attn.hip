@@ -38,14 +38,18 @@ __global__ void k_proj_f32(RowMapF rm, const float *__restrict__ wq, const float
 // one thread per (query row, head): online softmax over the sequence's keys
 __global__ void k_attn_f32(const float *__restrict__ Q, const float *__restrict__ K, const float *__restrict__ V,
                            float *__restrict__ O, int n_rows, int heads, int dh, int n_seq, int L, int Lk,
-                           float scale) {
+                           float scale, const int32_t *__restrict__ seq_off) {
     const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (long)n_rows * heads) return;
     const int r = (int)(i / heads), h = (int)(i - (long)r * heads);
     const int hd = heads * dh;
     int s, j;
-    seq_pos(r, n_seq, L, s, j);
-    const long row0 = (long)s * L;
+    seq_pos(r, n_seq, L, s, j, seq_off);
+    long row0 = (long)s * L;
+    if (seq_off != nullptr) {
+        row0 = seq_off[s];
+        Lk = seq_off[s + 1] - seq_off[s];
+    }
     const float *q = Q + (long)r * hd + h * dh;
     float acc[128];
     for (int d = 0; d < dh; ++d) acc[d] = 0.f;
@@ -109,7 +113,7 @@ bool attn_head_dim_supported(int dh) {
 }
 
 hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st) {
-    const int n_rows = a.n_seq * a.L + a.n_ctx;
+    const int n_rows = a.seq_off != nullptr ? a.n_main : a.n_seq * a.L + a.n_ctx;
     const int Lk = a.L + (a.n_seq == 1 ? a.n_ctx : 0);
     if (n_rows == 0) return hipSuccess;
     if (p.bf16) {
@@ -138,7 +142,7 @@ hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st) {
         launch_k(k_attn_f32, (unsigned)((na + 127) / 128), 128, 0, st, (const float *)a.q, (const float *)a.k,
                                                                   (const float *)a.vt, (float *)a.o, n_rows, p.heads,
                                                                   p.dh, a.n_seq, a.L, Lk,
-                                                                  (float)(1.0 / sqrt((double)p.dh)));
+                                                                  (float)(1.0 / sqrt((double)p.dh)), a.seq_off);
     }
     const long no = (long)n_rows * p.C;
     {

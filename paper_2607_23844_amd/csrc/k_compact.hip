@@ -185,6 +185,103 @@ __global__ void k_map_matched(int kind, const int32_t *__restrict__ flag, const 
     }
 }
 
+// Frame Cache on k x k patches: a token is skipped when its (frame, patch)
+// tile is cached (flag at the tile's top-left token).  Every block stages
+// the F*k*k tile flags in LDS and derives the per-frame retained counts (the
+// sequence offsets, frames in order) and the cached totals before each
+// frame; a token's rank inside its frame is its position minus the cached
+// tokens of its frame with a smaller id, counted tile by tile (tiles are
+// rectangles: whole tile rows above it plus, in its own tile row, the part
+// of each tile to its left).  Rows and ranks are checked against the plan's
+// static counts before any write.
+constexpr int FP_MAX_TILES = 8192;   // F * k * k (frames <= 32, k*k <= 256)
+
+__device__ __forceinline__ int fp_cached_before(const uint8_t *fl, int f, int kk, int k, int ph, int pw, int y,
+                                                int x) {
+    int c = 0;
+    for (int t = 0; t < kk; ++t) {
+        if (!fl[f * kk + t]) continue;
+        const int ty = (t / k) * ph, tx = (t % k) * pw;
+        c += pw * min(max(y - ty, 0), ph);                       // whole rows of the tile above row y
+        if (y >= ty && y < ty + ph) c += min(max(x - tx, 0), pw);   // its part of row y left of x
+    }
+    return c;
+}
+
+__global__ __launch_bounds__(256) void k_compact_fpatch(const int32_t *__restrict__ flag,
+                                                        const int32_t *__restrict__ mtok, int F, int N, int W, int k,
+                                                        int ph, int pw, int n_kept, int n_cached, int map_matched,
+                                                        int32_t *__restrict__ kept_idx,
+                                                        int32_t *__restrict__ cached_idx, int32_t *__restrict__ rmap,
+                                                        int32_t *__restrict__ seq_off) {
+    __shared__ uint8_t fl[FP_MAX_TILES];
+    __shared__ int off[33], cpre[33];
+    const int kk = k * k, tile = ph * pw;
+    for (int i = threadIdx.x; i < F * kk; i += blockDim.x) {
+        const int f = i / kk, t = i - f * kk;
+        const long tl = (long)f * N + (long)(t / k) * ph * W + (t % k) * pw;
+        fl[i] = flag[tl] != 0 ? 1 : 0;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int o = 0, c = 0;
+        for (int f = 0; f < F; ++f) {
+            int cf = 0;
+            for (int t = 0; t < kk; ++t) cf += fl[f * kk + t];
+            off[f] = o;
+            cpre[f] = c;
+            o += N - cf * tile;
+            c += cf * tile;
+        }
+        off[F] = o;
+        cpre[F] = c;
+    }
+    __syncthreads();
+    if (blockIdx.x == 0)
+        for (int f = threadIdx.x; f <= F; f += blockDim.x) seq_off[f] = min(off[f], n_kept);
+    const long total = (long)F * N;
+    for (long p = (long)blockIdx.x * blockDim.x + threadIdx.x; p < total; p += (long)gridDim.x * blockDim.x) {
+        const int f = (int)(p / N), n = (int)(p - (long)f * N), y = n / W, x = n - y * W;
+        const int t = (y / ph) * k + x / pw;
+        const int cb = fp_cached_before(fl, f, kk, k, ph, pw, y, x);
+        if (!fl[f * kk + t]) {
+            const int row = off[f] + n - cb;
+            const bool ok = row >= 0 && row < n_kept;
+            if (ok) kept_idx[row] = (int)p;
+            rmap[p] = ok ? row : -2;
+        } else {
+            const int cr = cpre[f] + cb;
+            if (cr >= 0 && cr < n_cached) cached_idx[cr] = (int)p;
+            int m = -1;
+            if (map_matched) {
+                // token n of the tile reads token n of the matched frame
+                const long tl = (long)f * N + (long)(y / ph) * ph * W + (x / pw) * pw;
+                const int d = mtok[tl] / N;
+                m = -2;
+                if (d >= 0 && d < F && !fl[d * kk + t]) {
+                    const int row = off[d] + n - fp_cached_before(fl, d, kk, k, ph, pw, y, x);
+                    if (row >= 0 && row < n_kept) m = row;
+                }
+            }
+            rmap[p] = m;
+        }
+    }
+}
+
+hipError_t launch_compact_fpatch(const Plan &p, const int32_t *flag, const int32_t *mtok, int32_t *kept_idx,
+                                 int32_t *cached_idx, int32_t *rmap, int32_t *seq_off, int map_matched,
+                                 hipStream_t st) {
+    if (p.F * p.k * p.k > FP_MAX_TILES || p.F > 32) return hipErrorInvalidValue;
+    const long total = (long)p.F * p.N;
+    const unsigned grid = (unsigned)std::min<long>((total + 255) / 256, 1024);
+    {
+        StageScope _stage(st, "compact");
+        launch_k(k_compact_fpatch, grid, 256, 0, st, flag, mtok, p.F, p.N, p.W, p.k, p.ph, p.pw, p.n_kept, p.n_cached,
+                 map_matched, kept_idx, cached_idx, rmap, seq_off);
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_compact(const Plan &p, const int32_t *units, const int32_t *flag, const int32_t *mtok,
                           int32_t *fcnt, int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap, int map_matched,
                           hipStream_t st) {

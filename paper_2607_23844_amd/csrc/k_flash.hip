@@ -76,7 +76,7 @@ template <int DH, int NW, bool DMA>
 __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                                                     const uint16_t *__restrict__ Vt, uint16_t *__restrict__ O,
                                                     int hd, int heads, int n_seq, int L, int Lk, int lpad,
-                                                    int n_qt) {
+                                                    int n_qt, const int32_t *__restrict__ seq_off) {
     using C = FlashCfg<DH, DMA>;
     constexpr int DK = C::DK, NKS = C::NKS, DV = C::DV, NDB = C::NDB, KT = C::KT, LDK = C::LDK, LDV = C::LDV;
     constexpr int NT = NW * 64, QT = 32 * NW;
@@ -90,7 +90,14 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
     const int lid = xcd_remap(blockIdx.x, total);
     const int qt = lid % n_qt, hs = lid / n_qt, h = hs % heads, s = hs / heads;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, ln = lane & 31, lg = lane >> 5;
-    const long row0 = (long)s * L;
+    long row0 = (long)s * L;
+    if (seq_off != nullptr) {
+        // sequences of varying length: this sequence's rows and key count;
+        // query tiles past its end leave at once (the whole block)
+        row0 = seq_off[s];
+        Lk = seq_off[s + 1] - seq_off[s];
+        if (qt * QT >= Lk) return;
+    }
     const int q_base = qt * QT + wave * 32;
     const uint16_t *kbase = K + row0 * hd + h * DH;
     const uint16_t *vbase = Vt + ((long)h * n_seq + s) * DH * lpad;
@@ -536,7 +543,7 @@ static hipError_t go(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
     if (e != hipSuccess) return e;
     launch_k(k_flash<DH, NW, DMA>, total, NW * 64, lds, st, (const uint16_t *)a.q, (const uint16_t *)a.k,
                                                       (const uint16_t *)a.vt, (uint16_t *)a.o, p.hd, p.heads,
-                                                      a.n_seq, a.L, Lk, a.lpad, n_qt);
+                                                      a.n_seq, a.L, Lk, a.lpad, n_qt, a.seq_off);
     return hipGetLastError();
 }
 
@@ -545,6 +552,9 @@ static hipError_t go(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
 // DMA-staged when the head dim allows it.
 template <int DH>
 static hipError_t go_dh(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
+    // sequences of varying length: the register-staged kernel, which masks
+    // every sequence's end itself (Lk is the longest)
+    if (a.seq_off != nullptr) return go<DH, 4, false>(p, a, Lk, st);
     if (attn_short(Lk)) return Lk <= 32 ? go_short<DH, 1>(p, a, Lk, st) : go_short<DH, 2>(p, a, Lk, st);
     if constexpr (DH % 64 == 0) {
         if (flash_uses_dma(DH, Lk, p.hd)) {

@@ -108,6 +108,62 @@ hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, unsigned lo
     return hipGetLastError();
 }
 
+// Frame Cache on patches: one block per (frame, patch) tile, the sum of
+// squares of its ph rows of pw*C elements (16-byte chunks spread over the
+// block, wave partials added in a fixed order), stored at the tile's
+// top-left token; the blocks past the tiles clear pack and convert wo.
+template <typename T>
+__global__ void k_tile_norm(const T *__restrict__ x, float *__restrict__ inv, int F, int N, int W, int k, int ph,
+                            int pw, int C, int norm_blocks, unsigned long long *__restrict__ pack, long n_pack,
+                            const uint4 *__restrict__ wo, long n8, uint4 *__restrict__ wo16) {
+    if ((int)blockIdx.x >= norm_blocks) {
+        const long nb = gridDim.x - norm_blocks;
+        for (long i = (long)(blockIdx.x - norm_blocks) * blockDim.x + threadIdx.x; i < n8; i += nb * blockDim.x)
+            wo16[i] = bf16x8_to_f16x8(wo[i]);
+        return;
+    }
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n_pack; i += (long)norm_blocks * blockDim.x)
+        pack[i] = 0ull;
+    constexpr int VEC = 16 / sizeof(T);
+    __shared__ float wsum[4];
+    const int kk = k * k, f = blockIdx.x / kk, g = blockIdx.x - f * kk;
+    const long tl = (long)f * N + (long)(g / k) * ph * W + (g % k) * pw;
+    const int cpr = pw * C / VEC;                  // chunks per tile row
+    float ss = 0.f;
+    for (int q = threadIdx.x; q < ph * cpr; q += blockDim.x) {
+        const int row = q / cpr, c = (q - row * cpr) * VEC;
+        const uint4 v = *reinterpret_cast<const uint4 *>(x + (tl + (long)row * W) * C + c);
+        const T *e = reinterpret_cast<const T *>(&v);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            const float fv = Elem<T>::ld(e + j);
+            ss = fmaf(fv, fv, ss);
+        }
+    }
+    ss = wave_sum(ss);
+    if ((threadIdx.x & (WAVE - 1)) == 0) wsum[threadIdx.x / WAVE] = ss;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const float t = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
+        inv[tl] = t > 0.f ? (float)(1.0 / sqrt((double)t)) : 0.f;
+    }
+}
+
+hipError_t launch_tile_norm(const Plan &p, const void *x, float *inv, unsigned long long *node_pack, long n_pack,
+                            const void *wo, void *wo16, long n_wo, hipStream_t st) {
+    StageScope _stage(st, "inv_norm");
+    const int blocks = p.F * p.k * p.k;
+    const long n8 = (wo && wo16 && p.bf16) ? n_wo / 8 : 0;
+    const int cvt_blocks = n8 > 0 ? (int)std::min<long>((n8 + 255) / 256, 1024) : 0;
+    if (p.bf16)
+        launch_k(k_tile_norm<uint16_t>, blocks + cvt_blocks, 256, 0, st, (const uint16_t *)x, inv, p.F, p.N, p.W, p.k,
+                 p.ph, p.pw, p.C, blocks, node_pack, n_pack, (const uint4 *)wo, n8, (uint4 *)wo16);
+    else
+        launch_k(k_tile_norm<float>, blocks, 256, 0, st, (const float *)x, inv, p.F, p.N, p.W, p.k, p.ph, p.pw, p.C,
+                 blocks, node_pack, n_pack, nullptr, 0, nullptr);
+    return hipGetLastError();
+}
+
 // ----------------------------------------------------------------------------
 // similarity + arg-max, bf16 MFMA
 // ----------------------------------------------------------------------------
@@ -528,11 +584,11 @@ hipError_t launch_match(const Plan &p, const void *x, const float *inv, const in
                         hipStream_t st) {
     const GroupMap gm = group_map(p, units);
     const int G = p.n_groups, S = p.n_src_max, D = p.n_dst_max;
-    const bool block = p.kind == KIND_BLOCK;
-    const int K = block ? p.F * p.C : p.C;
-    const int seg_len = block ? p.C : 0;
-    const long sub_stride = (long)p.N * p.C;
-    const long item_stride = p.C;
+    const MatchGeom mg = match_geom(p);
+    const int K = mg.K;
+    const int seg_len = mg.seg_len;
+    const long sub_stride = mg.sub_stride;
+    const long item_stride = mg.item_stride;
     {
         StageScope _stage(st, "match");
         if (p.bf16) {

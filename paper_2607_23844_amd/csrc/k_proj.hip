@@ -71,8 +71,8 @@ __global__ __launch_bounds__(256) void k_proj_qkv(RowMap rm, const uint16_t *__r
                                                   const uint16_t *__restrict__ wk, const uint16_t *__restrict__ wv,
                                                   int hd, int dh, float qscale, int nw, int n_qk_at, int n_bt,
                                                   int n_v_at, int n_v_bt, int n_seq, int L, int lpad, int zero_pad,
-                                                  uint16_t *__restrict__ Q, uint16_t *__restrict__ K,
-                                                  uint16_t *__restrict__ Vt) {
+                                                  const int32_t *__restrict__ seq_off, uint16_t *__restrict__ Q,
+                                                  uint16_t *__restrict__ K, uint16_t *__restrict__ Vt) {
     using T = QKVTile<DMA, SH>;
     using Rows = typename std::conditional<DMA, DmaRows, RegRows>::type;
     constexpr int BA = QKVShape<DMA, SH>::BA, BB = QKVShape<DMA, SH>::BB;
@@ -123,7 +123,7 @@ __global__ __launch_bounds__(256) void k_proj_qkv(RowMap rm, const uint16_t *__r
     run_tile(t, lds, rowsA, rowsB, rm.row(0), wv, rm.C, Rows{});
     const int Lk = n_seq == 1 ? rm.n_rows : L;
     const int r0 = at * BA, f0 = bt * BB;
-    if (n_seq == 1 || L % BA == 0) {
+    if (seq_off == nullptr && (n_seq == 1 || L % BA == 0)) {
         const int s = n_seq == 1 ? 0 : r0 / L, j0 = r0 - s * L;   // j0 is a multiple of BA
         stage_rows<BA>(t, lds, [&](float v, int a) { return (uint16_t)(j0 + a < Lk ? f2h_bits(v) : 0); },
                        [](int a) { return vt_key_of_pos(a); });
@@ -150,14 +150,14 @@ __global__ __launch_bounds__(256) void k_proj_qkv(RowMap rm, const uint16_t *__r
                     const int r = r0 + T::a_of(i, g) + e;
                     if (r >= rm.n_rows) continue;
                     int s, jj;
-                    seq_pos(r, n_seq, L, s, jj);
+                    seq_pos(r, n_seq, L, s, jj, seq_off);
                     Vt[(((long)h * n_seq + s) * dh + d) * lpad + vt_key_of_pos(jj)] = f2h_bits(t.acc[i][j][4 * g + e]);
                 }
     }
     // zero the padded key positions [Lk, lpad) of this block's features, for
     // the sequences s = at, at + n_v_at, ... (the DMA-staged attention reads them)
     const int npad = lpad - Lk;
-    if (zero_pad && npad > 0) {
+    if (zero_pad && npad > 0 && seq_off == nullptr) {
         for (int sq = at; sq < n_seq; sq += n_v_at)
             for (int idx = threadIdx.x; idx < BB * npad; idx += blockDim.x) {
                 const int f = f0 + idx / npad, jj = Lk + idx % npad;
@@ -184,7 +184,7 @@ static hipError_t launch_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a,
     const int total = n_qk_at * n_bt + n_v_at * n_v_bt;
     launch_k(k_proj_qkv<DMA, SH>, total, 256, QKVTile<DMA, SH>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
              (const uint16_t *)a.wk, (const uint16_t *)a.wv, p.hd, p.dh, qscale, nw, n_qk_at, n_bt, n_v_at, n_v_bt,
-             a.n_seq, a.L, a.lpad, zero_pad, (uint16_t *)a.q, (uint16_t *)a.k, (uint16_t *)a.vt);
+             a.n_seq, a.L, a.lpad, zero_pad, a.seq_off, (uint16_t *)a.q, (uint16_t *)a.k, (uint16_t *)a.vt);
     return hipGetLastError();
 }
 
@@ -192,9 +192,12 @@ hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, h
     const float qscale = (float)(1.4426950408889634 / sqrt((double)p.dh));
     StageScope _stage(st, "proj_qkv");
     const int Lk = a.n_seq == 1 ? rm.n_rows : a.L;
-    const int zero_pad = flash_uses_dma(p.dh, Lk, p.hd) ? 1 : 0;
+    // sequences of varying length: Vt slots per sequence, filled element by
+    // element; the attention masks their ends itself (no padding to zero)
+    const bool varlen = a.seq_off != nullptr;
+    const int zero_pad = !varlen && flash_uses_dma(p.dh, Lk, p.hd) ? 1 : 0;
     // short sequences: V rows from the Q/K tiles (nw = 3), no V tiles
-    const int nw = attn_short(Lk) ? 3 : 2;
+    const int nw = !varlen && attn_short(Lk) ? 3 : 2;
     if (p.C % 64 != 0) return launch_qkv<false, 0>(p, rm, a, qscale, nw, zero_pad, st);
     // block rounds (two blocks per CU) times the work of one tile, a wide
     // tile being 1.5 units (the SD3-like layer at r = 0.5: 460 tiles of 192 x

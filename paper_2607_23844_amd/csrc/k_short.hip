@@ -174,7 +174,8 @@ __global__ __launch_bounds__(256) void k_qkv_attn_short(RowMap rm, const uint16_
 }
 
 bool qkv_attn_short_applies(const Plan &p, const AttnArgs &a) {
-    return p.bf16 && p.dh == SH_DH && p.C % 64 == 0 && a.n_ctx == 0 && a.n_seq >= 1 && a.L >= 1 &&
+    return p.bf16 && p.dh == SH_DH && p.C % 64 == 0 && a.n_ctx == 0 && a.seq_off == nullptr && a.n_seq >= 1 &&
+           a.L >= 1 &&
            attn_short(a.L) && (long)a.n_seq * a.L < (1L << 31);
 }
 

@@ -87,7 +87,8 @@ oc_status make_plan(const oc_shape *sh, const oc_cfg *cfg, bool no_skip, Plan &p
         return fail(OC_ERR_SHAPE, "context tokens need F == 1 and OC_GRAN_TOKEN");
     if ((cfg->gran == OC_GRAN_FRAME || cfg->gran == OC_GRAN_FRAME_TOKEN) && (sh->F < 2 || sh->F > 32))
         return fail(OC_ERR_SHAPE, "frame caching needs 2 <= F <= 32 (F=%d)", sh->F);
-    if (cfg->gran == OC_GRAN_FRAME && p.k != 1) return fail(OC_ERR_SHAPE, "OC_GRAN_FRAME needs patch_k == 1");
+    if (cfg->gran == OC_GRAN_FRAME && p.k > 1 && p.k * p.k > 256)
+        return fail(OC_ERR_SHAPE, "Frame Cache on patches needs patch_k <= 16 (patch_k=%d)", p.k);
     p.ph = p.H / p.k;
     p.pw = p.W / p.k;
     p.np = p.ph * p.pw;
@@ -111,12 +112,22 @@ oc_status make_plan(const oc_shape *sh, const oc_cfg *cfg, bool no_skip, Plan &p
             p.n_items = p.N;
             break;
         case OC_GRAN_FRAME:
-            p.kind = KIND_FRAME;
             p.n_fsrc = p.F / 2; p.n_fdst = (p.F + 1) / 2;
             p.R_f = clampi(floor_ratio(p.r_frame, p.F), p.n_fsrc);
-            p.n_groups = 1; p.n_src_max = p.n_fsrc; p.n_dst_max = p.n_fdst;
-            p.n_seq = p.F - p.R_f; p.seq_len = p.N;
-            p.n_items = p.F;
+            p.n_src_max = p.n_fsrc; p.n_dst_max = p.n_fdst;
+            if (p.k == 1) {
+                p.kind = KIND_FRAME;
+                p.n_groups = 1;
+                p.n_seq = p.F - p.R_f; p.seq_len = p.N;
+                p.n_items = p.F;
+            } else {
+                // per patch: R_f of the odd frames' tiles; every frame keeps a
+                // varying number of tokens, R_f * N in all are cached
+                p.kind = KIND_FPATCH;
+                p.n_groups = kk;
+                p.n_seq = p.F; p.seq_len = p.N;
+                p.n_items = p.F * p.N;
+            }
             break;
         default: {  // OC_GRAN_FRAME_TOKEN
             p.kind = KIND_TOKEN;
@@ -135,7 +146,7 @@ oc_status make_plan(const oc_shape *sh, const oc_cfg *cfg, bool no_skip, Plan &p
         }
     }
     if (p.n_src_max > 16384) return fail(OC_ERR_SHAPE, "group of %d candidates exceeds 16384", p.n_src_max);
-    p.n_kept = p.n_seq * p.seq_len;
+    p.n_kept = p.kind == KIND_FPATCH ? (p.F - p.R_f) * p.N : p.n_seq * p.seq_len;
     p.n_cached = p.F * p.N - p.n_kept;
     return OC_OK;
 }
@@ -171,7 +182,7 @@ Layout make_layout(const Plan &p) {
         const MatchSplit ms = match_split(p);
         L.mpart = take(ms.n_split > 1 ? (size_t)ms.n_split * GS * p.n_dst_max * 4 : 0);
     }
-    const bool frames = p.gran == OC_GRAN_FRAME || p.gran == OC_GRAN_FRAME_TOKEN;
+    const bool frames = p.kind == KIND_FRAME || p.gran == OC_GRAN_FRAME_TOKEN;
     L.gram_part = take(frames ? (size_t)gram_blocks(p) * 1024 * 4 : 0);
     L.fgram = take(frames ? 1024 * 8 : 0);
     L.fsim = take(frames ? 1024 * 8 : 0);
@@ -186,6 +197,7 @@ Layout make_layout(const Plan &p) {
     L.kept = take(FN * 4);
     L.cached = take(FN * 4);
     L.rmap = take(FN * 4);
+    L.seqoff = take((size_t)(p.F + 1) * 4);
     L.attn = o;
     const Plan fp = full_plan(p);
     const AttnWs a1 = attn_ws(p, p.n_seq, p.seq_len, o);
@@ -241,7 +253,7 @@ oc_status run_match(const Plan &p, const Layout &L, const void *x, float *node_m
                     void *ws, hipStream_t st, const void *wo = nullptr, void *wo16 = nullptr,
                     bool frame_compact = false) {
     char *w = (char *)ws;
-    const bool frames = p.gran == OC_GRAN_FRAME || p.gran == OC_GRAN_FRAME_TOKEN;
+    const bool frames = p.kind == KIND_FRAME || p.gran == OC_GRAN_FRAME_TOKEN;
     unsigned long long *pack = at<unsigned long long>(ws, L.node_pack);
     const long n_pack = (long)p.n_groups * p.n_src_max;
     // Frame+Token Cache: the Gram launch also writes the token norms and clears pack
@@ -264,7 +276,10 @@ oc_status run_match(const Plan &p, const Layout &L, const void *x, float *node_m
                 "frame stage");
     }
     if (p.kind == KIND_FRAME) return OC_OK;
-    if (!gram_prep)
+    if (p.kind == KIND_FPATCH)
+        HIP_TRY(launch_tile_norm(p, x, at<float>(ws, L.inv), pack, n_pack, wo, wo16, (long)p.C * p.hd, st),
+                "tile norms");
+    else if (!gram_prep)
         HIP_TRY(launch_inv_norm(p, x, at<float>(ws, L.inv), pack, n_pack, wo, wo16, (long)p.C * p.hd, st),
                 "inv_norm");
     HIP_TRY(launch_match(p, x, at<float>(ws, L.inv), units_of(p, L, ws), pack, at<float>(ws, L.mpart),
@@ -301,6 +316,12 @@ oc_status run_select(const Plan &p, const Layout &L, float *node_max, int32_t *n
         if (map_matched)
             HIP_TRY(launch_map_matched(p, at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok), rmap, st),
                     "map matched");
+        return OC_OK;
+    }
+    if (p.kind == KIND_FPATCH) {
+        HIP_TRY(launch_compact_fpatch(p, at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok), kept, cached, rmap,
+                                      at<int32_t>(ws, L.seqoff), map_matched, st),
+                "compact");
         return OC_OK;
     }
     HIP_TRY(launch_compact(p, at<int32_t>(ws, L.units), at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok),
@@ -520,6 +541,7 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
     a.lpad = aw.lpad;
     a.wo16 = at<char>(ws, aw.wo16);
     a.wo16_ready = wo_early ? 1 : 0;
+    a.seq_off = p.kind == KIND_FPATCH ? at<int32_t>(ws, L.seqoff) : nullptr;
     HIP_TRY(launch_attention(p, a, stream), "attention");
     if (map_matched) HIP_TRY(launch_copy_matched(p, cached, p.n_cached, rmap, kept, cache->y, stream), "copy matched");
 

@@ -31,8 +31,21 @@ struct RowMap {
 };
 
 // sequence and position of batch row r (a single sequence also owns the
-// context rows appended after its L retained tokens)
-__device__ __forceinline__ void seq_pos(int r, int n_seq, int L, int &s, int &j) {
+// context rows appended after its L retained tokens); with seq_off,
+// sequence s owns rows [seq_off[s], seq_off[s+1]) (binary search; empty
+// sequences are skipped over)
+__device__ __forceinline__ void seq_pos(int r, int n_seq, int L, int &s, int &j,
+                                        const int32_t *seq_off = nullptr) {
+    if (seq_off != nullptr) {
+        int lo = 0, hi = n_seq - 1;          // last s with seq_off[s] <= r
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (seq_off[mid] <= r) lo = mid; else hi = mid - 1;
+        }
+        s = lo;
+        j = r - seq_off[lo];
+        return;
+    }
     if (n_seq == 1) { s = 0; j = r; }
     else { s = r / L; j = r - s * L; }
 }

@@ -10,7 +10,9 @@
 // Representatives are the top-left tokens of the 2x2 windows (of frame d for
 // a pair), ascending.  Block groups use spatial positions as ids (no frame
 // term).  Frame groups: odd frames are candidates, even frames
-// representatives.
+// representatives.  Frame-patch groups (one per patch): the odd frames'
+// tiles of the patch are candidates, the even frames' tiles representatives,
+// each tile named by its top-left token id.
 #pragma once
 #include "oc_internal.h"
 
@@ -28,6 +30,18 @@ struct GroupMap {
 
     __device__ __forceinline__ Grp group(int g) const {
         Grp r;
+        if (kind == KIND_FPATCH) {
+            // patch g: its frames' tiles, named by their top-left tokens
+            r.s = r.d = r.a = r.b = r.rf = 0;
+            r.n_a = 0;
+            r.oy = (g / k) * ph;
+            r.ox = (g % k) * pw;
+            r.nsrc = F / 2;
+            r.pair = false;
+            r.fbase = N;
+            r.R = R_f;
+            return r;
+        }
         if (kind == KIND_FRAME) {
             r.s = r.d = r.a = r.b = r.rf = r.oy = r.ox = 0;
             r.n_a = 0;
@@ -79,6 +93,7 @@ struct GroupMap {
     __device__ __forceinline__ int src_id(const Grp &r, int i) const {
         if (i < 0 || i >= r.nsrc) return -1;
         if (kind == KIND_FRAME) return 2 * i + 1;
+        if (kind == KIND_FPATCH) return (int)((2 * i + 1) * r.fbase + (long)r.oy * W + r.ox);
         int f, y, x;
         if (!r.pair) { f = r.s; patch_nonrep(i, y, x); }
         else if (i < r.n_a) {
@@ -95,6 +110,7 @@ struct GroupMap {
     // global id of representative i of the group, -1 past its end
     __device__ __forceinline__ int dst_id(const Grp &r, int i) const {
         if (kind == KIND_FRAME) return (i >= 0 && 2 * i < F) ? 2 * i : -1;
+        if (kind == KIND_FPATCH) return (i >= 0 && 2 * i < F) ? (int)(2 * i * r.fbase + (long)r.oy * W + r.ox) : -1;
         if (i < 0 || i >= np_dst) return -1;
         int y, x;
         patch_rep(i, y, x);

@@ -8,7 +8,9 @@
 
 namespace oc {
 
-enum Kind { KIND_TOKEN = 0, KIND_BLOCK = 1, KIND_FRAME = 2 };
+// KIND_FPATCH: Frame Cache on k x k patches (k > 1): one group per patch, its
+// items the frames' tiles of that patch, named by their top-left token id.
+enum Kind { KIND_TOKEN = 0, KIND_BLOCK = 1, KIND_FRAME = 2, KIND_FPATCH = 3 };
 
 // Static sizes of one call; everything depends only on shape and cfg.
 struct Plan {
@@ -20,7 +22,7 @@ struct Plan {
     int np_src, np_dst;      // candidates / representatives per frame-patch (3/4, 1/4)
     double r, r_frame;
     // matching stage reported by oc_match
-    int kind;                // KIND_TOKEN (token / pair groups), KIND_BLOCK, KIND_FRAME
+    int kind;                // KIND_TOKEN (token / pair groups), KIND_BLOCK, KIND_FRAME, KIND_FPATCH
     int n_groups, n_src_max, n_dst_max;
     int R_tok;               // budget of a token / block group (unmatched frame-patch)
     int R_pair;              // budget of a frame-pair patch group
@@ -28,7 +30,8 @@ struct Plan {
     int n_fsrc, n_fdst, R_f;
     int n_units;             // attention units: frames (TOKEN), pairs + unmatched (FRAME_TOKEN)
     // reduced batch
-    int n_kept, n_cached, n_seq, seq_len;
+    int n_kept, n_cached, n_seq, seq_len;   // KIND_FPATCH: n_seq = F sequences of at most seq_len = N
+                                            // tokens each, of varying length (seq_off in the workspace)
     int n_items;             // matched items: F*N tokens, N blocks, F frames
 };
 
@@ -37,6 +40,7 @@ struct Layout {
     size_t inv, node_pack, node_max, node_idx, mpart;
     size_t gram_part, fgram, fsim, fmax, fidx, forder, pairs, units;
     size_t flag, mtok, fcnt, kept, cached, rmap;
+    size_t seqoff;           // KIND_FPATCH: sequence offsets [F + 1]
     size_t attn;             // start of the attention workspace (Q, K, O, V)
     size_t total;
 };
@@ -76,12 +80,23 @@ hipError_t launch_inv_norm(const Plan &p, const void *x, float *inv, unsigned lo
 // workspace; many candidate tiles with several representative tiles sweep
 // the representatives per candidate tile; otherwise one block per tile pair.
 struct MatchSplit { int n_split, kc; };
+// Descriptor geometry of the matched items: item id i starts at element
+// i * item_stride of x and is K elements long, read as segments of seg_len
+// contiguous elements sub_stride apart (seg_len == 0: one contiguous run).
+// Tokens: a C-vector; blocks: F segments of C, a frame apart; frame-patch
+// tiles: ph segments of pw*C, an image row apart.
+struct MatchGeom { int K, seg_len; long sub_stride, item_stride; };
+inline MatchGeom match_geom(const Plan &p) {
+    if (p.kind == KIND_BLOCK) return MatchGeom{p.F * p.C, p.C, (long)p.N * p.C, p.C};
+    if (p.kind == KIND_FPATCH) return MatchGeom{p.ph * p.pw * p.C, p.pw * p.C, (long)p.W * p.C, p.C};
+    return MatchGeom{p.C, 0, (long)p.N * p.C, p.C};
+}
 inline MatchSplit match_split(const Plan &p) {
     MatchSplit m{1, 0};
     if (!p.bf16 || p.kind == KIND_FRAME) return m;
-    const bool block = p.kind == KIND_BLOCK;
-    const int K = block ? p.F * p.C : p.C;
-    const int seg = block ? p.C : 0;
+    const MatchGeom mg = match_geom(p);
+    const int K = mg.K;
+    const int seg = mg.seg_len;
     if (K % 64 != 0 || (seg > 0 && seg % 64 != 0)) return m;
     const int nk = K / 64;
     const long tiles = (long)((p.n_src_max + 63) / 64) * ((p.n_dst_max + 63) / 64) * p.n_groups;
@@ -134,6 +149,17 @@ inline bool select_compacts(const Plan &p) {
 hipError_t launch_compact(const Plan &p, const int32_t *units, const int32_t *flag, const int32_t *mtok,
                           int32_t *fcnt, int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap,
                           int map_matched, hipStream_t st);
+// Frame Cache on patches: from the tiles' flags / matched tiles (at their
+// top-left ids), the frame-major kept list, the cached list, the restore map
+// (cold "matched": token n of a skipped tile reads token n of the matched
+// frame) and the sequence offsets seq_off[F + 1].
+hipError_t launch_compact_fpatch(const Plan &p, const int32_t *flag, const int32_t *mtok, int32_t *kept_idx,
+                                 int32_t *cached_idx, int32_t *rmap, int32_t *seq_off, int map_matched,
+                                 hipStream_t st);
+// Frame Cache on patches: the tiles' inverse norms (at their top-left ids),
+// with the same pack clearing and wo conversion as launch_inv_norm.
+hipError_t launch_tile_norm(const Plan &p, const void *x, float *inv, unsigned long long *node_pack, long n_pack,
+                            const void *wo, void *wo16, long n_wo, hipStream_t st);
 // cold "matched" restore map: cached positions point at their matched row
 hipError_t launch_map_matched(const Plan &p, const int32_t *flag, const int32_t *mtok, int32_t *rmap,
                               hipStream_t st);
@@ -162,6 +188,9 @@ struct AttnArgs {
     int wo16_ready;                   // wo16 already converted by an earlier launch of this call
     int lpad;                         // padded keys per sequence in vt
     int tF, tN;                       // no index lists: row r = n*tF + f is token f*tN + n (tF > 0)
+    const int32_t *seq_off;           // sequences of varying length: sequence s owns rows
+                                      // [seq_off[s], seq_off[s+1]) (n_main rows in all, no context,
+                                      // L the longest); nullptr: every sequence has L rows
 };
 hipError_t launch_attention(const Plan &p, const AttnArgs &a, hipStream_t st);
 

@@ -86,6 +86,13 @@ RAW_EXCEPTIONS = {
     # 2 sequences of 256 tokens, 3 heads of 64: peak/RMS 8.7; measured raw
     # 0.0204, rounding-adjusted 0.0020
     "attn bf16 dh64 2x256+0": (0.0204, 0.025),
+    # Latte-like spatial layer, Frame Cache on 2x2 / 4x4 patches: frames that
+    # keep one or two patches (16-128 tokens) give outputs up to 13.3 times
+    # the layer's RMS, where half a bf16 ulp alone is 2.75% of the RMS;
+    # measured raw 0.0283 (k = 2, third step) and 0.0280 (k = 4), adjusted
+    # 0.0014-0.0018
+    "latte_spatial frame patches k2": (0.0283, 0.035),
+    "latte_spatial frame patches k4": (0.0280, 0.035),
 }
 
 
@@ -97,16 +104,19 @@ def check_output_bars(err: float, raw: float, dtype: str, what: str = "output", 
     assert raw <= raw_bar, f"{what}: raw error {raw:.3g} > {raw_bar}"
 
 
-def group_margins(x64: np.ndarray, g: O.Group) -> np.ndarray:
+def group_margins(x64: np.ndarray, g: O.Group, shape=None, k: int = 1) -> np.ndarray:
     """Per candidate: top-1 minus top-2 cosine similarity (inf with one rep)."""
-    S = O.cosine_matrix(O.descriptors(x64, g.kind, g.src), O.descriptors(x64, g.kind, g.dst))
+    if g.kind == "frame_patch":
+        S = O.cosine_matrix(O.tile_descriptors(x64, shape, k, g.src), O.tile_descriptors(x64, shape, k, g.dst))
+    else:
+        S = O.cosine_matrix(O.descriptors(x64, g.kind, g.src), O.descriptors(x64, g.kind, g.dst))
     if S.shape[1] < 2:
         return np.full(S.shape[0], np.inf)
     top = np.sort(S, axis=1)
     return top[:, -1] - top[:, -2]
 
 
-def check_match(x64, dec: O.Decisions, nm_gpu: np.ndarray, ni_gpu: np.ndarray, kind: str):
+def check_match(x64, dec: O.Decisions, nm_gpu: np.ndarray, ni_gpu: np.ndarray, kind: str, shape=None, k: int = 1):
     """node_max within tolerance; node_idx equal outside the margin band.
     Returns {candidate id: gpu rep id} for in-band disagreements."""
     tol = NODE_MAX_TOL[kind]
@@ -120,7 +130,7 @@ def check_match(x64, dec: O.Decisions, nm_gpu: np.ndarray, ni_gpu: np.ndarray, k
         assert np.all(nm_gpu[gi, n:] == -np.inf) and np.all(ni_gpu[gi, n:] == -1)
         diff = np.nonzero(ni_gpu[gi, :n] != dec.node_idx[gi])[0]
         if len(diff):
-            marg = group_margins(x64, g)
+            marg = group_margins(x64, g, shape, k)
             for i in diff:
                 assert marg[i] <= BAND, f"group {gi} cand {g.src[i]}: idx {ni_gpu[gi, i]} vs {dec.node_idx[gi][i]}, " \
                                         f"margin {marg[i]:.3g}"
@@ -148,9 +158,18 @@ def check_selection(dec: O.Decisions, gpu_cached_items: set):
     return n_diff
 
 
-def gpu_cached_items(kind_gran: str, cached_idx: np.ndarray, N: int) -> set:
+def gpu_cached_items(kind_gran: str, cached_idx: np.ndarray, N: int, shape=None, k: int = 1) -> set:
     if kind_gran == "block":
         return set(int(p) % N for p in cached_idx)
+    if kind_gran == "frame" and k > 1:
+        # Frame Cache on patches: the tiles (top-left token ids) of the cached tokens
+        h, w = shape.H // k, shape.W // k
+        out = set()
+        for p in cached_idx:
+            f, n = divmod(int(p), N)
+            y, x = divmod(n, shape.W)
+            out.add(f * N + (y // h) * h * shape.W + (x // w) * w)
+        return out
     if kind_gran == "frame":
         return set(int(p) // N for p in cached_idx)
     return set(int(p) for p in cached_idx)
@@ -203,9 +222,9 @@ def decision_parity(x64, osh, ocf, tr, valid):
     kind = "block" if ocf.gran == O.BLOCK else ("frame" if ocf.gran == O.FRAME else "token")
     nm = tr["node_max"].cpu().numpy()
     ni = tr["node_idx"].cpu().numpy()
-    ov, worst_nm = check_match(x64, dec, nm, ni, kind)
+    ov, worst_nm = check_match(x64, dec, nm, ni, kind, osh, ocf.patch_k)
     cached_idx = tr["cached_idx"].cpu().numpy()
-    items = gpu_cached_items(ocf.gran, cached_idx, osh.N)
+    items = gpu_cached_items(ocf.gran, cached_idx, osh.N, osh, ocf.patch_k)
     n_band = check_selection(dec, items)
     forced.update(cached=items, match=ov)
     dec = O.force_decisions(dec, items, ov)
@@ -218,7 +237,7 @@ def check_maps(tr, kept_idx, cached_idx, restore_map):
     np.testing.assert_array_equal(tr["restore_map"].cpu().numpy(), restore_map)
 
 
-def check_layer_step(x64, ctx64, W64, osh, ocf, ora_cache, valid, y, y_ctx, tr, dtype):
+def check_layer_step(x64, ctx64, W64, osh, ocf, ora_cache, valid, y, y_ctx, tr, dtype, case=""):
     """Checks one finished layer call (its output y, context output and
     trace) against the oracle step on the exact input x64, with the
     library's in-band choices forced on the oracle.  Returns the oracle's
@@ -232,13 +251,13 @@ def check_layer_step(x64, ctx64, W64, osh, ocf, ora_cache, valid, y, y_ctx, tr, 
     if ctx64 is not None:
         yc = to_f64(y_ctx)
         err, raw = max(err, rel_err(yc, res.y_ctx, dtype)), max(raw, rel_err(yc, res.y_ctx))
-    check_output_bars(err, raw, dtype, "layer output")
+    check_output_bars(err, raw, dtype, "layer output", case)
     st.update(err=err, err_raw=raw)
     return res, st
 
 
 def layer_step_parity(wl, x_np, sh, cf, osh, ocf, cache, ws, ora_cache, valid, ctx_dev=None, ctx64=None,
-                      W=None, W64=None):
+                      W=None, W64=None, case=""):
     """One oc_layer_cached step against the oracle (with in-band forcing).
     Returns the oracle's StepResult and the statistics."""
     W = W or weights_dev(wl)
@@ -246,7 +265,7 @@ def layer_step_parity(wl, x_np, sh, cf, osh, ocf, cache, ws, ora_cache, valid, c
     x = dev_tensor(wl, x_np)
     y, y_ctx, tr = oc.layer_cached(x, W, cache, sh, cf, ctx=ctx_dev, ws=ws, trace=True)
     torch.cuda.synchronize()
-    return check_layer_step(wl.f64(x_np), ctx64, W64, osh, ocf, ora_cache, valid, y, y_ctx, tr, wl.dtype)
+    return check_layer_step(wl.f64(x_np), ctx64, W64, osh, ocf, ora_cache, valid, y, y_ctx, tr, wl.dtype, case)
 
 
 def sampled_outputs(x64, W64, osh, seqs, kept_idx, restore_map, positions, y_prev):

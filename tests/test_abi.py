@@ -85,6 +85,8 @@ WORKLOAD_SHAPES = [
     ("latte_temporal", oc.Shape(16, 16, 16, 1152, 16, 72), oc.Cfg("block", r=0.5)),
     ("svdxt_level", oc.Shape(25, 72, 128, 320, 5, 64), oc.Cfg("frame_token", r=0.5, r_frame=0.2)),
     ("svdxt_level_k4", oc.Shape(25, 72, 128, 320, 5, 64), oc.Cfg("frame_token", r=0.5, r_frame=0.2, patch_k=4)),
+    ("latte_spatial_k2", oc.Shape(16, 16, 16, 1152, 16, 72), oc.Cfg("frame", r_frame=0.25, patch_k=2)),
+    ("latte_spatial_k4", oc.Shape(16, 16, 16, 1152, 16, 72), oc.Cfg("frame", r_frame=0.25, patch_k=4)),
 ]
 
 
@@ -100,6 +102,10 @@ def _oracle_counts(shape, cfg):
     if cfg.gran == "block":
         gs = O.block_groups(s, k, cfg.r)
         return len(gs), len(gs[0].src), len(gs[0].dst), s.N - sum(g.R for g in gs), s.F
+    if cfg.gran == "frame" and k > 1:
+        # per-patch frame groups; F sequences of at most N tokens
+        gs = O.frame_patch_groups(s, k, cfg.r_frame)
+        return len(gs), len(gs[0].src), len(gs[0].dst), s.F, s.N
     if cfg.gran == "frame":
         g = O.frame_group(s, cfg.r_frame)
         return 1, len(g.src), len(g.dst), s.F - g.R, s.N
@@ -158,7 +164,7 @@ GOOD = oc.Shape(1, 8, 8, 32, 2, 16, 0, "bf16")
     (oc.Shape(1, 8, 8, 32, 2, 16, 3, "bf16"), oc.Cfg("block", r=0.5), L.OC_ERR_SHAPE),
     (oc.Shape(1, 8, 8, 32, 2, 16, 0, "bf16"), oc.Cfg("frame", r_frame=0.5), L.OC_ERR_SHAPE),
     (oc.Shape(33, 8, 8, 32, 2, 16, 0, "bf16"), oc.Cfg("frame_token", r=0.5, r_frame=0.2), L.OC_ERR_SHAPE),
-    (oc.Shape(4, 8, 8, 32, 2, 16, 0, "bf16"), oc.Cfg("frame", r_frame=0.2, patch_k=2), L.OC_ERR_SHAPE),
+    (oc.Shape(4, 34, 34, 32, 2, 16, 0, "bf16"), oc.Cfg("frame", r_frame=0.2, patch_k=17), L.OC_ERR_SHAPE),
     (oc.Shape(1, 256, 256, 32, 2, 16, 0, "bf16"), oc.Cfg("token", r=0.5), L.OC_ERR_SHAPE),
 ])
 def test_plan_rejects(shape, cfg, status):

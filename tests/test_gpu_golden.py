@@ -100,3 +100,58 @@ def test_golden_decisions_bit_exact(name, gran, key, dtype):
             _say(f"  {mk} {mapkey}: output error {err:.3g} (raw {raw:.3g})")
             assert err <= TOL[dtype] and raw <= RAW_TOL[dtype]
             prev = res.y
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_golden_frame_patches_bit_exact(dtype):
+    """Frame Cache on 2x2 patches (§3.3) on the hand-worked 4-frame example:
+    per-patch best matches and selections at both ratios, the frame-major
+    kept rows with sequences of 16/4/16/12 and 16/0/16/0 tokens (frames that
+    keep nothing), and both restore maps, bit for bit."""
+    g, x = goldens.load("frame_patch_4x4x4_worked.json", np.float32)
+    F, H, W, C, k = g["F"], g["H"], g["W"], g["C"], g["patch_k"]
+    xp = np.zeros((F, H * W, C_PAD), dtype=np.float32)
+    xp[:, :, :C] = x
+    wl = small_workload("frame", F=F, H=H, W=W, C=C_PAD, heads=1, head_dim=16, dtype=dtype, seed=4)
+    x_np = bf16_bits(xp) if dtype == "bf16" else xp
+    sh = oc.Shape(F, H, W, C_PAD, 1, 16, 0, dtype)
+    x = dev_tensor(wl, x_np)
+    for ratio, cached in g["cached"].items():
+        cf = oc.Cfg("frame", 0.0, float(ratio), k, "matched")
+        ws = oc.workspace(sh, cf, x.device)
+        nm, ni = oc.match(x, sh, cf, ws)
+        kept, cidx, rmap = oc.select(nm, ni, sh, cf, ws)
+        torch.cuda.synchronize()
+        assert nm.shape[0] == k * k
+        for gi, gg in enumerate(g["groups"]):
+            np.testing.assert_array_equal(ni[gi].cpu().numpy(), gg["node_idx"])
+            d = np.abs(nm[gi].cpu().numpy().astype(np.float64) - np.array([goldens.value(s) for s in gg["node_max"]]))
+            assert d.max() <= 2e-6, d
+        assert len(cidx) == len(cached) * (H // k) * (W // k)
+        tiles = set()
+        for p in cidx.cpu().numpy():
+            f, n = divmod(int(p), H * W)
+            y, xx = divmod(n, W)
+            tiles.add(f * H * W + (y // 2) * 2 * W + (xx // 2) * 2)
+        assert tiles == set(cached)
+    W_dev, W64 = weights_dev(wl), weights_f64(wl)
+    osh = O.LayerShape(F, H, W, C_PAD, 1, 16)
+    x64 = wl.f64(x_np).reshape(F, H * W, C_PAD)
+    for mk in ("r0.25", "r0.5"):
+        cf = oc.Cfg("frame", 0.0, float(mk[1:]), k, "matched")
+        ocf = O.CacheCfg("frame", r_frame=cf.r_frame, patch_k=k)
+        ws = oc.workspace(sh, cf, x.device)
+        cache = oc.LayerCache(sh, x.device)
+        prev = None
+        for valid, mapkey in ((False, "restore_map_cold_matched"), (True, "restore_map_valid_cache")):
+            y, _, tr = oc.layer_cached(x, W_dev, cache, sh, cf, ws=ws, trace=True)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(tr["kept_idx"].cpu().numpy(), g[mk]["kept_idx"])
+            np.testing.assert_array_equal(tr["restore_map"].cpu().numpy(), g[mk][mapkey])
+            res = O.layer_step(x64, None, W64, osh, ocf, prev, valid)
+            assert [len(s) for s in res.sequences] == g[mk]["sequence_lengths"]
+            yg = to_f64(y).reshape(res.y.shape)
+            err, raw = rel_err(yg, res.y, dtype), rel_err(yg, res.y)
+            _say(f"  frame patches {mk} {mapkey}: output error {err:.3g} (raw {raw:.3g})")
+            assert err <= TOL[dtype] and raw <= RAW_TOL[dtype]
+            prev = res.y

@@ -34,7 +34,7 @@ def gpu():
     return torch.device("cuda:0")
 
 
-def chain(wl, n_steps, cold="matched", gran=None, r=None, r_frame=None, patch_k=None):
+def chain(wl, n_steps, cold="matched", gran=None, r=None, r_frame=None, patch_k=None, case=""):
     sh, cf, osh, ocf = shapes(wl, gran, r, r_frame, patch_k, cold)
     dev = torch.device("cuda:0")
     ws = oc.workspace(sh, cf, dev)
@@ -46,7 +46,8 @@ def chain(wl, n_steps, cold="matched", gran=None, r=None, r_frame=None, patch_k=
     stats = []
     for s in range(n_steps):
         _say(f"  step {s} of {wl.name} gran={cf.gran} r={cf.r} rf={cf.r_frame} k={cf.patch_k} cold={cold}")
-        res, st = layer_step_parity(wl, wl.steps[s], sh, cf, osh, ocf, cache, ws, ora, valid, ctx_dev, ctx64, W, W64)
+        res, st = layer_step_parity(wl, wl.steps[s], sh, cf, osh, ocf, cache, ws, ora, valid, ctx_dev, ctx64, W, W64,
+                                    case=case)
         _say(f"    {st}")
         stats.append(st)
         ora, valid = res.y, True
@@ -85,6 +86,17 @@ SMALL = [
     # Frame Cache at its largest frame count (32), compacted by the frame
     # stage's final block
     dict(gran="frame", F=32, H=4, W=4, C=64, heads=2, head_dim=32, dtype="bf16", planted=True, r_frame=0.4),
+    # Frame Cache on k x k patches (§3.3): per-patch tile decisions, frames
+    # of varying length; the last case caches every odd tile of every patch
+    # (odd frames keep no token at all)
+    dict(gran="frame", F=8, H=16, W=16, C=64, heads=2, head_dim=32, dtype="bf16", r_frame=0.3, patch_k=2,
+         frame_drift=0.3),
+    dict(gran="frame", F=6, H=8, W=12, C=32, heads=2, head_dim=16, dtype="f32", r_frame=0.34, patch_k=2,
+         frame_drift=0.3),
+    dict(gran="frame", F=9, H=16, W=16, C=64, heads=2, head_dim=64, dtype="bf16", r_frame=0.25, patch_k=4,
+         frame_drift=0.3),
+    dict(gran="frame", F=7, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r_frame=0.45, patch_k=2,
+         frame_drift=0.3),
 ]
 
 
@@ -211,10 +223,11 @@ def test_select_is_exact_on_library_similarities():
     np.testing.assert_array_equal(cached.cpu().numpy(), np.array(sorted(expect)))
 
 
-@pytest.mark.parametrize("gran,F", [("token", 1), ("block", 4), ("frame", 4), ("frame_token", 5)])
-def test_r0_is_bit_identical_to_full_attention(gran, F):
+@pytest.mark.parametrize("gran,F,k", [("token", 1, 1), ("block", 4, 1), ("frame", 4, 1), ("frame_token", 5, 1),
+                                      ("frame", 4, 2)])
+def test_r0_is_bit_identical_to_full_attention(gran, F, k):
     wl = small_workload(gran, F=F, H=16, W=16, C=64, heads=2, head_dim=32, dtype="bf16", seed=21)
-    sh, cf, osh, ocf = shapes(wl, r=0.0, r_frame=0.0)
+    sh, cf, osh, ocf = shapes(wl, r=0.0, r_frame=0.0, patch_k=k)
     dev = torch.device("cuda:0")
     x = dev_tensor(wl, wl.steps[0])
     ws = oc.workspace(sh, cf, dev)
@@ -329,6 +342,16 @@ def test_latte_spatial_chain():
     choices; the maps and outputs are then checked in full."""
     wl = make_workload("latte_spatial", 3)
     chain(wl, 3)
+
+
+@pytest.mark.parametrize("k", [2, 4])
+def test_latte_spatial_frame_patches_chain(k):
+    """The Latte-like spatial layer with Frame Cache on k x k patches (§3.3):
+    per-patch tile decisions and frames of varying length, three steps in
+    full.  Frames that keep one or two patches have outputs far above the
+    layer's RMS, so the raw bar is the one listed for these chains."""
+    wl = make_workload("latte_spatial", 3)
+    chain(wl, 3, patch_k=k, case=f"latte_spatial frame patches k{k}")
 
 
 def test_latte_temporal_chain():
