@@ -419,6 +419,38 @@ def run_k_sweep(args):
     return out
 
 
+def run_frame_patch_sweep(args):
+    """Frame Cache scope on the Latte-like spatial layer (§3.3): whole-frame
+    matching (k = 1) against per-patch matching on 2x2 and 4x4 patches
+    (k = 2, 4; frames then keep varying numbers of tokens), r_f = 0.25: the
+    step, its matching-stage kernels and the retained token count."""
+    import torch
+    import paper_2607_23844_amd as oc
+    from paper_2607_23844_amd.runner import LayerRunner
+    from oc_synth import make_workload
+
+    dev = torch.device("cuda:0")
+    K = args.cfg_steps
+    wl = make_workload("latte_spatial", 3)
+    shape = oc.Shape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, 0, "bf16")
+    xs = [_bf16_dev(s, dev) for s in wl.steps]
+    W = {k: _bf16_dev(getattr(wl, k), dev) for k in ("wq", "wk", "wv", "wo")}
+    out = {}
+    for k in (1, 2, 4):
+        cfg = oc.Cfg("frame", r_frame=0.25, patch_k=k)
+        run = LayerRunner(shape, cfg, W, dev)
+        run(xs[0])
+        ms = timed_ms(run, xs[1:], K, 3)
+        st = stage_times(run, xs[1:], K)
+        match_stages = ("frame_gram", "frame_reduce", "frame_final", "inv_norm", "match", "select", "compact")
+        out[str(k)] = dict(groups=oc.plan(shape, cfg).n_groups, step_us=round(ms * 1e3, 2),
+                           matching_us=round(sum(st[n][0] for n in match_stages if n in st) * 1e3 / K, 3),
+                           stages_us={n: round(v[0] * 1e3 / max(v[1], 1), 3) for n, v in st.items()},
+                           retained_tokens=oc.plan(shape, cfg).n_kept)
+        del run
+    return out
+
+
 def run_layered(args):
     """Layered Cache schedule proposal (Alg. 1) on SD3-shaped synthetic
     tables (24 blocks x 28 steps): host time of oc_layered_schedule and the
@@ -687,6 +719,7 @@ def main():
         extra["ffn_sd3"] = run_ffn(args)
         extra["blocks"] = run_blocks(args)
         extra["group_count_sweep_sd3"] = run_k_sweep(args)
+        extra["frame_patch_sweep_latte"] = run_frame_patch_sweep(args)
         extra["layered_schedule"] = run_layered(args)
     cpu = None if (args.no_cpu or args.only) else run_cpu_baselines(args)
     ms = g["ms"]
