@@ -72,7 +72,7 @@ __device__ __forceinline__ int lds_chunk(int r, int c) {
     return DMA ? r * LD + (dma_slot<LD>(r, c) << 3) : r * LD + (c << 3);
 }
 
-template <int DH, int NW, bool DMA>
+template <int DH, int NW, bool DMA, bool VARLEN = false>
 __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                                                     const uint16_t *__restrict__ Vt, uint16_t *__restrict__ O,
                                                     int hd, int heads, int n_seq, int L, int Lk, int lpad,
@@ -91,7 +91,7 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
     const int qt = lid % n_qt, hs = lid / n_qt, h = hs % heads, s = hs / heads;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, ln = lane & 31, lg = lane >> 5;
     long row0 = (long)s * L;
-    if (seq_off != nullptr) {
+    if constexpr (VARLEN) {
         // sequences of varying length: this sequence's rows and key count;
         // query tiles past its end leave at once (the whole block)
         row0 = seq_off[s];
@@ -534,14 +534,14 @@ static hipError_t go_short(const Plan &p, const AttnArgs &a, int Lk, hipStream_t
     return hipGetLastError();
 }
 
-template <int DH, int NW, bool DMA>
+template <int DH, int NW, bool DMA, bool VARLEN = false>
 static hipError_t go(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
     const int n_qt = cdiv(Lk, 32 * NW);
     const int total = n_qt * p.heads * a.n_seq;
     const size_t lds = FlashCfg<DH, DMA>::LDS_BYTES;
-    const hipError_t e = raise_lds_limit((const void *)k_flash<DH, NW, DMA>, lds);
+    const hipError_t e = raise_lds_limit((const void *)k_flash<DH, NW, DMA, VARLEN>, lds);
     if (e != hipSuccess) return e;
-    launch_k(k_flash<DH, NW, DMA>, total, NW * 64, lds, st, (const uint16_t *)a.q, (const uint16_t *)a.k,
+    launch_k(k_flash<DH, NW, DMA, VARLEN>, total, NW * 64, lds, st, (const uint16_t *)a.q, (const uint16_t *)a.k,
                                                       (const uint16_t *)a.vt, (uint16_t *)a.o, p.hd, p.heads,
                                                       a.n_seq, a.L, Lk, a.lpad, n_qt, a.seq_off);
     return hipGetLastError();
@@ -554,7 +554,7 @@ template <int DH>
 static hipError_t go_dh(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
     // sequences of varying length: the register-staged kernel, which masks
     // every sequence's end itself (Lk is the longest)
-    if (a.seq_off != nullptr) return go<DH, 4, false>(p, a, Lk, st);
+    if (a.seq_off != nullptr) return go<DH, 4, false, true>(p, a, Lk, st);
     if (attn_short(Lk)) return Lk <= 32 ? go_short<DH, 1>(p, a, Lk, st) : go_short<DH, 2>(p, a, Lk, st);
     if constexpr (DH % 64 == 0) {
         if (flash_uses_dma(DH, Lk, p.hd)) {

@@ -66,7 +66,7 @@ struct QKVShape<true, SH> {
 template <bool DMA, int SH = 0>
 using QKVTile = typename QKVShape<DMA, SH>::Tile;
 
-template <bool DMA, int SH>
+template <bool DMA, int SH, bool VARLEN>
 __global__ __launch_bounds__(256) void k_proj_qkv(RowMap rm, const uint16_t *__restrict__ wq,
                                                   const uint16_t *__restrict__ wk, const uint16_t *__restrict__ wv,
                                                   int hd, int dh, float qscale, int nw, int n_qk_at, int n_bt,
@@ -123,7 +123,7 @@ __global__ __launch_bounds__(256) void k_proj_qkv(RowMap rm, const uint16_t *__r
     run_tile(t, lds, rowsA, rowsB, rm.row(0), wv, rm.C, Rows{});
     const int Lk = n_seq == 1 ? rm.n_rows : L;
     const int r0 = at * BA, f0 = bt * BB;
-    if (seq_off == nullptr && (n_seq == 1 || L % BA == 0)) {
+    if (!VARLEN && (n_seq == 1 || L % BA == 0)) {
         const int s = n_seq == 1 ? 0 : r0 / L, j0 = r0 - s * L;   // j0 is a multiple of BA
         stage_rows<BA>(t, lds, [&](float v, int a) { return (uint16_t)(j0 + a < Lk ? f2h_bits(v) : 0); },
                        [](int a) { return vt_key_of_pos(a); });
@@ -150,14 +150,14 @@ __global__ __launch_bounds__(256) void k_proj_qkv(RowMap rm, const uint16_t *__r
                     const int r = r0 + T::a_of(i, g) + e;
                     if (r >= rm.n_rows) continue;
                     int s, jj;
-                    seq_pos(r, n_seq, L, s, jj, seq_off);
+                    seq_pos(r, n_seq, L, s, jj, VARLEN ? seq_off : nullptr);
                     Vt[(((long)h * n_seq + s) * dh + d) * lpad + vt_key_of_pos(jj)] = f2h_bits(t.acc[i][j][4 * g + e]);
                 }
     }
     // zero the padded key positions [Lk, lpad) of this block's features, for
     // the sequences s = at, at + n_v_at, ... (the DMA-staged attention reads them)
     const int npad = lpad - Lk;
-    if (zero_pad && npad > 0 && seq_off == nullptr) {
+    if (!VARLEN && zero_pad && npad > 0) {
         for (int sq = at; sq < n_seq; sq += n_v_at)
             for (int idx = threadIdx.x; idx < BB * npad; idx += blockDim.x) {
                 const int f = f0 + idx / npad, jj = Lk + idx % npad;
@@ -173,32 +173,27 @@ static long qkv_tiles(const Plan &p, int rows, int nw, int BA, int BB) {
     return (long)cdiv(nw * p.hd, BA) * cdiv(rows, BB) + (nw == 3 ? 0L : (long)cdiv(rows, BA) * cdiv(p.hd, BB));
 }
 
-template <bool DMA, int SH>
+template <bool DMA, int SH, bool VARLEN>
 static hipError_t launch_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, float qscale, int nw, int zero_pad,
                              hipStream_t st) {
     constexpr int BA = QKVShape<DMA, SH>::BA, BB = QKVShape<DMA, SH>::BB;
-    const hipError_t e = allow_lds(k_proj_qkv<DMA, SH>, QKVTile<DMA, SH>::LDS_BYTES);
+    const hipError_t e = allow_lds(k_proj_qkv<DMA, SH, VARLEN>, QKVTile<DMA, SH>::LDS_BYTES);
     if (e != hipSuccess) return e;
     const int n_qk_at = cdiv(nw * p.hd, BA), n_bt = cdiv(rm.n_rows, BB);
     const int n_v_at = nw == 3 ? 0 : cdiv(rm.n_rows, BA), n_v_bt = nw == 3 ? 0 : cdiv(p.hd, BB);
     const int total = n_qk_at * n_bt + n_v_at * n_v_bt;
-    launch_k(k_proj_qkv<DMA, SH>, total, 256, QKVTile<DMA, SH>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
+    launch_k(k_proj_qkv<DMA, SH, VARLEN>, total, 256, QKVTile<DMA, SH>::LDS_BYTES, st, rm, (const uint16_t *)a.wq,
              (const uint16_t *)a.wk, (const uint16_t *)a.wv, p.hd, p.dh, qscale, nw, n_qk_at, n_bt, n_v_at, n_v_bt,
              a.n_seq, a.L, a.lpad, zero_pad, a.seq_off, (uint16_t *)a.q, (uint16_t *)a.k, (uint16_t *)a.vt);
     return hipGetLastError();
 }
 
-hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, hipStream_t st) {
-    const float qscale = (float)(1.4426950408889634 / sqrt((double)p.dh));
-    StageScope _stage(st, "proj_qkv");
-    const int Lk = a.n_seq == 1 ? rm.n_rows : a.L;
-    // sequences of varying length: Vt slots per sequence, filled element by
-    // element; the attention masks their ends itself (no padding to zero)
-    const bool varlen = a.seq_off != nullptr;
-    const int zero_pad = !varlen && flash_uses_dma(p.dh, Lk, p.hd) ? 1 : 0;
-    // short sequences: V rows from the Q/K tiles (nw = 3), no V tiles
-    const int nw = !varlen && attn_short(Lk) ? 3 : 2;
-    if (p.C % 64 != 0) return launch_qkv<false, 0>(p, rm, a, qscale, nw, zero_pad, st);
+// Tile shape by block rounds; V: sequences of varying length (a separate
+// instance, so that the uniform kernels carry none of its code)
+template <bool V>
+static hipError_t launch_shape(const Plan &p, const RowMap &rm, const AttnArgs &a, float qscale, int nw,
+                               int zero_pad, hipStream_t st) {
+    if (p.C % 64 != 0) return launch_qkv<false, 0, V>(p, rm, a, qscale, nw, zero_pad, st);
     // block rounds (two blocks per CU) times the work of one tile, a wide
     // tile being 1.5 units (the SD3-like layer at r = 0.5: 460 tiles of 192 x
     // 128 in one round, 44 us, against 684 of 128 x 128 in two, 51 us; one
@@ -211,9 +206,23 @@ hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, h
     const long c192a = 3 * ((qkv_tiles(p, rm.n_rows, nw, 192, 128) + slots - 1) / slots);
     const long c192b = 3 * ((qkv_tiles(p, rm.n_rows, nw, 128, 192) + slots - 1) / slots);
     const bool rows192 = nw == 3 || a.n_seq == 1 || a.L % 192 == 0;
-    if (rows192 && c192a < c128 && c192a <= c192b) return launch_qkv<true, 1>(p, rm, a, qscale, nw, zero_pad, st);
-    if (c192b < c128) return launch_qkv<true, 2>(p, rm, a, qscale, nw, zero_pad, st);
-    return launch_qkv<true, 0>(p, rm, a, qscale, nw, zero_pad, st);
+    if (rows192 && c192a < c128 && c192a <= c192b) return launch_qkv<true, 1, V>(p, rm, a, qscale, nw, zero_pad, st);
+    if (c192b < c128) return launch_qkv<true, 2, V>(p, rm, a, qscale, nw, zero_pad, st);
+    return launch_qkv<true, 0, V>(p, rm, a, qscale, nw, zero_pad, st);
+}
+
+hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, hipStream_t st) {
+    const float qscale = (float)(1.4426950408889634 / sqrt((double)p.dh));
+    StageScope _stage(st, "proj_qkv");
+    const int Lk = a.n_seq == 1 ? rm.n_rows : a.L;
+    // sequences of varying length: Vt slots per sequence, filled element by
+    // element; the attention masks their ends itself (no padding to zero)
+    const bool varlen = a.seq_off != nullptr;
+    const int zero_pad = !varlen && flash_uses_dma(p.dh, Lk, p.hd) ? 1 : 0;
+    // short sequences: V rows from the Q/K tiles (nw = 3), no V tiles
+    const int nw = !varlen && attn_short(Lk) ? 3 : 2;
+    return varlen ? launch_shape<true>(p, rm, a, qscale, nw, zero_pad, st)
+                  : launch_shape<false>(p, rm, a, qscale, nw, zero_pad, st);
 }
 
 // ---------------------------------------------------------------------------
