@@ -128,25 +128,30 @@ def roofline_of(flop, nbytes, avg_us):
 def kernel_table(stages, K, work, workload):
     """Per-stage live timing (HIP events stamped at each kernel's start and
     end) with its roofline where the stage has algorithmic work, and the
-    roofline object of the dominant stage (largest time)."""
+    roofline object of the dominant stage (largest time).  A stage may run
+    several kernels per call (split-K similarity and its reduction, the two
+    compaction passes): avg_us is the mean kernel launch, us_per_step the
+    stage's time per call, which the roofline and traffic figures use."""
     kernels = {}
     for name, (tot_ms, n) in stages.items():
         avg_us = tot_ms * 1e3 / max(n, 1)
-        d = dict(avg_us=round(avg_us, 3), launches_per_step=round(n / K, 3))
+        step_us = tot_ms * 1e3 / K
+        d = dict(avg_us=round(avg_us, 3), launches_per_step=round(n / K, 3), us_per_step=round(step_us, 3))
         tr = kernel_traffic(name, workload)
         if tr is not None:
             d["traffic"] = tr
         if name in work and (work[name][0] > 0 or work[name][1] > 0):
-            d.update(roofline_of(work[name][0], work[name][1], avg_us))
+            d.update(roofline_of(work[name][0], work[name][1], step_us))
         kernels[name] = d
     dom = max(stages, key=lambda s: stages[s][0])
     roof = None
     if dom in work:
-        avg_us = stages[dom][0] * 1e3 / max(stages[dom][1], 1)
+        step_us = stages[dom][0] * 1e3 / K
         flop, nbytes = work[dom]
-        roof = dict(kernel=dom, **roofline_of(flop, nbytes, avg_us), traffic=kernel_traffic(dom, workload),
-                    avg_us=round(avg_us, 3),
-                    algorithmic_per_launch=flop if roofline_of(flop, nbytes, avg_us)["bound"] == "mfma" else nbytes)
+        r = roofline_of(flop, nbytes, step_us)
+        roof = dict(kernel=dom, **r, traffic=kernel_traffic(dom, workload), avg_us=round(step_us, 3),
+                    launches_per_step=round(stages[dom][1] / K, 3),
+                    algorithmic_per_launch=flop if r["bound"] == "mfma" else nbytes)
     return kernels, roof
 
 

@@ -1,11 +1,12 @@
-"""ctypes view of include/oc.h.  Loads the in-tree liboc.so and fails loudly
-if it has not been built: there is no fallback implementation."""
+"""ctypes view of include/oc.h.  Loads the in-tree liboc.so (or the build
+that OC_LIBRARY names, such as the host-sanitized liboc_asan.so) and fails
+loudly if it has not been built: there is no fallback implementation."""
 from __future__ import annotations
 
 import ctypes as C
 import os
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liboc.so")
+LIB_PATH = os.environ.get("OC_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "liboc.so")
 
 OC_OK, OC_ERR_INVALID_ARG, OC_ERR_SHAPE, OC_ERR_DTYPE, OC_ERR_WORKSPACE, OC_ERR_CACHE_STATE, OC_ERR_HIP = range(7)
 OC_F32, OC_BF16 = 0, 1
