@@ -182,8 +182,11 @@ def step_percentiles(fn, inputs, K):
                 p90_us=round(float(np.percentile(d, 90)), 2))
 
 
-def graph_latency(run, x, K):
-    """Mean latency (µs) of a warm step captured once in a HIP graph and replayed K times."""
+def graph_latency(run, x, K, pairs=4):
+    """A warm step captured once in a HIP graph, against the same step
+    launched eagerly: {graph_us, eager_us}, medians over `pairs` interleaved
+    blocks of K replays and K eager calls (the clock settles over the first
+    blocks, so the two are compared in the same phase of the run)."""
     import torch
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
@@ -200,13 +203,23 @@ def graph_latency(run, x, K):
     for _ in range(3):
         g.replay()
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(K):
-        g.replay()
-    e1.record()
-    torch.cuda.synchronize()
-    return round(e0.elapsed_time(e1) * 1e3 / K, 2)
+
+    def block(fn):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(K):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / K
+
+    gs, es = [], []
+    for _ in range(pairs):
+        es.append(block(lambda: run(x)))
+        gs.append(block(g.replay))
+    gs.sort()
+    es.sort()
+    return dict(graph_us=round(gs[len(gs) // 2], 2), eager_us=round(es[len(es) // 2], 2))
 
 
 def timed_ms(fn, inputs, K, W):
@@ -750,7 +763,8 @@ def main():
         },
         "latency_us": round(ms * 1e3, 2),
         "latency_pct_us": g["pct"],
-        "graph_latency_us": g["graph_us"],
+        "graph_latency_us": g["graph_us"]["graph_us"],
+        "graph_vs_eager_interleaved_us": g["graph_us"],
         "uncached_latency_us": round(g["full_ms"] * 1e3, 2),
         "speedup_vs_uncached": round(g["full_ms"] / ms, 4),
         "by_r": {k: {kk: round(vv, 4) for kk, vv in v.items()} for k, v in g["by_r"].items()},

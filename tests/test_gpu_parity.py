@@ -201,6 +201,38 @@ def test_gather_restore_bit_exact():
     np.testing.assert_array_equal(c2.view(torch.int16).cpu().numpy().reshape(-1, sh.C), ref)
 
 
+@pytest.mark.parametrize("dtype,F,H,W,C", [
+    ("bf16", 1, 64, 64, 1536),   # 48 units of 4 chunks per row: 16 positions per block
+    ("bf16", 3, 37, 61, 320),    # 10 units per row: 64 positions per block, ragged last block
+    ("bf16", 2, 13, 11, 24),     # rows of 3 chunks, one chunk per unit: 256 positions per block
+    ("f32", 1, 9, 9, 40),        # 10 one-chunk units per row, a single partial block
+    ("f32", 2, 16, 16, 64),      # 4 units of 4 chunks per row
+])
+def test_restore_in_place_bit_exact(dtype, F, H, W, C):
+    """In-place restoration (cached positions keep their values) moves only
+    the positions whose map names a row of y_kept; every other map value
+    (-1, -2, negative, at or past n_rows) leaves the position untouched, with
+    the cache as the output and with no cache at all."""
+    rng = np.random.default_rng(F * 1000 + C)
+    n_pos = F * H * W
+    n_rows = max(1, int(0.4 * n_pos))
+    sh = oc.Shape(F, H, W, C, 1, 16, 0, dtype)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    m = rng.integers(-3, n_rows + 3, size=n_pos).astype(np.int32)
+    rmap = torch.from_numpy(m).cuda()
+    yk = torch.randn((n_rows, C), device="cuda").to(tdt)
+    base = torch.randn((F, H * W, C), device="cuda").to(tdt)
+    iview = torch.int16 if dtype == "bf16" else torch.int32
+    ref = base.view(iview).cpu().numpy().reshape(n_pos, C).copy()
+    fresh = (m >= 0) & (m < n_rows)
+    ref[fresh] = yk.view(iview).cpu().numpy()[m[fresh]]
+    for with_cache in (True, False):
+        y = base.clone()
+        oc.restore(yk, rmap, sh, cache_y=y if with_cache else None, y=y)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(y.view(iview).cpu().numpy().reshape(n_pos, C), ref)
+
+
 def test_select_is_exact_on_library_similarities():
     """The selection kernel is integer work: given the library's own fp32
     node_max, its cached set equals the definition (largest first, smallest id
