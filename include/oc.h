@@ -22,9 +22,11 @@
  *    wq, wk, wv are [heads*head_dim, C] and wo is [C, heads*head_dim];
  *    q = x wq^T etc.  Same element type as x.
  *  - All device pointers are caller-owned device memory, 16-byte aligned.
- *    The library allocates no device memory and keeps no device state;
- *    scratch space is the caller's workspace of at least
- *    oc_plan_info.workspace_bytes.  Its only shared host state is a
+ *    The library allocates no device memory and keeps no device state
+ *    between calls; scratch space is the caller's workspace of at least
+ *    oc_plan_info.workspace_bytes.  The one exception is
+ *    oc_layer_cached_static, whose scratch is a static device array of the
+ *    library (see there).  Its only shared host state is a
  *    mutex-guarded record of the kernels whose dynamic-LDS limit it has
  *    raised on each device (plus the thread-local error message and stage
  *    timer), so concurrent calls from several threads are safe.
