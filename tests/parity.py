@@ -93,6 +93,10 @@ RAW_EXCEPTIONS = {
     # 0.0014-0.0018
     "latte_spatial frame patches k2": (0.0283, 0.035),
     "latte_spatial frame patches k4": (0.0280, 0.035),
+    # 2 sequences of 1000 tokens, 3 heads of 32: the peak output (5.95 times
+    # the RMS) lies just below a power of two, where half a bf16 ulp is
+    # 0.0198 of the RMS; measured raw 0.0224, rounding-adjusted 0.0026
+    "attn bf16 dh32 2x1000+0": (0.0224, 0.03),
 }
 
 

@@ -97,6 +97,12 @@ SMALL = [
          frame_drift=0.3),
     dict(gran="frame", F=7, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r_frame=0.45, patch_k=2,
          frame_drift=0.3),
+    # degenerate grids: one 2x2 window (three candidates, one representative),
+    # two frames (one candidate frame), and a bf16 channel count that is not a
+    # multiple of 64 (register-staged tiles instead of the DMA engine)
+    dict(gran="token", F=1, H=2, W=2, C=16, heads=1, head_dim=16, dtype="bf16", r=0.5),
+    dict(gran="frame", F=2, H=4, W=4, C=32, heads=2, head_dim=16, dtype="bf16", r_frame=0.6, planted=True),
+    dict(gran="token", F=1, H=8, W=12, C=40, heads=1, head_dim=16, dtype="bf16", n_ctx=2),
 ]
 
 
@@ -148,6 +154,9 @@ def test_heavy_tailed_activations_chain(gran, head_dim, F, scale):
     # whole sequences (ragged last tile; 2, 3, 5 and 128 sequences per tile)
     ("bf16", 64, 7, 25, 0), ("bf16", 64, 5, 64, 0), ("bf16", 64, 4, 33, 0), ("bf16", 64, 130, 1, 0), ("bf16", 72, 5, 77, 0), ("bf16", 72, 7, 16, 0),
     ("bf16", 16, 2, 9, 0), ("bf16", 128, 1, 200, 5), ("f32", 64, 1, 128, 0), ("f32", 16, 3, 33, 0),
+    # the other supported head dims, long and short sequences
+    ("bf16", 32, 2, 1000, 0), ("bf16", 48, 3, 100, 0), ("bf16", 80, 2, 150, 0), ("bf16", 96, 2, 300, 0),
+    ("bf16", 128, 3, 40, 0), ("bf16", 96, 1, 70, 3),
 ])
 def test_attn_reduced_vs_oracle(dtype, dh, n_seq, L, n_ctx):
     _say(f"attn_reduced {dtype} dh={dh} n_seq={n_seq} L={L} n_ctx={n_ctx}")
