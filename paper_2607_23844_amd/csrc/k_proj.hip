@@ -229,12 +229,18 @@ hipError_t launch_proj_qkv(const Plan &p, const RowMap &rm, const AttnArgs &a, h
 // Output projection: a in [0, C) = rows of wo (fp16); b = batch rows of O.
 // y[out row][a].
 // ---------------------------------------------------------------------------
-// Tiles (double-buffered DMA): 128 output features x 64 rows; for C a
-// multiple of 160 but not of 128 (e.g. 320) 160 features x 128 rows (one
-// wave row of four), so that no feature column is computed in vain.
+// Tiles (double-buffered DMA): 128 output features x 64 rows, or 64 x 64
+// where the 128 x 64 grid would give fewer than 1.5 blocks per CU (the
+// SD3-like layer at r = 0.75, 1357 rows: 528 small blocks instead of 264,
+// 2.4 us less per step; at r = 0.5 and 0.25 the 128-wide tiles are faster);
+// for C a multiple of 160 but not of 128 (e.g. 320) 160 features x 128 rows
+// (one wave row of four), so that no feature column is computed in vain.
 template <bool DMA, int BA = 128>
 using OTile = typename std::conditional<
-    DMA, typename std::conditional<BA == 160, DmaTile<160, 128, 1, 4, true, 2>, DmaTile<128, 64, 2, 2, true, 2>>::type,
+    DMA,
+    typename std::conditional<
+        BA == 160, DmaTile<160, 128, 1, 4, true, 2>,
+        typename std::conditional<BA == 64, DmaTile<64, 64, 2, 2, true, 2>, DmaTile<128, 64, 2, 2, true, 2>>::type>::type,
     MfmaTile<128, 128, 2, 2, true, false>>::type;
 
 template <bool DMA, int BA>
@@ -298,6 +304,8 @@ hipError_t launch_proj_out(const Plan &p, int n_rows, const AttnArgs &a, hipStre
             hipError_t e = allow_lds(k_proj_out<true, 160>, OTile<true, 160>::LDS_BYTES);
             if (e != hipSuccess) return e;
             go(k_proj_out<true, 160>, OTile<true, 160>::LDS_BYTES, 160, 128);
+        } else if (2L * cdiv(p.C, 128) * cdiv(n_rows, 64) < 3L * N_CUS) {
+            go(k_proj_out<true, 64>, OTile<true, 64>::LDS_BYTES, 64, 64);
         } else {
             hipError_t e = allow_lds(k_proj_out<true, 128>, OTile<true, 128>::LDS_BYTES);
             if (e != hipSuccess) return e;
