@@ -32,7 +32,9 @@ constexpr int SEL_SMALL = 512, SEL_LARGE = 1024;
 // ones go to cached_idx[g*Rc...] (Rc = the frame's static budget).  Block
 // Cache (tF = F > 0, one group of all N positions): the b-th retained
 // position becomes sequence b (rows b*F + f, token f*N + n), cached
-// positions ascend frame-major in cached_idx[f*Rc + rank].
+// positions ascend frame-major in cached_idx[f*Rc + rank].  The per-token
+// flag / mtok arrays are written only when given: a compacting warm step
+// passes none, since only the cold "matched" mapping reads them then.
 template <bool PACKED, int SEL_THREADS>
 __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict__ node_max_in,
                                                         const int32_t *__restrict__ node_idx_in,
@@ -267,15 +269,19 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
         if (j >= ipt || i >= n_src) continue;
         const bool c = all || (!none && cbyte[i] != 0);
         const int id = sids[j];
-        flag[id] = c ? 1 : 0;
-        mtok[id] = c ? nid[j] : -1;
+        if (flag != nullptr) {
+            flag[id] = c ? 1 : 0;
+            mtok[id] = c ? nid[j] : -1;
+        }
         if (compact) fl[id - fbase] = c ? 1 : 0;
     }
     for (int i = t; i < D; i += SEL_THREADS) {
         const int id = gm.dst_id(gr, i);
         if (id >= 0) {
-            flag[id] = 0;
-            mtok[id] = -1;
+            if (flag != nullptr) {
+                flag[id] = 0;
+                mtok[id] = -1;
+            }
             if (compact) fl[id - fbase] = 0;
         }
     }

@@ -297,9 +297,14 @@ oc_status run_select(const Plan &p, const Layout &L, float *node_max, int32_t *n
     const int32_t *units = units_of(p, L, ws);
     if (from_pack && p.kind != KIND_FRAME) {
         const bool fused = select_compacts(p);
+        // the per-token flags and matches stay in the workspace only where
+        // something reads them: the separate compaction, or the cold
+        // "matched" mapping after the fused one
+        const bool flags = !fused || map_matched;
         HIP_TRY(launch_select_packed(p, units, at<unsigned long long>(ws, L.node_pack), at<float>(ws, L.inv),
-                                     node_max, node_idx, at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok),
-                                     fused ? kept : nullptr, fused ? cached : nullptr, fused ? rmap : nullptr, st),
+                                     node_max, node_idx, flags ? at<int32_t>(ws, L.flag) : nullptr,
+                                     flags ? at<int32_t>(ws, L.mtok) : nullptr, fused ? kept : nullptr,
+                                     fused ? cached : nullptr, fused ? rmap : nullptr, st),
                 "select");
         if (fused) {
             if (map_matched)
