@@ -48,14 +48,29 @@ __global__ void k_inv_norm(const T *__restrict__ x, float *__restrict__ inv, int
         const int item = blockIdx.x;
         const int cpr = C / VEC;
         float ss = 0.f;
-        for (int q = threadIdx.x; q < n_sub * cpr; q += blockDim.x) {
-            const int sg = q / cpr, c = (q - sg * cpr) * VEC;
-            const uint4 v = *reinterpret_cast<const uint4 *>(x + sg * sub_stride + (long)item * C + c);
-            const T *e = reinterpret_cast<const T *>(&v);
+        const int nq = n_sub * cpr;
+        // four chunks' loads in flight before their sums (same order of
+        // accumulation as one chunk at a time)
+        for (int q0 = threadIdx.x; q0 < nq; q0 += 4 * blockDim.x) {
+            // (a chunk past the end re-reads the last one, unbranched, and
+            // its sum is dropped)
+            uint4 v[4];
 #pragma unroll
-            for (int j = 0; j < VEC; ++j) {
-                const float f = Elem<T>::ld(e + j);
-                ss = fmaf(f, f, ss);
+            for (int u = 0; u < 4; ++u) {
+                const int q = min(q0 + u * (int)blockDim.x, nq - 1);
+                const int sg = q / cpr, c = (q - sg * cpr) * VEC;
+                v[u] = *reinterpret_cast<const uint4 *>(x + sg * sub_stride + (long)item * C + c);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const T *e = reinterpret_cast<const T *>(&v[u]);
+                float part = ss;
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) {
+                    const float f = Elem<T>::ld(e + j);
+                    part = fmaf(f, f, part);
+                }
+                ss = q0 + u * (int)blockDim.x < nq ? part : ss;
             }
         }
         ss = wave_sum(ss);
@@ -75,13 +90,26 @@ __global__ void k_inv_norm(const T *__restrict__ x, float *__restrict__ inv, int
     if (item >= n_items) return;   // (whole lane groups: the reduction below stays inside one)
     const T *row = x + (long)item * C;
     float ss = 0.f;
-    for (int c = sub * VEC; c < C; c += lpi * VEC) {
-        const uint4 v = *reinterpret_cast<const uint4 *>(row + c);
-        const T *e = reinterpret_cast<const T *>(&v);
+    // up to four chunks' loads in flight before their sums (same order of
+    // accumulation as one chunk at a time)
+    const int step = lpi * VEC;
+    for (int c0 = sub * VEC; c0 < C; c0 += 4 * step) {
+        // (a chunk past the end re-reads the last one, unbranched, and its
+        // sum is dropped)
+        uint4 v[4];
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) {
-            const float f = Elem<T>::ld(e + j);
-            ss = fmaf(f, f, ss);
+        for (int u = 0; u < 4; ++u)
+            v[u] = *reinterpret_cast<const uint4 *>(row + min(c0 + u * step, C - VEC));
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const T *e = reinterpret_cast<const T *>(&v[u]);
+            float part = ss;
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) {
+                const float f = Elem<T>::ld(e + j);
+                part = fmaf(f, f, part);
+            }
+            ss = c0 + u * step < C ? part : ss;
         }
     }
     for (int o = lpi >> 1; o > 0; o >>= 1) ss += __shfl_xor(ss, o, WAVE);
