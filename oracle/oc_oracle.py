@@ -128,6 +128,8 @@ class CacheCfg:
     r_frame: float = 0.0      # frame ratio r_f
     patch_k: int = 1          # k x k patch-local matching (§3.3)
     cold: str = COLD_MATCHED  # reading R9
+    coarse_k: int = 0         # second, coarser level of the hierarchy (R23): 0 none
+    r_coarse: float = 0.0     # its ratio
 
 
 @dataclass
@@ -450,16 +452,59 @@ def decide(x: np.ndarray, shape: LayerShape, cfg: CacheCfg, no_skip: bool = Fals
         raise ValueError(cfg.gran)
 
     node_max, node_idx, cached = [], [], []
-    for g in groups:
-        if len(g.src) == 0:
-            nm, ni = np.zeros(0), np.zeros(0, dtype=np.int64)
-        else:
-            _, (nm, ni) = _match_group(x, g, shape, k)
-        node_max.append(nm)
-        node_idx.append(np.asarray(ni, dtype=np.int64))
-        cached.append(select_cached(nm, g.src, g.R))
+
+    def match_and_select(level_groups, kk):
+        for g in level_groups:
+            if len(g.src) == 0:
+                nm, ni = np.zeros(0), np.zeros(0, dtype=np.int64)
+            else:
+                _, (nm, ni) = _match_group(x, g, shape, kk)
+            node_max.append(nm)
+            node_idx.append(np.asarray(ni, dtype=np.int64))
+            cached.append(select_cached(nm, g.src, g.R))
+
+    match_and_select(groups, k)
+    if cfg.coarse_k:
+        force = forced.get("cached")
+        if force is not None:
+            # a forced selection fixes the first level before the second is
+            # formed from what it left
+            cached = [_forced_in(g, force) for g in groups]
+        n1 = len(groups)
+        groups = groups + coarse_groups(shape, cfg, set(i for c in cached for i in c),
+                                        0.0 if no_skip else cfg.r_coarse)
+        match_and_select(groups[n1:], cfg.coarse_k)
+        if force is not None:
+            cached = cached[:n1] + [_forced_in(g, force) for g in groups[n1:]]
+        dec = Decisions(groups, node_max, node_idx, cached, **dec_frame)
+        return force_decisions(dec, None, forced.get("match"))
     dec = Decisions(groups, node_max, node_idx, cached, **dec_frame)
     return force_decisions(dec, forced.get("cached"), forced.get("match"))
+
+
+def _forced_in(g: Group, cached: set) -> List[int]:
+    c = sorted(i for i in g.src if i in cached)
+    assert len(c) == g.R, "forced selection must keep the group's budget"
+    return c
+
+
+def coarse_groups(shape: LayerShape, cfg: CacheCfg, cached_first: set, ratio: float) -> List[Group]:
+    """The second, coarser level of the hierarchy (§3.3, reading R23): the
+    groups of coarse_k x coarse_k patches, each a union of first-level
+    patches; their candidates are those the first level did not cache,
+    their representatives the same top-left items, and each caches
+    min(floor(r_coarse * items), remaining candidates)."""
+    if cfg.gran not in (TOKEN, BLOCK):
+        raise ValueError("a coarser level is defined for Token and Block Cache")
+    if not (1 <= cfg.coarse_k < cfg.patch_k and cfg.patch_k % cfg.coarse_k == 0):
+        raise ValueError("coarse_k must divide patch_k and be smaller")
+    base = token_groups(shape, cfg.coarse_k, range(shape.F), ratio) if cfg.gran == TOKEN else \
+        block_groups(shape, cfg.coarse_k, ratio)
+    out = []
+    for g in base:
+        rest = [i for i in g.src if i not in cached_first]
+        out.append(Group(g.items, g.dst, rest, skip_count(ratio, len(g.items), len(rest)), g.kind))
+    return out
 
 
 def force_decisions(dec: Decisions, cached: Optional[set] = None, match: Optional[dict] = None) -> Decisions:
