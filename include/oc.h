@@ -108,7 +108,12 @@ typedef struct {
     double  r;                /* token / block ratio in [0,1) */
     double  r_frame;          /* frame ratio in [0,1) (FRAME, FRAME_TOKEN) */
     int32_t cold;             /* oc_cold */
-    int32_t reserved;         /* must be 0 */
+    int32_t coarse_k;         /* 0: one level.  Otherwise a second, coarser level of
+                                 the hierarchy (§3.3: reuse first inside k x k
+                                 patches, then in coarser patches or the whole
+                                 frame), TOKEN and BLOCK only: 1 <= coarse_k <
+                                 patch_k, patch_k % coarse_k == 0 */
+    double  r_coarse;         /* the second level's ratio in [0,1) */
 } oc_cfg;
 
 typedef struct {
@@ -174,6 +179,14 @@ typedef struct {
  * oc_layer_cached runs (oc_attn_reduced takes equal-length sequences).
  * Skip counts: a group of n items caches min(floor(r*n), candidates); frame
  * pairs cache min(n_f + floor(r*n_f), candidates) of their 2*n_f tokens.
+ * With coarse_k > 0 the first level's groups are those of patch_k; then
+ * every coarse_k x coarse_k patch (a union of (patch_k/coarse_k)^2 of them)
+ * of n2 items caches min(floor(r_coarse*n2), the candidates the first level
+ * left) more, by the same rule among those candidates against the same
+ * representatives.  The reduced batch holds the tokens neither level
+ * cached; n_groups, n_src_max and n_dst_max describe the first level, and
+ * only oc_layer_cached (and the calls built on it) runs two levels
+ * (oc_match and oc_select return OC_ERR_INVALID_ARG).
  */
 oc_status oc_plan(const oc_shape *shape, const oc_cfg *cfg, oc_plan_info *out);
 

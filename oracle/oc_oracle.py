@@ -415,7 +415,9 @@ def decide(x: np.ndarray, shape: LayerShape, cfg: CacheCfg, no_skip: bool = Fals
     budget to 0 (the "full" cold policy).  ``forced`` may override, for
     parity tests only, decisions that the oracle itself places inside its
     ambiguity band: keys "frame_order" (selected frames in selection order),
-    "pairs", "cached" (set of cached item ids), "match" (item -> rep id)."""
+    "pairs", "cached" (set of cached item ids), "match" (item -> rep id),
+    and with a second level "cached_first" (the first level's cached set
+    only, the second level then decided from what it left)."""
     forced = forced or {}
     ratio = 0.0 if no_skip else cfg.r
     fratio = 0.0 if no_skip else cfg.r_frame
@@ -466,10 +468,11 @@ def decide(x: np.ndarray, shape: LayerShape, cfg: CacheCfg, no_skip: bool = Fals
     match_and_select(groups, k)
     if cfg.coarse_k:
         force = forced.get("cached")
-        if force is not None:
+        first = forced.get("cached_first", force)
+        if first is not None:
             # a forced selection fixes the first level before the second is
-            # formed from what it left
-            cached = [_forced_in(g, force) for g in groups]
+            # formed from what it left ("cached_first": the first level only)
+            cached = [_forced_in(g, first) for g in groups]
         n1 = len(groups)
         groups = groups + coarse_groups(shape, cfg, set(i for c in cached for i in c),
                                         0.0 if no_skip else cfg.r_coarse)

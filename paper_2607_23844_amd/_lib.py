@@ -32,7 +32,7 @@ class oc_shape(C.Structure):
 
 class oc_cfg(C.Structure):
     _fields_ = [("gran", C.c_int32), ("patch_k", C.c_int32), ("r", C.c_double), ("r_frame", C.c_double),
-                ("cold", C.c_int32), ("reserved", C.c_int32)]
+                ("cold", C.c_int32), ("coarse_k", C.c_int32), ("r_coarse", C.c_double)]
 
 
 class oc_cache(C.Structure):

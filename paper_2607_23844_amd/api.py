@@ -47,9 +47,12 @@ class Cfg:
     r_frame: float = 0.0
     patch_k: int = 1
     cold: str = "matched"    # matched | full
+    coarse_k: int = 0        # second, coarser level of the hierarchy (Token / Block Cache); 0: none
+    r_coarse: float = 0.0
 
     def c(self) -> L.oc_cfg:
-        return L.oc_cfg(L.GRANS[self.gran], self.patch_k, self.r, self.r_frame, L.COLDS[self.cold], 0)
+        return L.oc_cfg(L.GRANS[self.gran], self.patch_k, self.r, self.r_frame, L.COLDS[self.cold], self.coarse_k,
+                        self.r_coarse)
 
 
 @dataclass
@@ -212,7 +215,7 @@ def _trace(shape: Shape, cfg: Cfg, cache: LayerCache, pl: PlanInfo, dev):
     """Device buffers for a layer call's decisions and the oc_trace pointing
     at them (a cold "full" step runs with every ratio at 0)."""
     cold_full = cache.valid == 0 and cfg.cold == "full"
-    tp = plan(shape, Cfg(cfg.gran, 0.0, 0.0, cfg.patch_k, cfg.cold)) if cold_full else pl
+    tp = plan(shape, Cfg(cfg.gran, 0.0, 0.0, cfg.patch_k, cfg.cold, cfg.coarse_k, 0.0)) if cold_full else pl
     n_kept, n_cached = tp.n_kept, tp.n_cached
     out = dict(node_max=torch.empty((tp.n_groups, tp.n_src_max), dtype=torch.float32, device=dev),
                node_idx=torch.empty((tp.n_groups, tp.n_src_max), dtype=torch.int32, device=dev),

@@ -42,10 +42,11 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
                                                         const float *__restrict__ inv,
                                                         float *__restrict__ node_max_out,
                                                         int32_t *__restrict__ node_idx_out, GroupMap gm, int /*G*/,
-                                                        int S, int D, int32_t *__restrict__ flag,
+                                                        int S, int D, int32_t *flag,
                                                         int32_t *__restrict__ mtok, int32_t *__restrict__ kept_idx,
                                                         int32_t *__restrict__ cached_idx,
-                                                        int32_t *__restrict__ rmap, int N, int L, int tF) {
+                                                        int32_t *__restrict__ rmap, int N, int L, int tF,
+                                                        const int32_t *excl) {   // may alias flag (read first, per block)
     constexpr int SEL_WAVES = SEL_THREADS / 64;
     // digit histograms, one per SIMD (waves w, w+4, ... share one),
     // double-buffered across radix passes
@@ -68,13 +69,14 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
 
     // slab layout: every load of the thread's candidates is issued first
     // (one round trip), then they are unpacked
-    int32_t nid[SEL_IPT], sids[SEL_IPT];
+    int32_t nid[SEL_IPT], sids[SEL_IPT], exv[SEL_IPT];
     unsigned long long pk[SEL_IPT];
     float iv[SEL_IPT];
 #pragma unroll
     for (int j = 0; j < SEL_IPT; ++j) {
         nid[j] = -1;
         sids[j] = -1;
+        exv[j] = 0;
         if (j >= ipt) continue;
         const int i = j * SEL_THREADS + t;
         const long gi = (long)g * S + i;
@@ -90,17 +92,26 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
                 iv[j] = node_max_in[gi];
                 nid[j] = node_idx_in[gi];
             }
+            if (excl != nullptr) exv[j] = excl[sid];
         }
     }
+    // excluded candidates (slab layout bits): key 0 in LDS, which no value
+    // maps to (float_key gives 0 only for one NaN pattern), marks them for
+    // the run layout
+    uint32_t exm = 0;
 #pragma unroll
     for (int j = 0; j < SEL_IPT; ++j) {
         const int i = j * SEL_THREADS + t;
         if (j >= ipt || i >= S) continue;
         const long gi = (long)g * S + i;
-        if (sids[j] < 0) {
+        if (sids[j] < 0 || exv[j] != 0) {
             if (PACKED && node_max_out != nullptr) {
                 node_max_out[gi] = -INFINITY;
                 node_idx_out[gi] = -1;
+            }
+            if (sids[j] >= 0) {
+                exm |= 1u << j;
+                klds[i] = 0u;
             }
             continue;
         }
@@ -128,6 +139,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
         const int i = t * ipt + j;
         if (j >= ipt || i >= n_src) continue;
         key[j] = klds[i];
+        if (key[j] == 0u) continue;   // excluded
         vmask |= 1u << j;
         ++nvalid_local;
         lo = min(lo, key[j]);
@@ -266,7 +278,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
 #pragma unroll
     for (int j = 0; j < SEL_IPT; ++j) {
         const int i = j * SEL_THREADS + t;
-        if (j >= ipt || i >= n_src) continue;
+        if (j >= ipt || i >= n_src || ((exm >> j) & 1u)) continue;
         const bool c = all || (!none && cbyte[i] != 0);
         const int id = sids[j];
         if (flag != nullptr) {
@@ -353,20 +365,22 @@ hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_
         if (select_small(p, false))
             launch_k(k_select<false, SEL_SMALL>, p.n_groups, SEL_SMALL, lds, st, node_max, node_idx, nullptr, nullptr,
                      nullptr, nullptr, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok, nullptr,
-                     nullptr, nullptr, p.N, p.seq_len, 0);
+                     nullptr, nullptr, p.N, p.seq_len, 0, nullptr);
         else
             launch_k(k_select<false, SEL_LARGE>, p.n_groups, SEL_LARGE, lds, st, node_max, node_idx, nullptr, nullptr,
                      nullptr, nullptr, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok, nullptr,
-                     nullptr, nullptr, p.N, p.seq_len, 0);
+                     nullptr, nullptr, p.N, p.seq_len, 0, nullptr);
     }
     return hipGetLastError();
 }
 
 hipError_t launch_select_packed(const Plan &p, const int32_t *units, const unsigned long long *node_pack,
                                 const float *inv, float *node_max, int32_t *node_idx, int32_t *flag, int32_t *mtok,
-                                int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap, hipStream_t st) {
+                                int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap, hipStream_t st,
+                                const int32_t *excl) {
     const bool compact = kept_idx != nullptr;
     if (compact && !select_compacts(p)) return hipErrorInvalidValue;
+    if (compact && excl != nullptr) return hipErrorInvalidValue;   // an excluding selection never compacts
     // Block Cache: sequences of F tokens, n_seq of them
     const int tF = compact && p.kind == KIND_BLOCK ? p.F : 0;
     const int L = tF > 0 ? p.n_seq : p.seq_len;
@@ -376,11 +390,11 @@ hipError_t launch_select_packed(const Plan &p, const int32_t *units, const unsig
         if (select_small(p, compact))
             launch_k(k_select<true, SEL_SMALL>, p.n_groups, SEL_SMALL, lds, st, nullptr, nullptr, node_pack, inv,
                      node_max, node_idx, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok,
-                     kept_idx, cached_idx, rmap, p.N, L, tF);
+                     kept_idx, cached_idx, rmap, p.N, L, tF, excl);
         else
             launch_k(k_select<true, SEL_LARGE>, p.n_groups, SEL_LARGE, lds, st, nullptr, nullptr, node_pack, inv,
                      node_max, node_idx, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok,
-                     kept_idx, cached_idx, rmap, p.N, L, tF);
+                     kept_idx, cached_idx, rmap, p.N, L, tF, excl);
     }
     return hipGetLastError();
 }

@@ -59,7 +59,15 @@ oc_status check_cfg(const oc_cfg *cfg) {
     if (cfg->gran < 0 || cfg->gran > 3) return fail(OC_ERR_INVALID_ARG, "unknown granularity %d", cfg->gran);
     if (cfg->cold != OC_COLD_MATCHED && cfg->cold != OC_COLD_FULL)
         return fail(OC_ERR_INVALID_ARG, "unknown cold policy %d", cfg->cold);
-    if (cfg->reserved != 0) return fail(OC_ERR_INVALID_ARG, "cfg.reserved must be 0");
+    if (cfg->coarse_k != 0) {
+        if (cfg->gran != OC_GRAN_TOKEN && cfg->gran != OC_GRAN_BLOCK)
+            return fail(OC_ERR_INVALID_ARG, "a coarser level (coarse_k) is defined for Token and Block Cache only");
+        if (cfg->coarse_k < 1 || cfg->coarse_k >= cfg->patch_k || cfg->patch_k % cfg->coarse_k != 0)
+            return fail(OC_ERR_SHAPE, "coarse_k=%d must divide patch_k=%d and be smaller", cfg->coarse_k,
+                        cfg->patch_k);
+        if (!(cfg->r_coarse >= 0.0 && cfg->r_coarse < 1.0))
+            return fail(OC_ERR_INVALID_ARG, "r_coarse=%g outside [0,1)", cfg->r_coarse);
+    }
     if (!(cfg->r >= 0.0 && cfg->r < 1.0)) return fail(OC_ERR_INVALID_ARG, "r=%g outside [0,1)", cfg->r);
     if (!(cfg->r_frame >= 0.0 && cfg->r_frame < 1.0))
         return fail(OC_ERR_INVALID_ARG, "r_frame=%g outside [0,1)", cfg->r_frame);
@@ -146,9 +154,44 @@ oc_status make_plan(const oc_shape *sh, const oc_cfg *cfg, bool no_skip, Plan &p
         }
     }
     if (p.n_src_max > 16384) return fail(OC_ERR_SHAPE, "group of %d candidates exceeds 16384", p.n_src_max);
+    if (cfg->coarse_k > 0) {
+        // second level: each coarse patch holds (k/k2)^2 first-level patches,
+        // every one of which cached exactly R_tok, so its remaining
+        // candidates and its budget are static
+        p.k2 = cfg->coarse_k;
+        p.r2 = no_skip ? 0.0 : cfg->r_coarse;
+        p.np2 = (p.H / p.k2) * (p.W / p.k2);
+        p.np2_dst = p.np2 / 4;
+        p.np2_src = p.np2 - p.np2_dst;
+        const int sub = (p.k / p.k2) * (p.k / p.k2);
+        p.R2 = clampi(floor_ratio(p.r2, p.np2), p.np2_src - sub * p.R_tok);
+        if (p.np2_src > 16384) return fail(OC_ERR_SHAPE, "coarse group of %d candidates exceeds 16384", p.np2_src);
+        const int more = p.k2 * p.k2 * p.R2;   // per frame (Token) or in all (Block)
+        if (p.kind == KIND_TOKEN) p.seq_len -= more;
+        else p.n_seq -= more;
+    }
     p.n_kept = p.kind == KIND_FPATCH ? (p.F - p.R_f) * p.N : p.n_seq * p.seq_len;
     p.n_cached = p.F * p.N - p.n_kept;
     return OC_OK;
+}
+
+// The matching problem of the second level: the same plan with its patches
+// and budget (the reduced batch and the counts stay those of the whole call).
+Plan coarse_plan(const Plan &p) {
+    Plan q = p;
+    q.k = p.k2;
+    q.ph = p.H / p.k2;
+    q.pw = p.W / p.k2;
+    q.np = p.np2;
+    q.np_src = p.np2_src;
+    q.np_dst = p.np2_dst;
+    q.R_tok = p.R2;
+    q.r = p.r2;
+    q.n_groups = (p.kind == KIND_TOKEN ? p.F : 1) * p.k2 * p.k2;
+    q.n_src_max = p.np2_src;
+    q.n_dst_max = p.np2_dst;
+    q.k2 = 0;
+    return q;
 }
 
 // The plan of the uncached layer: spatial (per frame) or temporal (per position).
@@ -175,12 +218,23 @@ Layout make_layout(const Plan &p) {
     const size_t FN = (size_t)p.F * p.N;
     const size_t GS = (size_t)p.n_groups * p.n_src_max;
     L.inv = take(FN * 4);
-    L.node_pack = take(GS * 8);
+    // (the second level's arg-max uses the same buffer: as many candidates in all)
+    const size_t GS2 = p.k2 > 0 ? (size_t)coarse_plan(p).n_groups * p.np2_src : 0;
+    L.node_pack = take((GS > GS2 ? GS : GS2) * 8);
     L.node_max = take(GS * 4);
     L.node_idx = take(GS * 4);
     {
         const MatchSplit ms = match_split(p);
-        L.mpart = take(ms.n_split > 1 ? (size_t)ms.n_split * GS * p.n_dst_max * 4 : 0);
+        size_t mp = ms.n_split > 1 ? (size_t)ms.n_split * GS * p.n_dst_max * 4 : 0;
+        if (p.k2 > 0) {
+            // the second level reuses the arg-max and partial-sum buffers
+            const Plan q = coarse_plan(p);
+            const MatchSplit m2 = match_split(q);
+            const size_t GS2 = (size_t)q.n_groups * q.n_src_max;
+            if (m2.n_split > 1 && (size_t)m2.n_split * GS2 * q.n_dst_max * 4 > mp)
+                mp = (size_t)m2.n_split * GS2 * q.n_dst_max * 4;
+        }
+        L.mpart = take(mp);
     }
     const bool frames = p.kind == KIND_FRAME || p.gran == OC_GRAN_FRAME_TOKEN;
     L.gram_part = take(frames ? (size_t)gram_blocks(p) * 1024 * 4 : 0);
@@ -293,7 +347,8 @@ oc_status run_match(const Plan &p, const Layout &L, const void *x, float *node_m
 // the selection kernel (writing node_max / node_idx too), and compact there
 // as well when every frame is one group.
 oc_status run_select(const Plan &p, const Layout &L, float *node_max, int32_t *node_idx, bool from_pack,
-                     int32_t *kept, int32_t *cached, int32_t *rmap, int map_matched, void *ws, hipStream_t st) {
+                     int32_t *kept, int32_t *cached, int32_t *rmap, int map_matched, void *ws, hipStream_t st,
+                     const void *x = nullptr) {
     const int32_t *units = units_of(p, L, ws);
     if (from_pack && p.kind != KIND_FRAME) {
         const bool fused = select_compacts(p);
@@ -311,6 +366,23 @@ oc_status run_select(const Plan &p, const Layout &L, float *node_max, int32_t *n
                 HIP_TRY(launch_map_matched(p, at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok), rmap, st),
                         "map matched");
             return OC_OK;
+        }
+        if (p.k2 > 0) {
+            // second, coarser level (§3.3): similarity over the coarse
+            // patches, then the selection among the candidates the first
+            // level left (its flags exclude the rest and stay as they are)
+            if (!x) return fail(OC_ERR_INVALID_ARG, "internal: the coarse level needs x");
+            const Plan q = coarse_plan(p);
+            unsigned long long *pack = at<unsigned long long>(ws, L.node_pack);
+            const long n_pack2 = (long)q.n_groups * q.n_src_max;
+            int32_t *flag = at<int32_t>(ws, L.flag);
+            HIP_TRY(launch_fill_i32(reinterpret_cast<int32_t *>(pack), 2 * n_pack2, 0, st), "clear arg-max");
+            HIP_TRY(launch_match(q, x, at<float>(ws, L.inv), units, pack, at<float>(ws, L.mpart), nullptr, nullptr,
+                                 st),
+                    "coarse match");
+            HIP_TRY(launch_select_packed(q, units, pack, at<float>(ws, L.inv), nullptr, nullptr, flag,
+                                         at<int32_t>(ws, L.mtok), nullptr, nullptr, nullptr, st, flag),
+                    "coarse select");
         }
     } else if (!(from_pack && p.kind == KIND_FRAME)) {
         HIP_TRY(launch_select(p, units, node_max, node_idx, at<int32_t>(ws, L.flag), at<int32_t>(ws, L.mtok), st),
@@ -408,6 +480,8 @@ oc_status oc_match(const oc_shape *shape, const oc_cfg *cfg, const void *x, floa
     Plan p;
     oc_status s = make_plan(shape, cfg, false, p);
     if (s != OC_OK) return s;
+    if (p.k2 > 0)
+        return fail(OC_ERR_INVALID_ARG, "the two-level hierarchy (coarse_k > 0) runs in oc_layer_cached only");
     if (!x || !node_max || !node_idx) return fail(OC_ERR_INVALID_ARG, "NULL pointer");
     if (!aligned16(x)) return fail(OC_ERR_INVALID_ARG, "x must be 16-byte aligned");
     const Layout L = make_layout(p);
@@ -427,6 +501,8 @@ oc_status oc_select(const oc_shape *shape, const oc_cfg *cfg, const float *node_
     Plan p;
     oc_status s = make_plan(shape, cfg, false, p);
     if (s != OC_OK) return s;
+    if (p.k2 > 0)
+        return fail(OC_ERR_INVALID_ARG, "the two-level hierarchy (coarse_k > 0) runs in oc_layer_cached only");
     if (!node_max || !node_idx || !kept_idx || !cached_idx || !restore_map)
         return fail(OC_ERR_INVALID_ARG, "NULL pointer");
     if (map_matched != 0 && map_matched != 1) return fail(OC_ERR_INVALID_ARG, "map_matched must be 0 or 1");
@@ -533,7 +609,7 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
                        wo_early ? at<char>(ws, aw.wo16) : nullptr, true)) != OC_OK)
         return s;
     int32_t *kept = at<int32_t>(ws, L.kept), *cached = at<int32_t>(ws, L.cached), *rmap = at<int32_t>(ws, L.rmap);
-    if ((s = run_select(p, L, nm, ni, true, kept, cached, rmap, map_matched, ws, stream)) != OC_OK) return s;
+    if ((s = run_select(p, L, nm, ni, true, kept, cached, rmap, map_matched, ws, stream, x)) != OC_OK) return s;
 
     AttnArgs a;
     std::memset(&a, 0, sizeof(a));

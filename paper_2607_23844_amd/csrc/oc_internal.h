@@ -33,7 +33,13 @@ struct Plan {
     int n_kept, n_cached, n_seq, seq_len;   // KIND_FPATCH: n_seq = F sequences of at most seq_len = N
                                             // tokens each, of varying length (seq_off in the workspace)
     int n_items;             // matched items: F*N tokens, N blocks, F frames
+    // second, coarser level of the hierarchy (§3.3), Token and Block Cache:
+    // k2 = 0 none; else patches of k2 x k2 (k2 divides k), np2 items each,
+    // R2 more of the candidates the first level left cached per patch
+    int k2, np2, np2_src, np2_dst, R2;
+    double r2;
 };
+
 
 // Workspace carve-up (byte offsets from the caller's ws base).
 struct Layout {
@@ -137,9 +143,13 @@ hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_
 // patch_k == 1: one group per frame, or one group of all positions) the same
 // launch also compacts into kept_idx, cached_idx and rmap, as
 // launch_compact would.
+// excl (optional, per item): candidates with a nonzero entry are not
+// candidates of this selection and their flag / mtok entries stay as they
+// are (the second level of the hierarchy after the first).
 hipError_t launch_select_packed(const Plan &p, const int32_t *units, const unsigned long long *node_pack,
                                 const float *inv, float *node_max, int32_t *node_idx, int32_t *flag, int32_t *mtok,
-                                int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap, hipStream_t st);
+                                int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap, hipStream_t st,
+                                const int32_t *excl = nullptr);
 // whether launch_select_packed can compact in the same launch (the frame's
 // flags are staged in LDS: N below SEL_COMPACT_MAX_N)
 constexpr int SEL_COMPACT_MAX_N = 24576;

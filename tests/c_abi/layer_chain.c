@@ -7,10 +7,10 @@
  *
  *   layer_chain <in.bin> <out.bin>
  *
- * in.bin (little endian): 13 int32 (F, H, W, C, heads, head_dim, n_ctx,
- * dtype, gran, patch_k, cold, n_steps, element size), 2 float64 (r,
- * r_frame), then the raw elements of wq, wk, wv, wo, ctx (n_ctx rows, if
- * any) and the n_steps inputs x.  out.bin: per step, the layer output y
+ * in.bin (little endian): 14 int32 (F, H, W, C, heads, head_dim, n_ctx,
+ * dtype, gran, patch_k, cold, n_steps, element size, coarse_k), 3 float64
+ * (r, r_frame, r_coarse), then the raw elements of wq, wk, wv, wo, ctx
+ * (n_ctx rows, if any) and the n_steps inputs x.  out.bin: per step, the layer output y
  * [F, N, C] followed by the context rows' output [n_ctx, C].
  * Exit status 0 on success; on any error the status, oc_last_error() and
  * the failing call are printed and the status is 1.
@@ -55,14 +55,14 @@ int main(int argc, char **argv) {
         perror(argv[1]);
         return 1;
     }
-    int32_t hd[13];
-    double ratios[2];
-    if (fread(hd, sizeof(int32_t), 13, in) != 13 || fread(ratios, sizeof(double), 2, in) != 2) {
+    int32_t hd[14];
+    double ratios[3];
+    if (fread(hd, sizeof(int32_t), 14, in) != 14 || fread(ratios, sizeof(double), 3, in) != 3) {
         fprintf(stderr, "bad header\n");
         return 1;
     }
     oc_shape sh = {hd[0], hd[1], hd[2], hd[3], hd[4], hd[5], hd[6], hd[7]};
-    oc_cfg cfg = {hd[8], hd[9], ratios[0], ratios[1], hd[10], 0};
+    oc_cfg cfg = {hd[8], hd[9], ratios[0], ratios[1], hd[10], hd[13], ratios[2]};
     const int n_steps = hd[11];
     const size_t esz = (size_t)hd[12];
     const size_t FN = (size_t)sh.F * sh.H * sh.W, hdim = (size_t)sh.heads * sh.head_dim;

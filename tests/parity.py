@@ -52,15 +52,15 @@ def to_f64(t: torch.Tensor) -> np.ndarray:
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
-def shapes(wl, gran=None, r=None, r_frame=None, patch_k=None, cold="matched"):
+def shapes(wl, gran=None, r=None, r_frame=None, patch_k=None, cold="matched", coarse_k=0, r_coarse=0.0):
     gran = gran or wl.gran
     r = wl.r if r is None else r
     r_frame = wl.r_frame if r_frame is None else r_frame
     k = wl.patch_k if patch_k is None else patch_k
     sh = oc.Shape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, wl.n_ctx, wl.dtype)
-    cf = oc.Cfg(gran, r, r_frame, k, cold)
+    cf = oc.Cfg(gran, r, r_frame, k, cold, coarse_k, r_coarse)
     osh = O.LayerShape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, wl.n_ctx)
-    ocf = O.CacheCfg(gran, r, r_frame, k, cold)
+    ocf = O.CacheCfg(gran, r, r_frame, k, cold, coarse_k, r_coarse)
     return sh, cf, osh, ocf
 
 
@@ -210,10 +210,66 @@ def check_frame_stage(x64, osh, ocf, dec: O.Decisions, fmax, fidx, pairs):
     return dict(frame_order=g_order, pairs=[(int(s), int(dd)) for s, dd in pairs])
 
 
+def _part(dec: O.Decisions, lo: int, hi: int) -> O.Decisions:
+    return O.Decisions(dec.groups[lo:hi], dec.node_max[lo:hi], dec.node_idx[lo:hi], dec.cached[lo:hi])
+
+
+def decision_parity_two_levels(x64, osh, ocf, tr, valid):
+    """The same for a two-level hierarchy (coarse_k > 0).  The trace holds the
+    first level's similarities; the library's selection is exact on them, so
+    its first-level cached set is the definition applied to those values.
+    That set is checked against the oracle's first level (band rule), the
+    oracle's second level is formed from it, and the rest of the library's
+    cached tokens is checked against that second level.  On a cold "matched"
+    step the restore map names the representative each cached token was
+    matched with; the second level's are checked against the oracle's
+    margins and forced where in band."""
+    no_skip = (not valid) and ocf.cold == O.COLD_FULL
+    kind = "block" if ocf.gran == O.BLOCK else "token"
+    nm = tr["node_max"].cpu().numpy()
+    ni = tr["node_idx"].cpu().numpy()
+    n1 = nm.shape[0]
+    dec0 = O.decide(x64, osh, ocf, no_skip=no_skip)
+    ov, worst_nm = check_match(x64, _part(dec0, 0, n1), nm, ni, kind, osh, ocf.patch_k)
+    first = set()
+    for gi, g in enumerate(dec0.groups[:n1]):
+        first |= set(O.select_cached(nm[gi, :len(g.src)].astype(np.float64), g.src, g.R))
+    n_band = check_selection(_part(dec0, 0, n1), first)
+    dec1 = O.decide(x64, osh, ocf, no_skip=no_skip, forced={"cached_first": first})
+    items = gpu_cached_items(ocf.gran, tr["cached_idx"].cpu().numpy(), osh.N, osh, ocf.patch_k)
+    assert first <= items
+    n_band += check_selection(_part(dec1, n1, len(dec1.groups)), items - first)
+    if not valid and ocf.cold == O.COLD_MATCHED and not no_skip:
+        kept = tr["kept_idx"].cpu().numpy()
+        rmap = tr["restore_map"].cpu().numpy()
+        N = osh.N
+        for gi in range(n1, len(dec1.groups)):
+            g = dec1.groups[gi]
+            pos = {s_: i for i, s_ in enumerate(g.src)}
+            marg = None
+            for item in items - first:
+                if item not in pos:
+                    continue
+                # the token whose row this cached item was restored from
+                tok = int(item) if kind == "token" else int(item)
+                src_tok = int(kept[rmap[tok]])
+                rep = src_tok if kind == "token" else src_tok % N
+                want = int(dec1.node_idx[gi][pos[item]])
+                if rep != want:
+                    marg = group_margins(x64, g, osh, ocf.coarse_k) if marg is None else marg
+                    assert marg[pos[item]] <= BAND, f"coarse group {gi} item {item}: rep {rep} vs {want}"
+                    ov[int(item)] = rep
+    forced = dict(cached_first=first, cached=items, match=ov)
+    dec = O.decide(x64, osh, ocf, no_skip=no_skip, forced=forced)
+    return dec, forced, dict(node_max_err=worst_nm, in_band=n_band, idx_overrides=len(ov))
+
+
 def decision_parity(x64, osh, ocf, tr, valid):
     """Matching and selection of one oc_layer_cached call (its trace) against
     the oracle; returns the oracle's decisions with the library's in-band
     choices forced on them, the forcing, and statistics."""
+    if ocf.coarse_k:
+        return decision_parity_two_levels(x64, osh, ocf, tr, valid)
     no_skip = (not valid) and ocf.cold == O.COLD_FULL
     forced = {}
     dec = O.decide(x64, osh, ocf, no_skip=no_skip)

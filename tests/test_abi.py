@@ -64,7 +64,7 @@ def test_python_binding_covers_every_declared_symbol():
 
 def test_struct_sizes_match_the_header_layout():
     assert C.sizeof(L.oc_shape) == 32
-    assert C.sizeof(L.oc_cfg) == 32
+    assert C.sizeof(L.oc_cfg) == 40
     assert C.sizeof(L.oc_cache) == 16
     assert C.sizeof(L.oc_attn_weights) == 32
     assert C.sizeof(L.oc_plan_info) == 48
@@ -179,9 +179,16 @@ def test_plan_rejects_bad_enums_and_dtype():
     cf = oc.Cfg("token", r=0.5).c()
     cf.gran = 9
     assert lib.oc_plan(C.byref(sh), C.byref(cf), C.byref(info)) == L.OC_ERR_INVALID_ARG
-    cf = oc.Cfg("token", r=0.5).c()
-    cf.reserved = 1
-    assert lib.oc_plan(C.byref(sh), C.byref(cf), C.byref(info)) == L.OC_ERR_INVALID_ARG
+    # a coarser level: Token and Block Cache only, coarse_k dividing patch_k
+    # and smaller, its ratio in [0, 1)
+    for bad, status in ((oc.Cfg("frame", r_frame=0.3, patch_k=2, coarse_k=1, r_coarse=0.1), L.OC_ERR_INVALID_ARG),
+                        (oc.Cfg("token", r=0.3, patch_k=4, coarse_k=3, r_coarse=0.1), L.OC_ERR_SHAPE),
+                        (oc.Cfg("token", r=0.3, patch_k=2, coarse_k=2, r_coarse=0.1), L.OC_ERR_SHAPE),
+                        (oc.Cfg("token", r=0.3, patch_k=2, coarse_k=-1, r_coarse=0.1), L.OC_ERR_SHAPE),
+                        (oc.Cfg("block", r=0.3, patch_k=2, coarse_k=1, r_coarse=1.0), L.OC_ERR_INVALID_ARG),
+                        (oc.Cfg("block", r=0.3, patch_k=2, coarse_k=1, r_coarse=float("nan")), L.OC_ERR_INVALID_ARG)):
+        cf = bad.c()
+        assert lib.oc_plan(C.byref(sh), C.byref(cf), C.byref(info)) == status, bad
     cf = oc.Cfg("token", r=0.5).c()
     sh.dtype = 7
     assert lib.oc_plan(C.byref(sh), C.byref(cf), C.byref(info)) == L.OC_ERR_DTYPE
@@ -323,3 +330,22 @@ def test_ffn_entry_point_validates_before_launching():
     assert lib.oc_ffn_reduced(C.byref(c72), FAKE, FAKE, 32, C.byref(w), FAKE * 2, 1, FAKE, need, None) == \
         L.OC_ERR_SHAPE
     assert lib.oc_ffn_reduced(C.byref(sh), FAKE, FAKE, 0, C.byref(w), FAKE * 2, 1, FAKE, 0, None) == L.OC_OK
+
+
+@pytest.mark.parametrize("gran,F,H,W,k1,k2,r1,r2", [
+    ("token", 1, 64, 64, 4, 1, 0.25, 0.25), ("token", 2, 16, 16, 4, 2, 0.2, 0.3), ("token", 1, 32, 32, 8, 2, 0.3, 0.4),
+    ("token", 1, 16, 16, 2, 1, 0.7, 0.7), ("block", 4, 16, 16, 4, 1, 0.25, 0.25), ("block", 6, 8, 16, 2, 1, 0.1, 0.5),
+])
+def test_plan_of_two_levels_matches_the_oracle(gran, F, H, W, k1, k2, r1, r2):
+    """Host only: the plan of a two-level hierarchy (coarse_k) gives the
+    sequence count, lengths and retained total of the oracle's decisions
+    for the same configuration."""
+    from oracle import oc_oracle as O
+    sh = oc.Shape(F, H, W, 8, 1, 16, 0, "bf16")
+    pl = oc.plan(sh, oc.Cfg(gran, r=r1, patch_k=k1, coarse_k=k2, r_coarse=r2))
+    osh = O.LayerShape(F, H, W, 8, 1, 16)
+    x = np.random.default_rng(1).standard_normal((F, H * W, 8))
+    dec = O.decide(x, osh, O.CacheCfg(gran, r=r1, patch_k=k1, coarse_k=k2, r_coarse=r2))
+    seqs = O.build_sequences(osh, O.CacheCfg(gran, r=r1, patch_k=k1, coarse_k=k2, r_coarse=r2), dec)
+    assert pl.n_seq == len(seqs) and all(len(s) == pl.seq_len for s in seqs)
+    assert pl.n_kept == sum(len(s) for s in seqs) and pl.n_cached == F * H * W - pl.n_kept

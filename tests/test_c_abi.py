@@ -36,10 +36,10 @@ def test_c_program_compiles_against_the_header(tmp_path):
 def _write_input(path, wl, sh, cf, n_steps):
     esz = 2 if wl.dtype == "bf16" else 4
     with open(path, "wb") as f:
-        f.write(struct.pack("<13i", sh.F, sh.H, sh.W, sh.C, sh.heads, sh.head_dim, sh.n_ctx,
+        f.write(struct.pack("<14i", sh.F, sh.H, sh.W, sh.C, sh.heads, sh.head_dim, sh.n_ctx,
                             1 if wl.dtype == "bf16" else 0, GRANS[cf.gran], cf.patch_k,
-                            0 if cf.cold == "matched" else 1, n_steps, esz))
-        f.write(struct.pack("<2d", cf.r, cf.r_frame))
+                            0 if cf.cold == "matched" else 1, n_steps, esz, cf.coarse_k))
+        f.write(struct.pack("<3d", cf.r, cf.r_frame, cf.r_coarse))
         for a in [wl.wq, wl.wk, wl.wv, wl.wo] + ([wl.ctx] if wl.n_ctx else []) + list(wl.steps[:n_steps]):
             f.write(np.ascontiguousarray(a).tobytes())
     return esz

@@ -34,8 +34,9 @@ def gpu():
     return torch.device("cuda:0")
 
 
-def chain(wl, n_steps, cold="matched", gran=None, r=None, r_frame=None, patch_k=None, case=""):
-    sh, cf, osh, ocf = shapes(wl, gran, r, r_frame, patch_k, cold)
+def chain(wl, n_steps, cold="matched", gran=None, r=None, r_frame=None, patch_k=None, case="", coarse_k=0,
+          r_coarse=0.0):
+    sh, cf, osh, ocf = shapes(wl, gran, r, r_frame, patch_k, cold, coarse_k, r_coarse)
     dev = torch.device("cuda:0")
     ws = oc.workspace(sh, cf, dev)
     cache = oc.LayerCache(sh, dev)
@@ -45,7 +46,8 @@ def chain(wl, n_steps, cold="matched", gran=None, r=None, r_frame=None, patch_k=
     ora, valid = None, False
     stats = []
     for s in range(n_steps):
-        _say(f"  step {s} of {wl.name} gran={cf.gran} r={cf.r} rf={cf.r_frame} k={cf.patch_k} cold={cold}")
+        _say(f"  step {s} of {wl.name} gran={cf.gran} r={cf.r} rf={cf.r_frame} k={cf.patch_k} cold={cold}"
+             + (f" coarse k={cf.coarse_k} r={cf.r_coarse}" if cf.coarse_k else ""))
         res, st = layer_step_parity(wl, wl.steps[s], sh, cf, osh, ocf, cache, ws, ora, valid, ctx_dev, ctx64, W, W64,
                                     case=case)
         _say(f"    {st}")
@@ -363,6 +365,37 @@ def test_sd3_match_patch_sizes(k):
     dec = O.decide(x64, osh, ocf)
     ov, worst = check_match(x64, dec, nm.cpu().numpy(), ni.cpu().numpy(), "token")
     _say(f"sd3 k={k}: node_max err {worst:.3g}, in-band idx differences {len(ov)}")
+
+
+# two levels of the hierarchy (§3.3): patch-local first, then coarser
+# patches or the whole frame among the candidates left
+TWO_LEVEL = [
+    (dict(gran="token", F=2, H=16, W=16, C=64, heads=2, head_dim=32, dtype="bf16"), 4, 0.25, 1, 0.25),
+    (dict(gran="token", F=1, H=16, W=24, C=64, heads=2, head_dim=32, dtype="bf16", n_ctx=5), 4, 0.2, 2, 0.3),
+    (dict(gran="token", F=1, H=16, W=16, C=32, heads=2, head_dim=16, dtype="f32"), 2, 0.3, 1, 0.2),
+    (dict(gran="block", F=6, H=16, W=16, C=64, heads=2, head_dim=32, dtype="bf16"), 4, 0.25, 1, 0.25),
+    (dict(gran="block", F=5, H=8, W=16, C=48, heads=3, head_dim=16, dtype="f32"), 2, 0.2, 1, 0.4),
+    # the first level caches every candidate it may: the second finds none left
+    (dict(gran="token", F=1, H=16, W=16, C=64, heads=2, head_dim=32, dtype="bf16"), 2, 0.9, 1, 0.5),
+]
+
+
+@pytest.mark.parametrize("case", range(len(TWO_LEVEL)))
+@pytest.mark.parametrize("cold", ["matched", "full"])
+def test_two_level_chain(case, cold):
+    kw, k1, r1, k2, r2 = TWO_LEVEL[case]
+    kw = dict(kw)
+    wl = small_workload(n_steps=3, seed=300 + case, **kw)
+    _say(f"two levels {case}: {kw} k={k1} r={r1} then k={k2} r={r2} cold={cold}")
+    chain(wl, 3, cold=cold, r=r1, patch_k=k1, coarse_k=k2, r_coarse=r2)
+
+
+@pytest.mark.parametrize("k1,r1,k2,r2", [(4, 0.25, 1, 0.25), (8, 0.3, 2, 0.2)])
+def test_sd3_two_level_chain(k1, r1, k2, r2):
+    """The SD3-like layer (4096 image + 333 text tokens): patch-local Token
+    Cache, then a coarser level, cold and warm."""
+    wl = make_workload("sd3_1024", 3)
+    chain(wl, 3, r=r1, patch_k=k1, coarse_k=k2, r_coarse=r2)
 
 
 @pytest.mark.parametrize("r", [0.25, 0.5, 0.75])
