@@ -437,6 +437,44 @@ def run_k_sweep(args):
     return out
 
 
+def run_two_level(args):
+    """The hierarchy of §3.3 at the SD3-like shape: Token Cache matched in
+    k x k patches first, then in coarser patches or the whole frame among the
+    candidates left, against one level at the same total ratio (r = 0.5):
+    the step, the uncached layer, and the bookkeeping stages."""
+    import torch
+    import paper_2607_23844_amd as oc
+    from paper_2607_23844_amd.runner import FullRunner, LayerRunner
+    from oc_synth import make_workload
+
+    dev = torch.device("cuda:0")
+    K = args.cfg_steps
+    wl = make_workload("sd3_1024", 3)
+    shape = oc.Shape(wl.F, wl.H, wl.W, wl.C, wl.heads, wl.head_dim, wl.n_ctx, "bf16")
+    xs = [_bf16_dev(s, dev) for s in wl.steps]
+    W = {k: _bf16_dev(getattr(wl, k), dev) for k in ("wq", "wk", "wv", "wo")}
+    ctx = _bf16_dev(wl.ctx, dev)
+    full_ms = timed_ms(FullRunner(shape, oc.Cfg("token", 0.0), W, dev, ctx), xs, K, 3)
+    out = dict(uncached_us=round(full_ms * 1e3, 2))
+    for name, cfg in (("one level, k=1, r=0.5", oc.Cfg("token", r=0.5)),
+                      ("one level, k=4, r=0.5", oc.Cfg("token", r=0.5, patch_k=4)),
+                      ("k=4 r=0.25, then k=1 r=0.25", oc.Cfg("token", r=0.25, patch_k=4, coarse_k=1, r_coarse=0.25)),
+                      ("k=8 r=0.25, then k=2 r=0.25", oc.Cfg("token", r=0.25, patch_k=8, coarse_k=2, r_coarse=0.25)),
+                      ("k=4 r=0.4, then k=1 r=0.1", oc.Cfg("token", r=0.4, patch_k=4, coarse_k=1, r_coarse=0.1))):
+        run = LayerRunner(shape, cfg, W, dev, ctx)
+        run(xs[0])
+        ms = timed_ms(run, xs[1:], K, 3)
+        st = stage_times(run, xs[1:], K)
+        book = ("inv_norm", "match", "select", "compact", "fill")
+        pl = oc.plan(shape, cfg)
+        out[name] = dict(step_us=round(ms * 1e3, 2), speedup_vs_uncached=round(full_ms / ms, 4),
+                         retained_tokens=pl.n_kept,
+                         bookkeeping_us=round(sum(st[n][0] for n in book if n in st) * 1e3 / K, 3),
+                         stages_us={n: round(v[0] * 1e3 / K, 3) for n, v in st.items()})
+        del run
+    return out
+
+
 def run_frame_patch_sweep(args):
     """Frame Cache scope on the Latte-like spatial layer (§3.3): whole-frame
     matching (k = 1) against per-patch matching on 2x2 and 4x4 patches
@@ -733,7 +771,7 @@ def run_cpu_baselines(args):
 
 
 ONLY = ("sd3_1024", "latte_spatial", "latte_temporal", "svdxt_level", "svdxt_level_k4", "sd3_ffn", "latte_block",
-        "svdxt_block", "k_sweep")
+        "svdxt_block", "k_sweep", "two_level")
 
 
 def main():
@@ -765,7 +803,8 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     if args.only and args.only != "sd3_1024":
-        fn = {"sd3_ffn": run_ffn, "latte_block": run_blocks, "svdxt_block": run_blocks, "k_sweep": run_k_sweep}.get(
+        fn = {"sd3_ffn": run_ffn, "latte_block": run_blocks, "svdxt_block": run_blocks, "k_sweep": run_k_sweep,
+              "two_level": run_two_level}.get(
             args.only, run_other_configs)
         print(json.dumps({"only": args.only, "result": fn(args)}))
         return
@@ -777,6 +816,7 @@ def main():
         extra["ffn_sd3"] = run_ffn(args)
         extra["blocks"] = run_blocks(args)
         extra["group_count_sweep_sd3"] = run_k_sweep(args)
+        extra["two_level_hierarchy_sd3"] = run_two_level(args)
         extra["frame_patch_sweep_latte"] = run_frame_patch_sweep(args)
         extra["layered_schedule"] = run_layered(args)
     cpu = None if (args.no_cpu or args.only) else run_cpu_baselines(args)

@@ -38,7 +38,7 @@ constexpr int SEL_SMALL = 512, SEL_LARGE = 1024;
 template <bool PACKED, int SEL_THREADS>
 __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict__ node_max_in,
                                                         const int32_t *__restrict__ node_idx_in,
-                                                        const unsigned long long *__restrict__ node_pack,
+                                                        unsigned long long *__restrict__ node_pack,
                                                         const float *__restrict__ inv,
                                                         float *__restrict__ node_max_out,
                                                         int32_t *__restrict__ node_idx_out, GroupMap gm, int /*G*/,
@@ -46,7 +46,8 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
                                                         int32_t *__restrict__ mtok, int32_t *__restrict__ kept_idx,
                                                         int32_t *__restrict__ cached_idx,
                                                         int32_t *__restrict__ rmap, int N, int L, int tF,
-                                                        const int32_t *excl) {   // may alias flag (read first, per block)
+                                                        const int32_t *excl,   // may alias flag (read first, per block)
+                                                        int clear_pack) {
     constexpr int SEL_WAVES = SEL_THREADS / 64;
     // digit histograms, one per SIMD (waves w, w+4, ... share one),
     // double-buffered across radix passes
@@ -93,6 +94,16 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
                 nid[j] = node_idx_in[gi];
             }
             if (excl != nullptr) exv[j] = excl[sid];
+        }
+    }
+    // a second level follows: leave the packed arg-max zeroed for its
+    // similarity kernel (every slot g*S + i of this launch, read above)
+    if (PACKED && clear_pack) {
+        // (the thread that read a slot clears it, after its load in program order)
+#pragma unroll
+        for (int j = 0; j < SEL_IPT; ++j) {
+            const int i = j * SEL_THREADS + t;
+            if (j < ipt && i < S) node_pack[(long)g * S + i] = 0ull;
         }
     }
     // excluded candidates (slab layout bits): key 0 in LDS, which no value
@@ -365,19 +376,19 @@ hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_
         if (select_small(p, false))
             launch_k(k_select<false, SEL_SMALL>, p.n_groups, SEL_SMALL, lds, st, node_max, node_idx, nullptr, nullptr,
                      nullptr, nullptr, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok, nullptr,
-                     nullptr, nullptr, p.N, p.seq_len, 0, nullptr);
+                     nullptr, nullptr, p.N, p.seq_len, 0, nullptr, 0);
         else
             launch_k(k_select<false, SEL_LARGE>, p.n_groups, SEL_LARGE, lds, st, node_max, node_idx, nullptr, nullptr,
                      nullptr, nullptr, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok, nullptr,
-                     nullptr, nullptr, p.N, p.seq_len, 0, nullptr);
+                     nullptr, nullptr, p.N, p.seq_len, 0, nullptr, 0);
     }
     return hipGetLastError();
 }
 
-hipError_t launch_select_packed(const Plan &p, const int32_t *units, const unsigned long long *node_pack,
+hipError_t launch_select_packed(const Plan &p, const int32_t *units, unsigned long long *node_pack,
                                 const float *inv, float *node_max, int32_t *node_idx, int32_t *flag, int32_t *mtok,
                                 int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap, hipStream_t st,
-                                const int32_t *excl) {
+                                const int32_t *excl, int clear_pack) {
     const bool compact = kept_idx != nullptr;
     if (compact && !select_compacts(p)) return hipErrorInvalidValue;
     if (compact && excl != nullptr) return hipErrorInvalidValue;   // an excluding selection never compacts
@@ -390,11 +401,11 @@ hipError_t launch_select_packed(const Plan &p, const int32_t *units, const unsig
         if (select_small(p, compact))
             launch_k(k_select<true, SEL_SMALL>, p.n_groups, SEL_SMALL, lds, st, nullptr, nullptr, node_pack, inv,
                      node_max, node_idx, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok,
-                     kept_idx, cached_idx, rmap, p.N, L, tF, excl);
+                     kept_idx, cached_idx, rmap, p.N, L, tF, excl, clear_pack);
         else
             launch_k(k_select<true, SEL_LARGE>, p.n_groups, SEL_LARGE, lds, st, nullptr, nullptr, node_pack, inv,
                      node_max, node_idx, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok,
-                     kept_idx, cached_idx, rmap, p.N, L, tF, excl);
+                     kept_idx, cached_idx, rmap, p.N, L, tF, excl, clear_pack);
     }
     return hipGetLastError();
 }

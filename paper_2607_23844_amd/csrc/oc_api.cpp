@@ -359,7 +359,7 @@ oc_status run_select(const Plan &p, const Layout &L, float *node_max, int32_t *n
         HIP_TRY(launch_select_packed(p, units, at<unsigned long long>(ws, L.node_pack), at<float>(ws, L.inv),
                                      node_max, node_idx, flags ? at<int32_t>(ws, L.flag) : nullptr,
                                      flags ? at<int32_t>(ws, L.mtok) : nullptr, fused ? kept : nullptr,
-                                     fused ? cached : nullptr, fused ? rmap : nullptr, st),
+                                     fused ? cached : nullptr, fused ? rmap : nullptr, st, nullptr, p.k2 > 0 ? 1 : 0),
                 "select");
         if (fused) {
             if (map_matched)
@@ -373,10 +373,10 @@ oc_status run_select(const Plan &p, const Layout &L, float *node_max, int32_t *n
             // level left (its flags exclude the rest and stay as they are)
             if (!x) return fail(OC_ERR_INVALID_ARG, "internal: the coarse level needs x");
             const Plan q = coarse_plan(p);
+            // (the first level's selection left the packed arg-max zeroed:
+            // both levels cover the same number of candidate slots)
             unsigned long long *pack = at<unsigned long long>(ws, L.node_pack);
-            const long n_pack2 = (long)q.n_groups * q.n_src_max;
             int32_t *flag = at<int32_t>(ws, L.flag);
-            HIP_TRY(launch_fill_i32(reinterpret_cast<int32_t *>(pack), 2 * n_pack2, 0, st), "clear arg-max");
             HIP_TRY(launch_match(q, x, at<float>(ws, L.inv), units, pack, at<float>(ws, L.mpart), nullptr, nullptr,
                                  st),
                     "coarse match");
