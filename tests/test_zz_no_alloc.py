@@ -1,8 +1,8 @@
 """oc_layer_cached_static (the entry point for callers that cannot
-allocate) against oc_layer_cached with a caller workspace: two layers in a
-row through the library's static scratch, the second smaller than the
-first (so it runs over the first call's leftover scratch contents), each
-for a cold and a warm step.  Same kernels on the same inputs: outputs,
+allocate) against oc_layer_cached with a caller workspace: four layers in
+a row through the library's static scratch, each smaller than the one
+before (so it runs over the previous call's leftover scratch contents),
+each for a cold and a warm step.  Same kernels on the same inputs: outputs,
 context outputs and decision traces must be bit-identical."""
 import sys
 
@@ -33,12 +33,16 @@ def test_static_scratch_matches_workspace_entry_point():
         pytest.skip("no GPU")
     dev = torch.device("cuda:0")
     # the SD3-like layer (57 MiB of scratch), then the smaller Latte-like
-    # spatial Frame Cache layer (41 MiB), then a small Frame+Token Cache layer
-    layers = [make_workload("sd3_1024", 2), make_workload("latte_spatial", 2),
-              small_workload("frame_token", F=7, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r_frame=0.3,
-                             planted=True, n_steps=2, seed=8)]
-    for wl in layers:
-        sh, cf, _, _ = shapes(wl)
+    # spatial Frame Cache layer (41 MiB), then a small Frame+Token Cache
+    # layer, then a small two-level Token Cache layer (patches of 4 x 4, then
+    # the whole frame)
+    layers = [(make_workload("sd3_1024", 2), {}), (make_workload("latte_spatial", 2), {}),
+              (small_workload("frame_token", F=7, H=8, W=8, C=64, heads=2, head_dim=32, dtype="bf16", r_frame=0.3,
+                              planted=True, n_steps=2, seed=8), {}),
+              (small_workload("token", F=1, H=16, W=16, C=64, heads=2, head_dim=32, dtype="bf16", n_steps=2, seed=9),
+               dict(r=0.25, patch_k=4, coarse_k=1, r_coarse=0.25))]
+    for wl, kw in layers:
+        sh, cf, _, _ = shapes(wl, **kw)
         need = oc.plan(sh, cf).workspace_bytes
         _say(f"{wl.name}: scratch {need / 2**20:.1f} MiB of {oc.static_scratch_bytes() / 2**20:.0f}")
         assert need <= oc.static_scratch_bytes()
