@@ -35,7 +35,7 @@ constexpr int SEL_SMALL = 512, SEL_LARGE = 1024;
 // positions ascend frame-major in cached_idx[f*Rc + rank].  The per-token
 // flag / mtok arrays are written only when given: a compacting warm step
 // passes none, since only the cold "matched" mapping reads them then.
-template <bool PACKED, int SEL_THREADS>
+template <bool PACKED, int SEL_THREADS, int IPT>
 __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict__ node_max_in,
                                                         const int32_t *__restrict__ node_idx_in,
                                                         unsigned long long *__restrict__ node_pack,
@@ -70,11 +70,11 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
 
     // slab layout: every load of the thread's candidates is issued first
     // (one round trip), then they are unpacked
-    int32_t nid[SEL_IPT], sids[SEL_IPT], exv[SEL_IPT];
-    unsigned long long pk[SEL_IPT];
-    float iv[SEL_IPT];
+    int32_t nid[IPT], sids[IPT], exv[IPT];
+    unsigned long long pk[IPT];
+    float iv[IPT];
 #pragma unroll
-    for (int j = 0; j < SEL_IPT; ++j) {
+    for (int j = 0; j < IPT; ++j) {
         nid[j] = -1;
         sids[j] = -1;
         exv[j] = 0;
@@ -101,7 +101,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
     if (PACKED && clear_pack) {
         // (the thread that read a slot clears it, after its load in program order)
 #pragma unroll
-        for (int j = 0; j < SEL_IPT; ++j) {
+        for (int j = 0; j < IPT; ++j) {
             const int i = j * SEL_THREADS + t;
             if (j < ipt && i < S) node_pack[(long)g * S + i] = 0ull;
         }
@@ -111,7 +111,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
     // the run layout
     uint32_t exm = 0;
 #pragma unroll
-    for (int j = 0; j < SEL_IPT; ++j) {
+    for (int j = 0; j < IPT; ++j) {
         const int i = j * SEL_THREADS + t;
         if (j >= ipt || i >= S) continue;
         const long gi = (long)g * S + i;
@@ -140,12 +140,12 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
         klds[i] = float_key(v);
     }
     __syncthreads();
-    uint32_t key[SEL_IPT];   // run layout
+    uint32_t key[IPT];   // run layout
     uint32_t vmask = 0;
     int nvalid_local = 0;
     uint32_t lo = 0xFFFFFFFFu, hi = 0u;
 #pragma unroll
-    for (int j = 0; j < SEL_IPT; ++j) {
+    for (int j = 0; j < IPT; ++j) {
         key[j] = 0;
         const int i = t * ipt + j;
         if (j >= ipt || i >= n_src) continue;
@@ -204,7 +204,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
             const uint32_t dmask = (1u << nbits) - 1u;
             int *hw = hist[buf][wave % SEL_HISTS];
 #pragma unroll
-            for (int j = 0; j < SEL_IPT; ++j)
+            for (int j = 0; j < IPT; ++j)
                 if (((vmask >> j) & 1u) && (key[j] & mask) == prefix) atomicAdd(&hw[(key[j] >> bit_lo) & dmask], 1);
             __syncthreads();
             if (t < 64) {
@@ -262,7 +262,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
     if (tie) {
         int eq_local = 0;
 #pragma unroll
-        for (int j = 0; j < SEL_IPT; ++j)
+        for (int j = 0; j < IPT; ++j)
             if (((vmask >> j) & 1u) && key[j] == tau) ++eq_local;
         int eq_total;
         eq_rank = block_exclusive_scan(eq_local, sh, eq_total);
@@ -272,7 +272,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
     uint8_t *cbyte = reinterpret_cast<uint8_t *>(klds);
     if (!none && !all) {
 #pragma unroll
-        for (int j = 0; j < SEL_IPT; ++j) {
+        for (int j = 0; j < IPT; ++j) {
             if (!((vmask >> j) & 1u)) continue;
             bool c;
             if (key[j] > tau) c = true;
@@ -287,7 +287,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
     const bool compact = kept_idx != nullptr;
     const long fbase = (long)g * N;
 #pragma unroll
-    for (int j = 0; j < SEL_IPT; ++j) {
+    for (int j = 0; j < IPT; ++j) {
         const int i = j * SEL_THREADS + t;
         if (j >= ipt || i >= n_src || ((exm >> j) & 1u)) continue;
         const bool c = all || (!none && cbyte[i] != 0);
@@ -362,6 +362,19 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
     }
 }
 
+// The kernel instance whose unrolled per-thread loops fit ipt = candidates
+// per thread (1, 2, 4, 8 or 16): a selection runs once per group from a
+// cold instruction cache, so its code is kept to the loops it needs (the
+// SD3-like group, 3 per thread, runs 4-wide loops instead of 16-wide).
+template <bool PACKED, int T, typename... A>
+static void go_sel(int ipt, unsigned grid, size_t lds, hipStream_t st, A... args) {
+    if (ipt <= 1) launch_k(k_select<PACKED, T, 1>, grid, T, lds, st, args...);
+    else if (ipt <= 2) launch_k(k_select<PACKED, T, 2>, grid, T, lds, st, args...);
+    else if (ipt <= 4 || T == SEL_SMALL) launch_k(k_select<PACKED, T, 4>, grid, T, lds, st, args...);
+    else if (ipt <= 8) launch_k(k_select<PACKED, T, 8>, grid, T, lds, st, args...);
+    else launch_k(k_select<PACKED, T, SEL_IPT>, grid, T, lds, st, args...);
+}
+
 // the small block while the candidates fit 4 per thread and the
 // compaction's (slab, wave) counts fit one per thread
 static bool select_small(const Plan &p, bool compact) {
@@ -374,13 +387,17 @@ hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_
         StageScope _stage(st, "select");
         const size_t lds = (size_t)p.n_src_max * 4;
         if (select_small(p, false))
-            launch_k(k_select<false, SEL_SMALL>, p.n_groups, SEL_SMALL, lds, st, node_max, node_idx, nullptr, nullptr,
-                     nullptr, nullptr, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok, nullptr,
-                     nullptr, nullptr, p.N, p.seq_len, 0, nullptr, 0);
+            go_sel<false, SEL_SMALL>(cdiv(p.n_src_max, SEL_SMALL), p.n_groups, lds, st, node_max, node_idx,
+                                     (unsigned long long *)nullptr, (const float *)nullptr, (float *)nullptr,
+                                     (int32_t *)nullptr, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max,
+                                     flag, mtok, (int32_t *)nullptr, (int32_t *)nullptr, (int32_t *)nullptr, p.N,
+                                     p.seq_len, 0, (const int32_t *)nullptr, 0);
         else
-            launch_k(k_select<false, SEL_LARGE>, p.n_groups, SEL_LARGE, lds, st, node_max, node_idx, nullptr, nullptr,
-                     nullptr, nullptr, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok, nullptr,
-                     nullptr, nullptr, p.N, p.seq_len, 0, nullptr, 0);
+            go_sel<false, SEL_LARGE>(cdiv(p.n_src_max, SEL_LARGE), p.n_groups, lds, st, node_max, node_idx,
+                                     (unsigned long long *)nullptr, (const float *)nullptr, (float *)nullptr,
+                                     (int32_t *)nullptr, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max,
+                                     flag, mtok, (int32_t *)nullptr, (int32_t *)nullptr, (int32_t *)nullptr, p.N,
+                                     p.seq_len, 0, (const int32_t *)nullptr, 0);
     }
     return hipGetLastError();
 }
@@ -399,13 +416,15 @@ hipError_t launch_select_packed(const Plan &p, const int32_t *units, unsigned lo
         StageScope _stage(st, "select");
         const size_t lds = (size_t)p.n_src_max * 4;
         if (select_small(p, compact))
-            launch_k(k_select<true, SEL_SMALL>, p.n_groups, SEL_SMALL, lds, st, nullptr, nullptr, node_pack, inv,
-                     node_max, node_idx, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok,
-                     kept_idx, cached_idx, rmap, p.N, L, tF, excl, clear_pack);
+            go_sel<true, SEL_SMALL>(cdiv(p.n_src_max, SEL_SMALL), p.n_groups, lds, st, (const float *)nullptr,
+                                    (const int32_t *)nullptr, node_pack, inv, node_max, node_idx, group_map(p, units),
+                                    p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok, kept_idx, cached_idx, rmap, p.N,
+                                    L, tF, excl, clear_pack);
         else
-            launch_k(k_select<true, SEL_LARGE>, p.n_groups, SEL_LARGE, lds, st, nullptr, nullptr, node_pack, inv,
-                     node_max, node_idx, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok,
-                     kept_idx, cached_idx, rmap, p.N, L, tF, excl, clear_pack);
+            go_sel<true, SEL_LARGE>(cdiv(p.n_src_max, SEL_LARGE), p.n_groups, lds, st, (const float *)nullptr,
+                                    (const int32_t *)nullptr, node_pack, inv, node_max, node_idx, group_map(p, units),
+                                    p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok, kept_idx, cached_idx, rmap, p.N,
+                                    L, tF, excl, clear_pack);
     }
     return hipGetLastError();
 }
