@@ -12,6 +12,8 @@
 #include "oc_device.h"
 #include "oc_block.h"
 #include "oc_groups.h"
+#include "oc_mfma_tile.h"
+#include "oc_attn_common.h"
 #include <algorithm>
 
 namespace oc {
@@ -41,13 +43,22 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(const float *__restrict_
                                                         unsigned long long *__restrict__ node_pack,
                                                         const float *__restrict__ inv,
                                                         float *__restrict__ node_max_out,
-                                                        int32_t *__restrict__ node_idx_out, GroupMap gm, int /*G*/,
+                                                        int32_t *__restrict__ node_idx_out, GroupMap gm, int G,
                                                         int S, int D, int32_t *flag,
                                                         int32_t *__restrict__ mtok, int32_t *__restrict__ kept_idx,
                                                         int32_t *__restrict__ cached_idx,
                                                         int32_t *__restrict__ rmap, int N, int L, int tF,
                                                         const int32_t *excl,   // may alias flag (read first, per block)
-                                                        int clear_pack) {
+                                                        int clear_pack, const uint4 *__restrict__ wo, long n8,
+                                                        uint4 *__restrict__ wo16) {
+    // blocks past the groups: convert wo to fp16 for the output projection
+    // (independent work on the CUs the selection leaves idle)
+    if ((int)blockIdx.x >= G) {
+        const long nb = gridDim.x - G;
+        for (long i = (long)(blockIdx.x - G) * SEL_THREADS + threadIdx.x; i < n8; i += nb * SEL_THREADS)
+            wo16[i] = bf16x8_to_f16x8(wo[i]);
+        return;
+    }
     constexpr int SEL_WAVES = SEL_THREADS / 64;
     // digit histograms, one per SIMD (waves w, w+4, ... share one),
     // double-buffered across radix passes
@@ -391,13 +402,15 @@ hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_
                                      (unsigned long long *)nullptr, (const float *)nullptr, (float *)nullptr,
                                      (int32_t *)nullptr, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max,
                                      flag, mtok, (int32_t *)nullptr, (int32_t *)nullptr, (int32_t *)nullptr, p.N,
-                                     p.seq_len, 0, (const int32_t *)nullptr, 0);
+                                     p.seq_len, 0, (const int32_t *)nullptr, 0, (const uint4 *)nullptr, 0L,
+                                     (uint4 *)nullptr);
         else
             go_sel<false, SEL_LARGE>(cdiv(p.n_src_max, SEL_LARGE), p.n_groups, lds, st, node_max, node_idx,
                                      (unsigned long long *)nullptr, (const float *)nullptr, (float *)nullptr,
                                      (int32_t *)nullptr, group_map(p, units), p.n_groups, p.n_src_max, p.n_dst_max,
                                      flag, mtok, (int32_t *)nullptr, (int32_t *)nullptr, (int32_t *)nullptr, p.N,
-                                     p.seq_len, 0, (const int32_t *)nullptr, 0);
+                                     p.seq_len, 0, (const int32_t *)nullptr, 0, (const uint4 *)nullptr, 0L,
+                                     (uint4 *)nullptr);
     }
     return hipGetLastError();
 }
@@ -405,7 +418,7 @@ hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_
 hipError_t launch_select_packed(const Plan &p, const int32_t *units, unsigned long long *node_pack,
                                 const float *inv, float *node_max, int32_t *node_idx, int32_t *flag, int32_t *mtok,
                                 int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap, hipStream_t st,
-                                const int32_t *excl, int clear_pack) {
+                                const int32_t *excl, int clear_pack, const void *wo, void *wo16, long n_wo) {
     const bool compact = kept_idx != nullptr;
     if (compact && !select_compacts(p)) return hipErrorInvalidValue;
     if (compact && excl != nullptr) return hipErrorInvalidValue;   // an excluding selection never compacts
@@ -415,16 +428,21 @@ hipError_t launch_select_packed(const Plan &p, const int32_t *units, unsigned lo
     {
         StageScope _stage(st, "select");
         const size_t lds = (size_t)p.n_src_max * 4;
-        if (select_small(p, compact))
-            go_sel<true, SEL_SMALL>(cdiv(p.n_src_max, SEL_SMALL), p.n_groups, lds, st, (const float *)nullptr,
+        const long n8 = (wo && wo16 && p.bf16) ? n_wo / 8 : 0;
+        const bool small = select_small(p, compact);
+        const int threads = small ? SEL_SMALL : SEL_LARGE;
+        const int cvt_blocks = n8 > 0 ? (int)std::min<long>((n8 + threads - 1) / threads, 2 * N_CUS) : 0;
+        const unsigned grid = p.n_groups + cvt_blocks;
+        if (small)
+            go_sel<true, SEL_SMALL>(cdiv(p.n_src_max, SEL_SMALL), grid, lds, st, (const float *)nullptr,
                                     (const int32_t *)nullptr, node_pack, inv, node_max, node_idx, group_map(p, units),
                                     p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok, kept_idx, cached_idx, rmap, p.N,
-                                    L, tF, excl, clear_pack);
+                                    L, tF, excl, clear_pack, (const uint4 *)wo, n8, (uint4 *)wo16);
         else
-            go_sel<true, SEL_LARGE>(cdiv(p.n_src_max, SEL_LARGE), p.n_groups, lds, st, (const float *)nullptr,
+            go_sel<true, SEL_LARGE>(cdiv(p.n_src_max, SEL_LARGE), grid, lds, st, (const float *)nullptr,
                                     (const int32_t *)nullptr, node_pack, inv, node_max, node_idx, group_map(p, units),
                                     p.n_groups, p.n_src_max, p.n_dst_max, flag, mtok, kept_idx, cached_idx, rmap, p.N,
-                                    L, tF, excl, clear_pack);
+                                    L, tF, excl, clear_pack, (const uint4 *)wo, n8, (uint4 *)wo16);
     }
     return hipGetLastError();
 }

@@ -346,9 +346,16 @@ oc_status run_match(const Plan &p, const Layout &L, const void *x, float *node_m
 // Selection and compaction.  from_pack: unpack the similarity arg-max in
 // the selection kernel (writing node_max / node_idx too), and compact there
 // as well when every frame is one group.
+// Whether a layer call's selection launch converts wo (the packed selection
+// runs on one CU per group, the rest of the chip is idle); otherwise the
+// first launch of the match stage does.
+bool select_converts_wo(const Plan &p) {
+    return p.bf16 && p.kind != KIND_FRAME && !(p.gran == OC_GRAN_FRAME_TOKEN && gram_norms(p));
+}
+
 oc_status run_select(const Plan &p, const Layout &L, float *node_max, int32_t *node_idx, bool from_pack,
                      int32_t *kept, int32_t *cached, int32_t *rmap, int map_matched, void *ws, hipStream_t st,
-                     const void *x = nullptr) {
+                     const void *x = nullptr, const void *wo = nullptr, void *wo16 = nullptr) {
     const int32_t *units = units_of(p, L, ws);
     if (from_pack && p.kind != KIND_FRAME) {
         const bool fused = select_compacts(p);
@@ -359,7 +366,8 @@ oc_status run_select(const Plan &p, const Layout &L, float *node_max, int32_t *n
         HIP_TRY(launch_select_packed(p, units, at<unsigned long long>(ws, L.node_pack), at<float>(ws, L.inv),
                                      node_max, node_idx, flags ? at<int32_t>(ws, L.flag) : nullptr,
                                      flags ? at<int32_t>(ws, L.mtok) : nullptr, fused ? kept : nullptr,
-                                     fused ? cached : nullptr, fused ? rmap : nullptr, st, nullptr, p.k2 > 0 ? 1 : 0),
+                                     fused ? cached : nullptr, fused ? rmap : nullptr, st, nullptr, p.k2 > 0 ? 1 : 0,
+                                     wo, wo16, (long)p.C * p.hd),
                 "select");
         if (fused) {
             if (map_matched)
@@ -603,13 +611,17 @@ oc_status oc_layer_cached(const oc_shape *shape, const oc_cfg *cfg, const void *
     float *nm = at<float>(ws, L.node_max);
     int32_t *ni = at<int32_t>(ws, L.node_idx);
     const AttnWs aw = attn_ws(p, p.n_seq, p.seq_len, L.attn);
-    // bf16 layers: the fp16 copy of wo is made by the first launch of the match stage
+    // bf16 layers: the fp16 copy of wo is made beside the selection, or by
+    // the first launch of the match stage
     const bool wo_early = p.bf16;
-    if ((s = run_match(p, L, x, nm, ni, false, ws, stream, wo_early ? w->wo : nullptr,
-                       wo_early ? at<char>(ws, aw.wo16) : nullptr, true)) != OC_OK)
+    const bool wo_sel = select_converts_wo(p);
+    if ((s = run_match(p, L, x, nm, ni, false, ws, stream, wo_early && !wo_sel ? w->wo : nullptr,
+                       wo_early && !wo_sel ? at<char>(ws, aw.wo16) : nullptr, true)) != OC_OK)
         return s;
     int32_t *kept = at<int32_t>(ws, L.kept), *cached = at<int32_t>(ws, L.cached), *rmap = at<int32_t>(ws, L.rmap);
-    if ((s = run_select(p, L, nm, ni, true, kept, cached, rmap, map_matched, ws, stream, x)) != OC_OK) return s;
+    if ((s = run_select(p, L, nm, ni, true, kept, cached, rmap, map_matched, ws, stream, x, wo_sel ? w->wo : nullptr,
+                        wo_sel ? at<char>(ws, aw.wo16) : nullptr)) != OC_OK)
+        return s;
 
     AttnArgs a;
     std::memset(&a, 0, sizeof(a));

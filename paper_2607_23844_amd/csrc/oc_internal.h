@@ -147,10 +147,13 @@ hipError_t launch_select(const Plan &p, const int32_t *units, const float *node_
 // candidates of this selection and their flag / mtok entries stay as they
 // are (the second level of the hierarchy after the first).  clear_pack:
 // leave the packed arg-max zeroed (a second level's similarity follows).
+// wo / wo16 given (bf16): extra blocks of the same launch convert the
+// output-projection weights (n_wo elements) to fp16 beside the selection.
 hipError_t launch_select_packed(const Plan &p, const int32_t *units, unsigned long long *node_pack,
                                 const float *inv, float *node_max, int32_t *node_idx, int32_t *flag, int32_t *mtok,
                                 int32_t *kept_idx, int32_t *cached_idx, int32_t *rmap, hipStream_t st,
-                                const int32_t *excl = nullptr, int clear_pack = 0);
+                                const int32_t *excl = nullptr, int clear_pack = 0, const void *wo = nullptr,
+                                void *wo16 = nullptr, long n_wo = 0);
 // whether launch_select_packed can compact in the same launch (the frame's
 // flags are staged in LDS: N below SEL_COMPACT_MAX_N)
 constexpr int SEL_COMPACT_MAX_N = 24576;
