@@ -270,6 +270,9 @@ def run_other_configs(args):
         cfg = oc.Cfg(wl.gran, r=wl.r, r_frame=wl.r_frame, patch_k=wl.patch_k)
         full = FullRunner(shape, oc.Cfg(wl.gran, 0.0, 0.0, 1), W, dev)
         full_ms = timed_ms(full, xs, K, Wm)
+        # the uncached layer's stages, live time per call (µs)
+        ust = stage_times(full, xs, K)
+        uncached_stages = {st: round(t * 1e3 / K, 3) for st, (t, n) in ust.items()}
         run = LayerRunner(shape, cfg, W, dev)
         run(xs[0])
         ms = timed_ms(run, xs[1:], K, Wm)
@@ -281,7 +284,8 @@ def run_other_configs(args):
                           f"r={wl.r} r_frame={wl.r_frame} patch_k={wl.patch_k}",
                  cached_us=round(ms * 1e3, 2), uncached_us=round(full_ms * 1e3, 2),
                  speedup_vs_uncached=round(full_ms / ms, 4), tokens_per_s=round(tokens / (ms * 1e-3), 1),
-                 retained_tokens=pl.n_kept, sequences=f"{pl.n_seq}x{pl.seq_len}", roofline=roof, kernels=kernels)
+                 retained_tokens=pl.n_kept, sequences=f"{pl.n_seq}x{pl.seq_len}", roofline=roof, kernels=kernels,
+                 uncached_stages_us=uncached_stages)
         if wl.t_weights is not None:
             TW = {k: _bf16_dev(v, dev) for k, v in wl.t_weights.items()}
             temporal = FullRunner(shape, oc.Cfg("block", 0.0, 0.0, 1), TW, dev)
@@ -552,8 +556,10 @@ def run_data_movement_svdxt(args):
 
 def run_data_movement(args, shape, cfg, W, xs, ctx):
     """The standalone gather and (in-place) restore entry points: kernel time
-    and HBM GB/s (2 n_kept C bytes-per-element moved) with warm caches and
-    after a 512 MiB write that flushes L2 and MALL."""
+    and HBM GB/s (2 n_kept C bytes-per-element moved) with warm caches, after
+    a 512 MiB write that flushes L2 and MALL ("flushed": the dirty lines it
+    leaves are written back during the measured kernel), and after a 512 MiB
+    read ("flushed_read": the caches hold clean, unrelated lines)."""
     import torch
     import paper_2607_23844_amd as oc
 
@@ -568,11 +574,13 @@ def run_data_movement(args, shape, cfg, W, xs, ctx):
     res = {}
     for name, fn in (("gather", lambda: oc.gather(xs[1], kept, shape, cfg)),
                      ("restore", lambda: oc.restore(y_kept, rmap, shape, cache_y=y_out, y=y_out))):
-        for mode in ("warm", "flushed"):
+        for mode in ("warm", "flushed", "flushed_read"):
             timer = oc.StageTimer()
             for i in range(args.cfg_steps + 3):
                 if mode == "flushed":
                     flush.zero_()
+                elif mode == "flushed_read":
+                    flush_sum = flush.view(torch.int32).sum()   # noqa: F841 (reads every line)
                 if i == 3:
                     timer.reset()
                 with timer:
