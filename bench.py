@@ -598,7 +598,8 @@ def run_data_movement(args, shape, cfg, W, xs, ctx):
 def achievable_peaks():
     """What vendor code reaches on this machine, beside the spec peaks the
     roofline uses: a bf16 GEMM of 8192 x 8192 x 8192 through torch.matmul
-    (hipBLASLt) and a 1 GiB device-to-device copy (read + write bytes)."""
+    (hipBLASLt), the same GEMM at the SD3-like layer's shapes, and a 1 GiB
+    device-to-device copy (read + write bytes)."""
     import torch
     dev = torch.device("cuda:0")
 
@@ -624,12 +625,25 @@ def achievable_peaks():
     dst = torch.empty_like(src)
     t_cp = best(lambda: dst.copy_(src))
     del src, dst
+    # the same vendor GEMM at the SD3-like layer's own shapes (r = 0.5:
+    # 2381 attention rows; the similarity at k = 1 without its arg-max)
+    same_shape = {}
+    for name, (m, nn, k) in (("similarity_3072x1024x1536", (3072, 1024, 1536)),
+                             ("qk_projection_2381x3072x1536", (2381, 3072, 1536)),
+                             ("v_or_out_projection_2381x1536x1536", (2381, 1536, 1536))):
+        a = torch.randn((m, k), device=dev).to(torch.bfloat16)
+        b = torch.randn((nn, k), device=dev).to(torch.bfloat16)
+        c = torch.empty((m, nn), device=dev, dtype=torch.bfloat16)
+        t = best(lambda: torch.matmul(a, b.t(), out=c), reps=50)
+        same_shape[name] = dict(us=round(t * 1e6, 2), tflops=round(2.0 * m * nn * k / t / 1e12, 1))
+        del a, b, c
     torch.cuda.empty_cache()
     mm = 2.0 * n ** 3 / t_mm / 1e12
     cp = 2.0 * (1 << 30) / t_cp / 1e9
     return dict(mfma_bf16_tflops=round(mm, 1), mfma_frac_of_spec=round(mm / PEAK_MFMA_TFLOPS, 4),
                 mfma_source="torch.matmul bf16 8192^3 (hipBLASLt)", hbm_gbs=round(cp, 1),
-                hbm_frac_of_spec=round(cp / PEAK_HBM_GBS, 4), hbm_source="torch copy_ of 1 GiB (read + write)")
+                hbm_frac_of_spec=round(cp / PEAK_HBM_GBS, 4), hbm_source="torch copy_ of 1 GiB (read + write)",
+                vendor_gemm_at_layer_shapes=same_shape)
 
 
 def run_gpu(args):
