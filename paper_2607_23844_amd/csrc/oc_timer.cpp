@@ -48,7 +48,11 @@ bool timed_launch_events(hipStream_t, hipEvent_t *start, hipEvent_t *stop) {
     if (!t || t->failed || g_stage < 0) return false;
     if (t->used == t->recs.size()) {
         oc_timer::Rec r{0, nullptr, nullptr};
-        if (hipEventCreate(&r.a) != hipSuccess || hipEventCreate(&r.b) != hipSuccess) {
+        // timing-only events: no system-scope fence when they are stamped
+        // (that fence writes back and invalidates the caches, which would
+        // lengthen the measured kernel and slow the next one)
+        if (hipEventCreateWithFlags(&r.a, hipEventDisableSystemFence) != hipSuccess ||
+            hipEventCreateWithFlags(&r.b, hipEventDisableSystemFence) != hipSuccess) {
             t->failed = true;
             return false;
         }
