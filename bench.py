@@ -692,6 +692,10 @@ def run_gpu(args):
         by_r[str(r)] = dict(ms=ms, tokens_per_s=tokens / (ms * 1e-3), speedup_vs_uncached=full_ms / ms)
         if r == args.r:
             primary = (cfg, run, ms, wall)
+        else:
+            # the other ratios' stages, live time per step (µs)
+            rs = stage_times(run, xs[1:4], K)
+            by_r[str(r)]["stages_us"] = {st: round(t * 1e3 / K, 2) for st, (t, n) in rs.items()}
     cfg, run, ms, wall = primary
     pct = step_percentiles(run, xs[1:], K)
     graph_us = graph_latency(run, xs[1], K)
@@ -869,7 +873,8 @@ def main():
         "graph_vs_eager_interleaved_us": g["graph_us"],
         "uncached_latency_us": round(g["full_ms"] * 1e3, 2),
         "speedup_vs_uncached": round(g["full_ms"] / ms, 4),
-        "by_r": {k: {kk: round(vv, 4) for kk, vv in v.items()} for k, v in g["by_r"].items()},
+        "by_r": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}
+                 for k, v in g["by_r"].items()},
         "roofline": g["roofline"],
         "kernels": g["kernels"],
         "data_movement": g["moves"],
