@@ -61,6 +61,18 @@ readings (the same list, with reasons, is kept with the design notes):
       previous step's FFN output at the same position, or, on a step with
       no valid cache under the "matched" policy, the fresh output of the
       position their best match occupies (the attention call's restore map).
+  R23 The hierarchy of §3.3 as a second level for Token and Block Cache:
+      coarse_k (dividing patch_k, smaller) and its own ratio r_coarse; its
+      groups are the coarse_k x coarse_k patches, their candidates the
+      candidates the first level left, their representatives the same
+      top-left items; each caches min(floor(r_coarse items), remaining) by
+      the usual rule, and a token cached at either level is restored from
+      its match at that level.
+  (R22, the Layered Cache proposal of Alg. 1, lives in oracle/layered.py.)
+
+Parity unpinned: the frame-pair budget (R12) and the greedy pairing (R14)
+have no example in the paper; they are checked by invariants and by an
+independent restatement of the greedy (oracle/brute.py) only.
 
 Group order (used to lay out per-candidate results):
   token        : frame-major, then k x k patches row-major
