@@ -25,16 +25,23 @@
 // K and Vt tiles go through a ring of LDS buffers with one barrier per tile;
 // the K fragments of tile kt+1 are read into registers while tile kt
 // finishes.  Two ways to fill the ring:
-//   DMA (head_dim a multiple of 64, long sequences): global_load_lds moves
-//     16 bytes per lane straight into LDS, three tiles ahead, into a ring of
-//     four unpadded buffers whose 16-byte chunks are XOR-swizzled by row
-//     (chunk c of row r at slot c ^ ((r >> sh) & 7), sh = 1 for 128-byte
-//     rows, two of which fill the 64 LDS banks, 0 for 256-byte rows), so the
-//     fragment reads of 16 consecutive rows hit distinct banks.  Key rows past the end are
-//     clamped to the last key (their scores are masked) and the V projection
-//     zeroes the padded key positions of Vt, so nothing needs masking in LDS;
-//   registers (other head dims, short sequences): global loads one tile
-//     ahead, masked, written to a ring of three padded buffers.
+//   DMA (long sequences): global_load_lds moves 16 bytes per lane straight
+//     into LDS, three tiles ahead, into a ring of four buffers.  Rows of 64
+//     or 128 features (K of a head dim that is a multiple of 64, and every
+//     Vt row of 64 keys) are unpadded with their 16-byte chunks XOR-swizzled
+//     by row (chunk c of row r at slot c ^ ((r >> sh) & 7), sh = 1 for
+//     128-byte rows, two of which fill the 64 LDS banks, 0 for 256-byte
+//     rows); K rows of other head dims (72, 80, 96, ...) are padded to an odd
+//     number of 16-byte chunks, whose feature padding the DMA fills with
+//     zeros.  Either way the fragment reads of 16 consecutive rows hit
+//     distinct banks.  Key rows past the end read as zeros (their scores
+//     are masked) and the V projection zeroes the padded key
+//     positions of Vt, so nothing needs masking in LDS; the Vt rows past the
+//     head dim are never loaded and only feed output rows that are not
+//     stored;
+//   registers (short sequences, large grids of padded head dims): global
+//     loads one tile ahead, masked, written to a ring of three padded
+//     buffers.
 // Only the last tile's scores are masked.  Blocks of one head are kept on one
 // XCD (xcd_remap) so its K/V stay in that XCD's L2.
 #include "oc_attn_common.h"
@@ -47,7 +54,7 @@ typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 constexpr float REBASE = 8.f;   // P = exp2(s - m) stays below 2^REBASE on the fast path
 
-template <int DH, bool DMA>
+template <int DH, bool DMA, int NW = 4>
 struct FlashCfg {
     static constexpr int DK = (DH + 15) / 16 * 16;   // S^T k-loop (16 per MFMA)
     static constexpr int NKS = DK / 16;
@@ -55,21 +62,33 @@ struct FlashCfg {
     static constexpr int NDB = DV / 32;
     static constexpr int KT = 64;                    // keys per tile
     static constexpr int NBUF = DMA ? 4 : 3;
-    // LDS rows (halves): unpadded and swizzled for DMA, padded by 16 bytes otherwise
-    static constexpr int LDK = DMA ? DK : DK + 8, LDV = DMA ? KT : KT + 8;
+    // K rows: unpadded and swizzled for DMA of a head dim that is a multiple
+    // of 64, else padded by 16 bytes (an odd number of 16-byte chunks per
+    // row, so 16 consecutive rows start in distinct bank groups).  V rows
+    // (64 keys): swizzled for DMA, padded otherwise.
+    static constexpr bool KSW = DMA && DK % 64 == 0;
+    static constexpr int LDK = KSW ? DK : DK + 8, LDV = DMA ? KT : KT + 8;
     static constexpr int KBUF = KT * LDK, VBUF = DV * LDV;
-    static constexpr size_t LDS_BYTES = (size_t)NBUF * (KBUF + VBUF) * 2;
-    static_assert(!DMA || (DK == DH && DV == DH && DH % 64 == 0), "DMA staging needs head_dim % 64 == 0");
+    // DMA: 64-lane instructions per tile (K: every slot of the padded rows;
+    // V: the DH real rows), spread over the NW waves; the surplus
+    // instructions of a wave load zeros into a spare 1 KB, so that every
+    // wave issues the same count (its vmcnt waits stay uniform)
+    static constexpr int NIK = KT * (LDK / 8) / 64, NIV = DH * (KT / 8) / 64;
+    static constexpr int IK = (NIK + NW - 1) / NW, IV = (NIV + NW - 1) / NW;
+    static constexpr bool SPARE = DMA && (IK * NW != NIK || IV * NW != NIV);
+    static constexpr size_t LDS_BYTES = (size_t)NBUF * (KBUF + VBUF) * 2 + (SPARE ? 1024 : 0);
+    static_assert(!DMA || (DH % 8 == 0 && (KT * (LDK / 8)) % 64 == 0), "DMA staging needs head_dim % 8 == 0");
 };
 
 // XOR swizzle of the DMA layout: slot of chunk c in row r (rows of LD halves)
 template <int LD>
 __device__ __forceinline__ int dma_slot(int r, int c) { return c ^ ((r >> (LD * 2 >= 256 ? 0 : 1)) & 7); }
 
-// LDS offset (halves) of the 8-element chunk c of row r in a buffer of rows of LD halves
-template <bool DMA, int LD>
+// LDS offset (halves) of the 8-element chunk c of row r in a buffer of rows
+// of LD halves, swizzled (SW) or plain
+template <bool SW, int LD>
 __device__ __forceinline__ int lds_chunk(int r, int c) {
-    return DMA ? r * LD + (dma_slot<LD>(r, c) << 3) : r * LD + (c << 3);
+    return SW ? r * LD + (dma_slot<LD>(r, c) << 3) : r * LD + (c << 3);
 }
 
 template <int DH, int NW, bool DMA, bool VARLEN = false>
@@ -77,8 +96,9 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
                                                     const uint16_t *__restrict__ Vt, uint16_t *__restrict__ O,
                                                     int hd, int heads, int n_seq, int L, int Lk, int lpad,
                                                     int n_qt, const int32_t *__restrict__ seq_off) {
-    using C = FlashCfg<DH, DMA>;
+    using C = FlashCfg<DH, DMA, NW>;
     constexpr int DK = C::DK, NKS = C::NKS, DV = C::DV, NDB = C::NDB, KT = C::KT, LDK = C::LDK, LDV = C::LDV;
+    constexpr bool KSW = C::KSW;
     constexpr int NT = NW * 64, QT = 32 * NW;
     constexpr int KCH = KT * (DK / 8), VCH = DV * (KT / 8);
     constexpr int KPT = (KCH + NT - 1) / NT, VPT = (VCH + NT - 1) / NT;
@@ -120,8 +140,13 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
     // with a fixed per-lane offset and the tile's offset in a scalar: K rows
     // past the end read as zeros (their scores are masked), and no address
     // arithmetic is left per tile.
-    constexpr int IK = DMA ? KCH / NT : 1, IV = DMA ? VCH / NT : 1;
-    static_assert(!DMA || (KCH % NT == 0 && VCH % NT == 0), "DMA tile split");
+    // instruction j of wave w covers the 64 slots of index j*NW + w; a slot
+    // past the tile's (a surplus instruction) or in a K row's padding
+    // (head-dim chunks >= DH/8 and the row's spare chunk) gets an offset past
+    // the end of the buffer by itself, which the hardware reads as zero
+    constexpr int IK = DMA ? C::IK : 1, IV = DMA ? C::IV : 1;
+    constexpr int KCPR = LDK / 8;   // 16-byte slots per K row in LDS
+    constexpr int OOB = 0x40000000;
     const int wv = __builtin_amdgcn_readfirstlane(wave);
     i32x4 krs = {0, 0, 0, 0}, vrs = {0, 0, 0, 0};
     int kvo[IK], vvo[IV];
@@ -130,27 +155,34 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
         vrs = buffer_rsrc(vbase, DH * lpad * 2);
 #pragma unroll
         for (int j = 0; j < IK; ++j) {
-            const int q = (wave * IK + j) * 64 + lane;
-            const int r = q / (DK / 8), c = dma_slot<LDK>(r, q % (DK / 8));
-            kvo[j] = (r * hd + c * 8) * 2;
+            const int q = (j * NW + wave) * 64 + lane;
+            const int r = q / KCPR, slot = q % KCPR, c = KSW ? dma_slot<LDK>(r, slot) : slot;
+            kvo[j] = (j * NW + wave < C::NIK && c < DH / 8) ? (r * hd + c * 8) * 2 : OOB;
         }
 #pragma unroll
         for (int j = 0; j < IV; ++j) {
-            const int q = (wave * IV + j) * 64 + lane;
+            const int q = (j * NW + wave) * 64 + lane;
             const int d = q / (KT / 8), c = dma_slot<LDV>(d, q % (KT / 8));
-            vvo[j] = (d * lpad + c * 8) * 2;
+            vvo[j] = j * NW + wave < C::NIV ? (d * lpad + c * 8) * 2 : OOB;
         }
     }
+    uint16_t *const spare = lds + C::NBUF * (C::KBUF + C::VBUF);
     auto issue = [&](int kt) {
         const int k0 = kt * KT, buf = kt & 3;
         uint16_t *kb = Ks + buf * C::KBUF;
         uint16_t *vb = Vs + buf * C::VBUF;
 #pragma unroll
-        for (int j = 0; j < IK; ++j)
-            buffer_load_lds(krs, (lds_vp)(kb + (wv * IK + j) * 512), 16, kvo[j], k0 * hd * 2, 0, 0);
+        for (int j = 0; j < IK; ++j) {
+            const int ix = j * NW + wv;
+            buffer_load_lds(krs, (lds_vp)(C::SPARE && ix >= C::NIK ? spare : kb + ix * 512), 16, kvo[j],
+                            k0 * hd * 2, 0, 0);
+        }
 #pragma unroll
-        for (int j = 0; j < IV; ++j)
-            buffer_load_lds(vrs, (lds_vp)(vb + (wv * IV + j) * 512), 16, vvo[j], k0 * 2, 0, 0);
+        for (int j = 0; j < IV; ++j) {
+            const int ix = j * NW + wv;
+            buffer_load_lds(vrs, (lds_vp)(C::SPARE && ix >= C::NIV ? spare : vb + ix * 512), 16, vvo[j], k0 * 2,
+                            0, 0);
+        }
     };
 
     // this thread's staging chunks (fixed across tiles)
@@ -224,14 +256,19 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
         for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
             for (int kb2 = 0; kb2 < 2; ++kb2)
-                kf[kb2][ks] = *reinterpret_cast<const f16x8 *>(kb + lds_chunk<DMA, LDK>(kb2 * 32 + ln, ks * 2 + lg));
+                kf[kb2][ks] = *reinterpret_cast<const f16x8 *>(kb + lds_chunk<KSW, LDK>(kb2 * 32 + ln, ks * 2 + lg));
     };
 
     // output accumulator o (MFMA) and the part saved at the last rebase osv;
     // the attention output is (osv + o) / l
-    f32x16 o[NDB], osv[NDB];
+    // wide heads (three or more row blocks of O) rescale o in place instead:
+    // the saved sum would cost 16 registers per row block
+    constexpr bool SAVE = NDB <= 2;
+    f32x16 o[NDB], osv[SAVE ? NDB : 1];
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) o[db] = osv[db] = f32x16{};
+    for (int db = 0; db < NDB; ++db) o[db] = f32x16{};
+#pragma unroll
+    for (int db = 0; db < (SAVE ? NDB : 1); ++db) osv[db] = f32x16{};
     float m = 0.f, l0 = 0.f, l1 = 0.f;
     // -m in every slot: the first S MFMA of a tile adds it (changes only on the slow path)
     f32x16 negm = f32x16{};
@@ -279,15 +316,16 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
 #pragma unroll
             for (int kb2 = 0; kb2 < 2; ++kb2)
                 sc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf[kb2][ks], qf[ks], sc[kb2], 0, 0, 0);
-        // V fragments of this tile
-        f16x8 vf[NDB][4];
-        {
-            const uint16_t *vb = Vs + b0 * C::VBUF;
+        // V fragments of this tile (wide heads: read per key block just before use)
+        constexpr int VK = SAVE ? 4 : 1;
+        f16x8 vf[NDB][VK];
+        const uint16_t *vbt = Vs + b0 * C::VBUF;
+        if constexpr (SAVE) {
 #pragma unroll
             for (int k4 = 0; k4 < 4; ++k4)
 #pragma unroll
                 for (int db = 0; db < NDB; ++db)
-                    vf[db][k4] = *reinterpret_cast<const f16x8 *>(vb + lds_chunk<DMA, LDV>(db * 32 + ln, k4 * 2 + lg));
+                    vf[db][k4] = *reinterpret_cast<const f16x8 *>(vbt + lds_chunk<DMA, LDV>(db * 32 + ln, k4 * 2 + lg));
         }
         // registers: tile kt+2 into the free buffer, then the global loads of tile kt+3
         if (!DMA && kt + 2 < n_kt) {
@@ -339,12 +377,20 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
             l1 *= alpha;
             // fold the MFMA accumulator into the rescaled saved sum and
             // restart it at zero: O itself is never scaled element-wise,
-            // which keeps it in the same registers on both paths
+            // which keeps it in the same registers on both paths (wide
+            // heads scale O in place)
+            if constexpr (SAVE) {
 #pragma unroll
-            for (int db = 0; db < NDB; ++db) {
+                for (int db = 0; db < NDB; ++db) {
 #pragma unroll
-                for (int i = 0; i < 16; ++i) osv[db][i] = (osv[db][i] + o[db][i]) * alpha;
-                o[db] = f32x16{};
+                    for (int i = 0; i < 16; ++i) osv[db][i] = (osv[db][i] + o[db][i]) * alpha;
+                    o[db] = f32x16{};
+                }
+            } else {
+#pragma unroll
+                for (int db = 0; db < NDB; ++db)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
             }
 #pragma unroll
             for (int kb2 = 0; kb2 < 2; ++kb2)
@@ -366,10 +412,16 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
         // K fragments of the next tile (its buffer was filled before the last barrier)
         if (kt + 1 < n_kt) read_k(b1);
 #pragma unroll
-        for (int k4 = 0; k4 < 4; ++k4)
+        for (int k4 = 0; k4 < 4; ++k4) {
+            if constexpr (!SAVE) {
+#pragma unroll
+                for (int db = 0; db < NDB; ++db)
+                    vf[db][0] = *reinterpret_cast<const f16x8 *>(vbt + lds_chunk<DMA, LDV>(db * 32 + ln, k4 * 2 + lg));
+            }
 #pragma unroll
             for (int db = 0; db < NDB; ++db)
-                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[db][k4], pf[k4], o[db], 0, 0, 0);
+                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[db][SAVE ? k4 : 0], pf[k4], o[db], 0, 0, 0);
+        }
         // DMA: this wave's part of tile kt+2 must have landed before the
         // barrier that publishes it (only tile kt+3 may still be in flight)
         if constexpr (DMA) {
@@ -401,7 +453,7 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
             if (d >= DH) continue;
             u16x4 v;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = f2h_bits((osv[db][4 * g4 + e] + o[db][4 * g4 + e]) * inv);
+            for (int e = 0; e < 4; ++e) v[e] = f2h_bits(((SAVE ? osv[SAVE ? db : 0][4 * g4 + e] : 0.f) + o[db][4 * g4 + e]) * inv);
             *reinterpret_cast<u16x4 *>(orow + d) = v;
         }
 }
@@ -538,7 +590,7 @@ template <int DH, int NW, bool DMA, bool VARLEN = false>
 static hipError_t go(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st) {
     const int n_qt = cdiv(Lk, 32 * NW);
     const int total = n_qt * p.heads * a.n_seq;
-    const size_t lds = FlashCfg<DH, DMA>::LDS_BYTES;
+    const size_t lds = FlashCfg<DH, DMA, NW>::LDS_BYTES;
     const hipError_t e = raise_lds_limit((const void *)k_flash<DH, NW, DMA, VARLEN>, lds);
     if (e != hipSuccess) return e;
     launch_k(k_flash<DH, NW, DMA, VARLEN>, total, NW * 64, lds, st, (const uint16_t *)a.q, (const uint16_t *)a.k,
@@ -556,14 +608,17 @@ static hipError_t go_dh(const Plan &p, const AttnArgs &a, int Lk, hipStream_t st
     // every sequence's end itself (Lk is the longest)
     if (a.seq_off != nullptr) return go<DH, 4, false, true>(p, a, Lk, st);
     if (attn_short(Lk)) return Lk <= 32 ? go_short<DH, 1>(p, a, Lk, st) : go_short<DH, 2>(p, a, Lk, st);
-    if constexpr (DH % 64 == 0) {
-        if (flash_uses_dma(DH, Lk, p.hd)) {
-            // a grid of four-wave blocks that would not fill two per CU:
-            // eight-wave blocks (256 queries share each K/V tile)
-            const long blocks4 = (long)cdiv(Lk, 128) * p.heads * a.n_seq;
-            if (blocks4 <= 2L * N_CUS) return go<DH, 8, true>(p, a, Lk, st);
-            return go<DH, 4, true>(p, a, Lk, st);
-        }
+    // a grid of four-wave blocks that would not fill two per CU: eight-wave
+    // blocks (256 queries share each K/V tile)
+    const bool eight = (long)cdiv(Lk, 128) * p.heads * a.n_seq <= 2L * N_CUS;
+    if (flash_uses_dma(DH, Lk, p.hd)) {
+        if (eight) return go<DH, 8, true>(p, a, Lk, st);
+        // padded head dims: the four-buffer ring with padded K rows would
+        // leave one four-wave block per CU
+        if constexpr (DH % 64 == 0) return go<DH, 4, true>(p, a, Lk, st);
+    }
+    if constexpr (DH <= 96) {
+        if (eight) return go<DH, 8, false>(p, a, Lk, st);
     }
     return go<DH, 4, false>(p, a, Lk, st);
 }

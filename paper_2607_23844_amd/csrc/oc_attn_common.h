@@ -68,12 +68,13 @@ __device__ __forceinline__ int xcd_remap(int id, int total) {
 // inverse).  The attention kernel's PV operand is then one 16-byte read.
 __device__ __forceinline__ int vt_key_of_pos(int p) { return (p & ~12) | ((p & 4) << 1) | ((p & 8) >> 1); }
 
-// Whether the attention kernel stages K/V by DMA for this head dim and key
-// count.  The DMA path relies on the V projection having zeroed the padded
-// key positions [Lk, lpad) of every Vt row.
+// Whether the attention kernel may stage K/V by DMA for this head dim and
+// key count (head dims that are not a multiple of 64 take it only for grids
+// of eight-wave blocks).  The DMA path relies on the V projection having
+// zeroed the padded key positions [Lk, lpad) of every Vt row.
 // (buffer offsets of K are 32-bit: Lk * hd * 2 bytes must stay below 2^31)
 inline bool flash_uses_dma(int dh, int Lk, int hd) {
-    return dh % 64 == 0 && dh <= 128 && Lk >= 256 && (long)Lk * hd * 2 < (1L << 31);
+    return dh % 8 == 0 && dh <= 128 && Lk >= 256 && (long)Lk * hd * 2 < (1L << 31);
 }
 
 // Whether the attention runs the register-only kernel for short sequences

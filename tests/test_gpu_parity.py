@@ -159,6 +159,8 @@ def test_heavy_tailed_activations_chain(gran, head_dim, F, scale):
     # the other supported head dims, long and short sequences
     ("bf16", 32, 2, 1000, 0), ("bf16", 48, 3, 100, 0), ("bf16", 80, 2, 150, 0), ("bf16", 96, 2, 300, 0),
     ("bf16", 128, 3, 40, 0), ("bf16", 96, 1, 70, 3),
+    # K/V staged by DMA into padded K rows (head dims not a multiple of 64), ragged last tiles
+    ("bf16", 48, 2, 333, 0), ("bf16", 80, 1, 700, 0), ("bf16", 16, 2, 260, 0), ("bf16", 72, 1, 456, 4),
 ])
 def test_attn_reduced_vs_oracle(dtype, dh, n_seq, L, n_ctx):
     _say(f"attn_reduced {dtype} dh={dh} n_seq={n_seq} L={L} n_ctx={n_ctx}")
