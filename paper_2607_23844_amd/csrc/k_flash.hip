@@ -297,7 +297,10 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
         OC_WAIT_VMCNT(0);
     }
     if constexpr (DMA) barrier_lds(); else __syncthreads();
-    read_k(0);
+    // K fragments one tile ahead, except for the widest heads, which read
+    // them at the top of each tile (the prefetch would cost a wave per SIMD)
+    constexpr bool KPRE = NKS <= 6;
+    if constexpr (KPRE) read_k(0);
 
     const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
     const _Float16 big = (_Float16)(float)(1 << (int)REBASE);
@@ -307,6 +310,7 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
         const int k0 = kt * KT;
         // DMA: tile kt+3 into the buffer that tile kt-1 left (free since the last barrier)
         if (DMA && kt + 3 < n_kt) issue(kt + 3);
+        if constexpr (!KPRE) read_k(b0);
         // S^T - m
         f32x16 sc[2];
 #pragma unroll
@@ -410,7 +414,7 @@ __global__ __launch_bounds__(NW * 64) void k_flash(const uint16_t *__restrict__ 
             l1 = __builtin_amdgcn_fdot2(pf[j].s67, ones, l1, false);
         }
         // K fragments of the next tile (its buffer was filled before the last barrier)
-        if (kt + 1 < n_kt) read_k(b1);
+        if (KPRE && kt + 1 < n_kt) read_k(b1);
 #pragma unroll
         for (int k4 = 0; k4 < 4; ++k4) {
             if constexpr (!SAVE) {
