@@ -18,6 +18,7 @@ import argparse
 import json
 import os
 import platform
+import statistics
 import sys
 import time
 
@@ -591,6 +592,36 @@ def run_data_movement(args, shape, cfg, W, xs, ctx):
             us = tot * 1e3 / max(n, 1)
             res[f"{name}_{mode}"] = dict(avg_us=round(us, 3), gbs=round(nbytes / (us * 1e-6) / 1e9, 1),
                                          frac_hbm=round(nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4))
+    # the same moves by torch's own kernels (index_select: a gather of the
+    # rows; index_copy_: the row scatter a kept-list restore would do), each
+    # call and the library's entry points alike timed by events around it,
+    # median of 10; a short spin kernel queued first keeps the GPU busy while
+    # the host queues the events and the call, so the host's launch time
+    # stays out of the interval
+    keptl = kept.long()
+    x2, y2 = xs[1].view(-1, shape.C), y_out.view(-1, shape.C)
+    vendor = {}
+    for name, fn in (("oc_gather", lambda: oc.gather(xs[1], kept, shape, cfg)),
+                     ("torch_index_select", lambda: torch.index_select(x2, 0, keptl)),
+                     ("oc_restore", lambda: oc.restore(y_kept, rmap, shape, cache_y=y_out, y=y_out)),
+                     ("torch_index_copy", lambda: y2.index_copy_(0, keptl, y_kept))):
+        for mode in ("warm", "flushed", "flushed_read"):
+            ts = []
+            for i in range(13):
+                if mode == "flushed":
+                    flush.zero_()
+                elif mode == "flushed_read":
+                    flush_sum = flush.view(torch.int32).sum()   # noqa: F841
+                torch.cuda._sleep(100000)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                fn()
+                e1.record()
+                torch.cuda.synchronize()
+                if i >= 3:
+                    ts.append(e0.elapsed_time(e1) * 1e3)
+            vendor[f"{name}_{mode}_us"] = round(statistics.median(ts), 1)
+    res["event_timed_vs_torch"] = vendor
     res["bytes_per_call"] = nbytes
     return res
 
