@@ -661,6 +661,7 @@ def achievable_peaks():
     same_shape = {}
     for name, (m, nn, k) in (("similarity_3072x1024x1536", (3072, 1024, 1536)),
                              ("qk_projection_2381x3072x1536", (2381, 3072, 1536)),
+                             ("qkv_projection_2381x4608x1536", (2381, 4608, 1536)),
                              ("v_or_out_projection_2381x1536x1536", (2381, 1536, 1536))):
         a = torch.randn((m, k), device=dev).to(torch.bfloat16)
         b = torch.randn((nn, k), device=dev).to(torch.bfloat16)
