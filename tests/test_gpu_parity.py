@@ -161,6 +161,9 @@ def test_heavy_tailed_activations_chain(gran, head_dim, F, scale):
     ("bf16", 128, 3, 40, 0), ("bf16", 96, 1, 70, 3),
     # K/V staged by DMA into padded K rows (head dims not a multiple of 64), ragged last tiles
     ("bf16", 48, 2, 333, 0), ("bf16", 80, 1, 700, 0), ("bf16", 16, 2, 260, 0), ("bf16", 72, 1, 456, 4),
+    # grids too large for eight-wave blocks: four-wave register staging for wide heads (O scaled in place,
+    # V fragments per key block) and four-wave DMA for head dim 128 (K fragments read per tile)
+    ("bf16", 72, 90, 200, 0), ("bf16", 96, 90, 130, 0), ("bf16", 128, 86, 256, 0),
 ])
 def test_attn_reduced_vs_oracle(dtype, dh, n_seq, L, n_ctx):
     _say(f"attn_reduced {dtype} dh={dh} n_seq={n_seq} L={L} n_ctx={n_ctx}")
