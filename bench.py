@@ -731,6 +731,7 @@ def run_gpu(args):
     cfg, run, ms, wall = primary
     pct = step_percentiles(run, xs[1:], K)
     graph_us = graph_latency(run, xs[1], K)
+    clock = sampled_clock(run, xs[1:])
     moves = run_data_movement(args, shape, cfg, W, xs, ctx)
     # (the per-kernel loop below is the last use of these kernels at this
     # shape, so a profiler trace can pick out exactly its launches)
@@ -743,7 +744,33 @@ def run_gpu(args):
     peaks = achievable_peaks()
     return dict(ms=ms, wall=wall, tokens=tokens, full_ms=full_ms, by_r=by_r, kernels=kernels, roofline=roof,
                 plan=dict(n_kept=pl.n_kept, n_cached=pl.n_cached, seq_len=pl.seq_len), pct=pct, graph_us=graph_us,
-                moves=moves, peaks=peaks)
+                moves=moves, peaks=peaks, clock=clock)
+
+
+def sampled_clock(fn, inputs, n=4000, gap=50):
+    """The shader clock while the step runs: the library's one-wave sampler
+    (oc_clock_sample) on a second stream takes n readings gap / 100 µs
+    apart (2 ms) while 30 steps run on the current stream, after the timed
+    region; the same sampler alone gives the idle clock.  GHz p10 / p50 /
+    p90 over the intervals."""
+    import numpy as np
+    import torch
+    import paper_2607_23844_amd as oc
+    dev = torch.device("cuda:0")
+    buf = torch.zeros(2 * n, dtype=torch.int64, device=dev)
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    oc.clock_sample(buf, n, gap, side)
+    torch.cuda.synchronize()
+    idle = float(np.median(oc.clock_ghz(buf)))
+    oc.clock_sample(buf, n, gap, side)
+    steps = 30                          # about 4.5 ms of steps: past the whole sampling window
+    for i in range(steps):
+        fn(inputs[i % len(inputs)])
+    torch.cuda.synchronize()
+    q = np.percentile(oc.clock_ghz(buf), [10, 50, 90])
+    return dict(idle=round(idle, 3), p10=round(float(q[0]), 3), p50=round(float(q[1]), 3),
+                p90=round(float(q[2]), 3), steps=steps, window_us=n * gap / 100.0)
 
 
 def _cpu_model():
@@ -903,6 +930,7 @@ def main():
         "latency_pct_us": g["pct"],
         "graph_latency_us": g["graph_us"]["graph_us"],
         "graph_vs_eager_interleaved_us": g["graph_us"],
+        "clock_under_load_ghz": g["clock"],
         "uncached_latency_us": round(g["full_ms"] * 1e3, 2),
         "speedup_vs_uncached": round(g["full_ms"] / ms, 4),
         "by_r": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}

@@ -426,6 +426,20 @@ oc_status oc_timer_reset(oc_timer *t);
 int32_t oc_timer_stage_count(const oc_timer *t);
 oc_status oc_timer_stage(const oc_timer *t, int32_t i, const char **name, double *total_ms, int64_t *launches);
 
+/*
+ * oc_clock_sample — shader clock sampler (a measurement aid, not part of the
+ * method).  Enqueues on `stream` a one-wave kernel that writes n pairs
+ * samples[2i] = shader clock count (s_memtime), samples[2i+1] = 100 MHz
+ * real-time count (s_memrealtime), one pair every gap_ticks real-time ticks
+ * (gap_ticks / 100 µs).  samples is a device buffer of 2n int64 owned by the
+ * caller.  Launched on a second stream beside a workload, the ratio of the
+ * differences gives the clock that workload runs at (GHz = d_clock /
+ * (10 d_realtime)).  The kernel occupies one wave slot of one CU and ends
+ * after n samples.  OC_ERR_INVALID_ARG for a null buffer, n <= 0 or gap_ticks
+ * outside [0, 1e8]; OC_ERR_HIP if the launch fails.
+ */
+oc_status oc_clock_sample(int64_t *samples, int32_t n, int32_t gap_ticks, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

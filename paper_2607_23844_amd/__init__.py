@@ -18,6 +18,8 @@ from .api import (  # noqa: F401
     attn_full,
     block_cached,
     block_workspace,
+    clock_ghz,
+    clock_sample,
     attn_reduced,
     attn_workspace_bytes,
     ffn_reduced,

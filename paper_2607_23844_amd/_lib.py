@@ -106,6 +106,7 @@ _SIGS = {
     "oc_timer_reset": (C.c_int, [C.c_void_p]),
     "oc_timer_stage_count": (C.c_int32, [C.c_void_p]),
     "oc_timer_stage": (C.c_int, [C.c_void_p, C.c_int32, P(C.c_char_p), P(C.c_double), P(C.c_int64)]),
+    "oc_clock_sample": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p]),
 }
 
 _lib = None

@@ -439,3 +439,21 @@ class StageTimer:
                 L.lib().oc_timer_destroy(self._t)
         except Exception:
             pass
+
+
+def clock_sample(samples: torch.Tensor, n: int, gap_ticks: int, stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Enqueue the shader clock sampler (oc_clock_sample) on `stream` (the
+    current stream if None): n pairs (shader clock, 100 MHz real-time clock)
+    into the int64 device tensor `samples` of at least 2n elements."""
+    _need(samples, torch.int64, "samples")
+    if samples.numel() < 2 * n:
+        raise ValueError("samples must hold 2n int64 values")
+    st = stream.cuda_stream if stream is not None else _stream(samples)
+    L.check(L.lib().oc_clock_sample(samples.data_ptr(), n, gap_ticks, st))
+
+
+def clock_ghz(samples: torch.Tensor) -> "np.ndarray":
+    """Shader clock in GHz over each interval of a finished clock_sample."""
+    import numpy as np
+    a = samples.view(-1, 2).cpu().numpy().astype(np.float64)
+    return np.diff(a[:, 0]) / (np.diff(a[:, 1]) * 10.0)
